@@ -1,0 +1,169 @@
+/*
+ * sparse_attn.h -- C ABI of the MI355X (gfx950) block-sparse attention library.
+ *
+ * The library computes the sparse branch O_s = A_M(Q, K, V) of compensated
+ * sparse attention (paper §2, Eq. comp-sparse; §4.1): the attention matrix is
+ * cut into contiguous query and key blocks (§2 "Block sparsity"), a selector
+ * M_phi keeps a few key blocks per query block, and exact softmax attention is
+ * evaluated only over the kept blocks (§3 states that the sparse branch of
+ * RoLA, VSA and SLA is exact softmax on a retained block subset).  The paper
+ * leaves the selector open ("top-k selection, blockwise scores, ..."); this
+ * library implements top-k over mean-pooled block scores.
+ *
+ * Conventions shared by every call
+ *  - All tensor pointers are DEVICE pointers; descriptors, strides and sizes
+ *    are host values.  The caller owns every buffer.  The library allocates
+ *    no memory and keeps no pointer after a call returns.
+ *  - Calls are asynchronous on `stream` (a hipStream_t passed as void*; NULL
+ *    is the default stream).  Inputs must stay alive until the stream has run.
+ *  - Return value: SA_OK (0) or a negative sa_status.  Every argument check
+ *    runs on the host before any HIP call, so an invalid call launches
+ *    nothing and leaves all outputs untouched.  SA_ERR_LAUNCH reports a HIP
+ *    launch error (hipGetLastError after the launches).
+ *  - bf16 tensors are indexed [batch][head][token][channel] through the
+ *    element strides in the descriptor; channels are contiguous; every stride
+ *    must be a multiple of 8 elements and every pointer 16-byte aligned.
+ *  - Inputs with NaN or Inf are outside the contract (results undefined).
+ *  - Calls are reentrant; overlapping calls that share a workspace race.
+ */
+#ifndef SPARSE_ATTN_H
+#define SPARSE_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPARSE_ATTN_VERSION 100 /* 1.0.0 */
+
+typedef enum {
+  SA_OK = 0,
+  SA_ERR_INVALID_ARG = -1, /* null pointer, bad size, misaligned pointer or stride */
+  SA_ERR_UNSUPPORTED = -2, /* head_dim != 128, block not in {64, 128}, ... */
+  SA_ERR_WORKSPACE = -3,   /* ws_bytes smaller than sparse_attn_workspace_size() */
+  SA_ERR_LAUNCH = -4,      /* a HIP launch failed */
+  SA_ERR_DEVICE = -5       /* no usable gfx950 device */
+} sa_status;
+
+/* Selection modes of sparse_attn_select. */
+enum {
+  SA_SELECT_ROW_TOPK = 0, /* every query block keeps exactly `budget` key blocks */
+  SA_SELECT_HEAD_TOPK = 1 /* ragged: `budget` (query, key) block pairs per head */
+};
+
+/* Workspace consumers (first argument of sparse_attn_workspace_size). */
+enum { SA_OP_SELECT = 0, SA_OP_FWD = 1, SA_OP_FWD_FP8 = 2 };
+
+/*
+ * Problem descriptor (host struct).
+ *  seqlen      tokens L of the flattened spatiotemporal sequence (>= 1)
+ *  head_dim    d; must be 128
+ *  block       tokens per query block and per key block: 64 (the paper's
+ *              64x64 blocks, appendix "Training Details") or 128
+ *  *_stride    element strides of (batch, head, token) for q, k, v, o
+ *  softmax_scale  tau in softmax(tau * q.k); 0 selects fp32(1/sqrt(head_dim))
+ * Blocks: nqb = nkb = ceil(seqlen / block); the last block holds the
+ * remainder tokens and is a regular candidate.
+ */
+typedef struct {
+  int32_t batch, heads, seqlen, head_dim, block;
+  int64_t q_stride[3];
+  int64_t k_stride[3];
+  int64_t v_stride[3];
+  int64_t o_stride[3];
+  float softmax_scale;
+} sparse_attn_desc;
+
+/* SPARSE_ATTN_VERSION of the built library. */
+int sparse_attn_version(void);
+
+/* Static text for a status code. */
+const char* sparse_attn_status_str(int status);
+
+/* Key blocks kept per query block for a keep ratio in basis points
+ * (1000 = 10%): ceil(keep_bp * nkb / 10000) clamped to [1, nkb]
+ * (sparsity = 1 - k / nkb, paper §2 "Block sparsity").  Returns -1 when
+ * keep_bp < 1 or nkb < 1. */
+int32_t sparse_attn_keep_count(int32_t keep_bp, int32_t nkb);
+
+/* Bytes of device workspace that `op` needs for this problem; `kmax` is the
+ * row stride of the index list (ignored for SA_OP_SELECT).  Returns 0 for an
+ * invalid descriptor. */
+size_t sparse_attn_workspace_size(const sparse_attn_desc* desc, int32_t op, int32_t kmax);
+
+/*
+ * Block selection M_phi (paper §2 Eq. comp-sparse; §4.3 keeps mask
+ * selection in BF16, so it reads the bf16 Q and K).
+ *   score s_ij = (sum_{t in I_i} q_t) . (sum_{u in J_j} k_u) / (n_i n_j),
+ * the mean unscaled logit of block (i, j), pooled and dotted in fp64.
+ *  q, k    bf16 [B][H][L][d] via desc strides (o_stride and v_stride unused)
+ *  mode    SA_SELECT_ROW_TOPK: each query block keeps the `budget` key blocks
+ *          with the largest score under (score desc, block index asc);
+ *          1 <= budget <= nkb <= kmax is required.
+ *          SA_SELECT_HEAD_TOPK: per (batch, head), `budget` block pairs in
+ *          total (nqb <= budget <= nqb * nkb): every query block first keeps
+ *          its best key block, then the remaining pairs go by (score desc,
+ *          query block asc, key block asc); a row keeps at most kmax blocks
+ *          (kmax >= 1), pairs beyond that are dropped.
+ *  idx     int32 [B][H][nqb][kmax] out: kept key-block indices, strictly
+ *          ascending in the first cnt entries, -1 after them
+ *  cnt     int32 [B][H][nqb] out: number of kept blocks per query block
+ *  ws      device workspace of ws_bytes >= sparse_attn_workspace_size(SA_OP_SELECT)
+ */
+int sparse_attn_select(const sparse_attn_desc* desc, const void* q, const void* k,
+                       int32_t mode, int64_t budget, int32_t* idx, int32_t* cnt,
+                       int32_t kmax, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Sparse branch O_s = A_M(Q, K, V) (paper §2 Eq. comp-sparse, §4.1), bf16.
+ * For query block i with key-block list S_i = idx[b][h][i][0 .. cnt-1] and
+ * U_i the tokens of those blocks, every query t of block i gets
+ *   O_t = sum_{u in U_i} softmax_u(tau q_t.k_u) v_u,  LSE_t = log sum_u exp(tau q_t.k_u)
+ * computed exactly (fp32 online softmax, bf16 MFMA products, fp32 accumulation).
+ * List entries outside [0, nkb) are skipped and cnt is clamped to [0, kmax];
+ * a query block with no valid entry gets O = 0 and LSE = -inf.
+ *  q, k, v  bf16 via desc strides;  o  bf16 out via desc->o_stride
+ *  idx/cnt  as written by sparse_attn_select (any ascending or not, duplicates
+ *           are the caller's error: a duplicated block is counted twice)
+ *  lse      fp32 [B][H][L] out, contiguous; may be NULL
+ *  ws       ws_bytes >= sparse_attn_workspace_size(SA_OP_FWD, kmax)
+ */
+int sparse_attn_fwd(const sparse_attn_desc* desc, const void* q, const void* k,
+                    const void* v, const int32_t* idx, const int32_t* cnt, int32_t kmax,
+                    void* o, float* lse, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * FP8 E4M3 (OCP e4m3fn) operand quantisation with one power-of-two scale per
+ * block of desc->block tokens (the paper quantises its linear layers to E4M3,
+ * §4.3; per-block scales for the attention operands are this library's choice).
+ * For every (b, h, block): amax over the block's tokens and all channels,
+ * scale = 2^e with the smallest integer e such that amax <= 448 * 2^e (scale 1
+ * for an all-zero block), x8 = e4m3(x / scale) rounded to nearest even.
+ *  x        bf16 [B][H][L][d] via x_stride (head_dim must be 128)
+ *  x8       uint8 out, contiguous [B][H][L][d]
+ *  scale    fp32 out, contiguous [B][H][nb]
+ */
+int sparse_attn_quant_fp8(const sparse_attn_desc* desc, const void* x, const int64_t x_stride[3],
+                          uint8_t* x8, float* scale, void* stream);
+
+/*
+ * Sparse branch on fp8 operands: the same result as sparse_attn_fwd computed
+ * on the dequantised Q = sq * q8, K = sk * k8, V = sv * v8, with QK^T and PV on
+ * the fp8 matrix cores; the probabilities are rounded to e4m3 for the PV
+ * product.  q8, k8, v8 are contiguous [B][H][L][d] e4m3 and sq, sk, sv are
+ * [B][H][nb] power-of-two scales, both as written by sparse_attn_quant_fp8.
+ * o, lse, idx, cnt, kmax and the workspace are as for sparse_attn_fwd
+ * (ws_bytes >= sparse_attn_workspace_size(SA_OP_FWD_FP8, kmax)).
+ */
+int sparse_attn_fwd_fp8(const sparse_attn_desc* desc, const uint8_t* q8, const float* sq,
+                        const uint8_t* k8, const float* sk, const uint8_t* v8, const float* sv,
+                        const int32_t* idx, const int32_t* cnt, int32_t kmax, void* o,
+                        float* lse, void* ws, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPARSE_ATTN_H */

@@ -86,10 +86,16 @@ def pool_blocks(x: np.ndarray, block: int) -> np.ndarray:
 
 
 def block_scores(q: np.ndarray, k: np.ndarray, block: int) -> np.ndarray:
-    """s_ij = (qhat_i . khat_j) / (n_i n_j): the mean unscaled logit of block (i, j)."""
+    """s_ij = (qhat_i . khat_j) / (n_i n_j): the mean unscaled logit of block (i, j).
+    Every dot product is evaluated with the same reduction order (an
+    elementwise product summed along the channel axis), so blocks with equal
+    pooled vectors get bit-identical scores and exact ties stay ties."""
     nq = block_sizes(q.shape[0], block).astype(np.float64)
     nk = block_sizes(k.shape[0], block).astype(np.float64)
-    dots = pool_blocks(q, block) @ pool_blocks(k, block).T
+    qh, kh = pool_blocks(q, block), pool_blocks(k, block)
+    dots = np.empty((qh.shape[0], kh.shape[0]))
+    for i0 in range(0, qh.shape[0], 32):
+        dots[i0:i0 + 32] = (qh[i0:i0 + 32, None, :] * kh[None, :, :]).sum(axis=-1)
     return dots / (nq[:, None] * nk[None, :])
 
 
@@ -232,12 +238,14 @@ def e4m3_encode(x: np.ndarray) -> np.ndarray:
 
 
 def fp8_scale_exponent(amax: float) -> int:
-    """Smallest integer e with amax <= 448 * 2^e (0 for an all-zero block)."""
+    """Smallest integer e with amax <= 448 * 2^e, but at least -126 so that the
+    scale 2^e is a normal fp32 number (and an E8M0 code); 0 for an all-zero
+    block."""
     if amax == 0.0:
         return 0
     frac, ex = math.frexp(amax)            # amax = frac * 2^ex, frac in [0.5, 1)
     # 448 = 0.875 * 2^9, so amax <= 0.875 * 2^(9+e) <=> e >= ex - 9 (+1 if frac > 0.875)
-    return ex - 9 + (1 if frac > 0.875 else 0)
+    return max(ex - 9 + (1 if frac > 0.875 else 0), -126)
 
 
 def quantize_fp8_blocks(x: np.ndarray, block: int = 64):

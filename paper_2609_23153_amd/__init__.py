@@ -1,0 +1,233 @@
+"""Python binding of libsparseattn (gfx950 block-sparse attention).
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels behind the C ABI declared in include/sparse_attn.h.  PyTorch provides
+device memory (tensors, workspaces) and the current HIP stream.  There is no
+fallback: if the shared library is missing, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+import torch
+
+__all__ = [
+    "LIB_PATH", "SparseAttnError", "SA_SELECT_ROW_TOPK", "SA_SELECT_HEAD_TOPK",
+    "SA_OP_SELECT", "SA_OP_FWD", "SA_OP_FWD_FP8", "library", "sparse_attn_version",
+    "sparse_attn_status_str", "sparse_attn_keep_count", "sparse_attn_workspace_size",
+    "sparse_attn_select", "sparse_attn_fwd", "sparse_attn_quant_fp8", "sparse_attn_fwd_fp8",
+    "make_desc", "EXPORTED_SYMBOLS",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsparseattn.so")
+
+SA_SELECT_ROW_TOPK = 0
+SA_SELECT_HEAD_TOPK = 1
+SA_OP_SELECT, SA_OP_FWD, SA_OP_FWD_FP8 = 0, 1, 2
+
+EXPORTED_SYMBOLS = (
+    "sparse_attn_version", "sparse_attn_status_str", "sparse_attn_keep_count",
+    "sparse_attn_workspace_size", "sparse_attn_select", "sparse_attn_fwd",
+    "sparse_attn_quant_fp8", "sparse_attn_fwd_fp8",
+)
+
+
+class SparseAttnError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {sparse_attn_status_str(status)} ({status})")
+        self.status = status
+
+
+class SparseAttnDesc(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32), ("heads", ctypes.c_int32), ("seqlen", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32), ("block", ctypes.c_int32),
+        ("q_stride", ctypes.c_int64 * 3), ("k_stride", ctypes.c_int64 * 3),
+        ("v_stride", ctypes.c_int64 * 3), ("o_stride", ctypes.c_int64 * 3),
+        ("softmax_scale", ctypes.c_float),
+    ]
+
+
+_LIB = None
+_P = ctypes.c_void_p
+_I32P = ctypes.POINTER(ctypes.c_int32)
+
+
+def library() -> ctypes.CDLL:
+    """The loaded shared library (raises if it has not been built)."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -c 'import __graft_entry__ as g; g.build()'`")
+        lib = ctypes.CDLL(LIB_PATH)
+        D = ctypes.POINTER(SparseAttnDesc)
+        sig = {
+            "sparse_attn_version": (ctypes.c_int, []),
+            "sparse_attn_status_str": (ctypes.c_char_p, [ctypes.c_int]),
+            "sparse_attn_keep_count": (ctypes.c_int32, [ctypes.c_int32, ctypes.c_int32]),
+            "sparse_attn_workspace_size": (ctypes.c_size_t, [D, ctypes.c_int32, ctypes.c_int32]),
+            "sparse_attn_select": (ctypes.c_int, [D, _P, _P, ctypes.c_int32, ctypes.c_int64,
+                                                  _P, _P, ctypes.c_int32, _P, ctypes.c_size_t, _P]),
+            "sparse_attn_fwd": (ctypes.c_int, [D, _P, _P, _P, _P, _P, ctypes.c_int32, _P, _P,
+                                               _P, ctypes.c_size_t, _P]),
+            "sparse_attn_quant_fp8": (ctypes.c_int, [D, _P, ctypes.POINTER(ctypes.c_int64),
+                                                     _P, _P, _P]),
+            "sparse_attn_fwd_fp8": (ctypes.c_int, [D, _P, _P, _P, _P, _P, _P, _P, _P,
+                                                   ctypes.c_int32, _P, _P, _P, ctypes.c_size_t,
+                                                   _P]),
+        }
+        for name, (res, args) in sig.items():
+            fn = getattr(lib, name)
+            fn.restype, fn.argtypes = res, args
+        _LIB = lib
+    return _LIB
+
+
+# ------------------------------------------------------------------ helpers
+def _strides(t):
+    if t is None:
+        return (0, 0, 0)
+    if t.dim() != 4 or t.stride(3) != 1:
+        raise ValueError("expected a [B, H, N, d] tensor with contiguous channels")
+    return tuple(t.stride()[:3])
+
+
+def make_desc(q, k=None, v=None, o=None, block: int = 64, softmax_scale: float = 0.0):
+    """Descriptor for [B, H, N, d] tensors (strides in elements)."""
+    B, H, N, d = q.shape
+    desc = SparseAttnDesc()
+    desc.batch, desc.heads, desc.seqlen, desc.head_dim, desc.block = B, H, N, d, block
+    for field, t in (("q_stride", q), ("k_stride", k), ("v_stride", v), ("o_stride", o)):
+        getattr(desc, field)[:] = _strides(t)
+    desc.softmax_scale = softmax_scale
+    return desc
+
+
+def _stream(t):
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _check(status, what):
+    if status != 0:
+        raise SparseAttnError(status, what)
+
+
+def _num_blocks(n, block):
+    return -(-n // block)
+
+
+# --------------------------------------------------------------------- API
+def sparse_attn_version() -> int:
+    return library().sparse_attn_version()
+
+
+def sparse_attn_status_str(status: int) -> str:
+    return library().sparse_attn_status_str(status).decode()
+
+
+def sparse_attn_keep_count(keep_bp: int, nkb: int) -> int:
+    return library().sparse_attn_keep_count(keep_bp, nkb)
+
+
+def sparse_attn_workspace_size(desc: SparseAttnDesc, op: int, kmax: int = 1) -> int:
+    return library().sparse_attn_workspace_size(ctypes.byref(desc), op, kmax)
+
+
+def _workspace(desc, op, kmax, device):
+    n = sparse_attn_workspace_size(desc, op, kmax)
+    if n == 0:
+        raise SparseAttnError(-2, "workspace size")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def sparse_attn_select(q, k, budget: int, block: int = 64, mode: int = SA_SELECT_ROW_TOPK,
+                       kmax: int | None = None, idx=None, cnt=None, ws=None):
+    """Block selection on bf16 q, k [B, H, N, 128].  Returns (idx, cnt):
+    idx int32 [B, H, nb, kmax] (ascending, -1 padded), cnt int32 [B, H, nb]."""
+    B, H, N, _ = q.shape
+    nb = _num_blocks(N, block)
+    if kmax is None:
+        kmax = budget if mode == SA_SELECT_ROW_TOPK else nb
+    desc = make_desc(q, k, block=block)
+    if idx is None:
+        idx = torch.empty(B, H, nb, kmax, dtype=torch.int32, device=q.device)
+    if cnt is None:
+        cnt = torch.empty(B, H, nb, dtype=torch.int32, device=q.device)
+    if ws is None:
+        ws = _workspace(desc, SA_OP_SELECT, kmax, q.device)
+    st = library().sparse_attn_select(ctypes.byref(desc), _ptr(q), _ptr(k), mode, budget,
+                                      _ptr(idx), _ptr(cnt), kmax, _ptr(ws), ws.numel(),
+                                      _stream(q))
+    _check(st, "sparse_attn_select")
+    return idx, cnt
+
+
+def sparse_attn_fwd(q, k, v, idx, cnt, block: int = 64, softmax_scale: float = 0.0,
+                    with_lse: bool = True, o=None, lse=None, ws=None):
+    """Block-sparse attention forward on bf16 q, k, v [B, H, N, 128] with the
+    lists from sparse_attn_select.  Returns (o bf16 [B, H, N, 128], lse fp32
+    [B, H, N] or None)."""
+    B, H, N, _ = q.shape
+    kmax = idx.shape[-1]
+    if o is None:
+        o = torch.empty_like(q, memory_format=torch.contiguous_format)
+    if with_lse and lse is None:
+        lse = torch.empty(B, H, N, dtype=torch.float32, device=q.device)
+    desc = make_desc(q, k, v, o, block=block, softmax_scale=softmax_scale)
+    if ws is None:
+        ws = _workspace(desc, SA_OP_FWD, kmax, q.device)
+    st = library().sparse_attn_fwd(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(idx),
+                                   _ptr(cnt), kmax, _ptr(o), _ptr(lse if with_lse else None),
+                                   _ptr(ws), ws.numel(), _stream(q))
+    _check(st, "sparse_attn_fwd")
+    return o, (lse if with_lse else None)
+
+
+def sparse_attn_quant_fp8(x, block: int = 64, x8=None, scale=None):
+    """e4m3 quantisation with one power-of-two scale per block of tokens.
+    Returns (x8 uint8 [B, H, N, 128] contiguous, scale fp32 [B, H, nb])."""
+    B, H, N, _ = x.shape
+    desc = make_desc(x, block=block)
+    if x8 is None:
+        x8 = torch.empty(B, H, N, x.shape[3], dtype=torch.uint8, device=x.device)
+    if scale is None:
+        scale = torch.empty(B, H, _num_blocks(N, block), dtype=torch.float32, device=x.device)
+    xs = (ctypes.c_int64 * 3)(*_strides(x))
+    st = library().sparse_attn_quant_fp8(ctypes.byref(desc), _ptr(x), xs, _ptr(x8),
+                                         _ptr(scale), _stream(x))
+    _check(st, "sparse_attn_quant_fp8")
+    return x8, scale
+
+
+def sparse_attn_fwd_fp8(q8, sq, k8, sk, v8, sv, idx, cnt, block: int = 64,
+                        softmax_scale: float = 0.0, with_lse: bool = True, o=None, lse=None,
+                        ws=None):
+    """Block-sparse attention forward on e4m3 operands from
+    sparse_attn_quant_fp8.  Returns (o bf16 [B, H, N, 128], lse or None)."""
+    B, H, N, d = q8.shape
+    kmax = idx.shape[-1]
+    if o is None:
+        o = torch.empty(B, H, N, d, dtype=torch.bfloat16, device=q8.device)
+    if with_lse and lse is None:
+        lse = torch.empty(B, H, N, dtype=torch.float32, device=q8.device)
+    desc = make_desc(o, o=o, block=block, softmax_scale=softmax_scale)
+    if ws is None:
+        ws = _workspace(desc, SA_OP_FWD_FP8, kmax, q8.device)
+    st = library().sparse_attn_fwd_fp8(ctypes.byref(desc), _ptr(q8), _ptr(sq), _ptr(k8),
+                                       _ptr(sk), _ptr(v8), _ptr(sv), _ptr(idx), _ptr(cnt), kmax,
+                                       _ptr(o), _ptr(lse if with_lse else None), _ptr(ws),
+                                       ws.numel(), _stream(q8))
+    _check(st, "sparse_attn_fwd_fp8")
+    return o, (lse if with_lse else None)
+
+
+def default_softmax_scale(d: int) -> float:
+    """fp32(1/sqrt(d)), the scale the library uses when 0 is passed."""
+    return float(torch.tensor(1.0 / math.sqrt(d), dtype=torch.float32))

@@ -1,0 +1,201 @@
+// C ABI of the library: argument checks on the host, then launches.
+// Every check runs before the first HIP call, so invalid calls launch nothing
+// (and can be exercised on a machine without a GPU).
+#include <math.h>
+
+#include "launch.h"
+#include "sparse_attn.h"
+
+namespace {
+
+using sa::Shape;
+using sa::Strides;
+
+constexpr int kMaxBlocks = 4096;  // nb limit of the selection kernels
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool strides_ok(const int64_t st[3]) {
+  for (int i = 0; i < 3; ++i)
+    if (st[i] < 0 || (st[i] & 7) != 0) return false;
+  return true;
+}
+
+// Shape checks shared by every call.  Returns SA_OK or an error code.
+int check_desc(const sparse_attn_desc* d, Shape* s) {
+  if (!d) return SA_ERR_INVALID_ARG;
+  if (d->batch < 1 || d->heads < 1 || d->seqlen < 1) return SA_ERR_INVALID_ARG;
+  if (!(d->softmax_scale >= 0.f) || isinf(d->softmax_scale)) return SA_ERR_INVALID_ARG;
+  if (d->head_dim != 128) return SA_ERR_UNSUPPORTED;
+  if (d->block != 64 && d->block != 128) return SA_ERR_UNSUPPORTED;
+  const int64_t nb = (d->seqlen + (int64_t)d->block - 1) / d->block;
+  if (nb > kMaxBlocks) return SA_ERR_UNSUPPORTED;
+  if ((int64_t)d->batch * d->heads * nb > (int64_t)1 << 30) return SA_ERR_UNSUPPORTED;
+  s->B = d->batch;
+  s->H = d->heads;
+  s->N = d->seqlen;
+  s->block = d->block;
+  s->nb = (int)nb;
+  return SA_OK;
+}
+
+Strides to_strides(const int64_t st[3]) { return Strides{st[0], st[1], st[2]}; }
+
+float effective_scale(const sparse_attn_desc* d) {
+  return d->softmax_scale > 0.f ? d->softmax_scale : (float)(1.0 / sqrt((double)d->head_dim));
+}
+
+int launch_status(hipError_t e) { return e == hipSuccess ? SA_OK : SA_ERR_LAUNCH; }
+
+size_t fwd_workspace(const Shape& s) { return sa::schedule_workspace_bytes(s); }
+
+int check_lists(const Shape& s, const int32_t* idx, const int32_t* cnt, int32_t kmax) {
+  if (!idx || !cnt) return SA_ERR_INVALID_ARG;
+  if (kmax < 1 || kmax > (1 << 16)) return SA_ERR_INVALID_ARG;
+  return SA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int sparse_attn_version(void) { return SPARSE_ATTN_VERSION; }
+
+const char* sparse_attn_status_str(int status) {
+  switch (status) {
+    case SA_OK: return "ok";
+    case SA_ERR_INVALID_ARG: return "invalid argument";
+    case SA_ERR_UNSUPPORTED: return "unsupported problem shape";
+    case SA_ERR_WORKSPACE: return "workspace too small";
+    case SA_ERR_LAUNCH: return "HIP launch failed";
+    case SA_ERR_DEVICE: return "no usable gfx950 device";
+    default: return "unknown status";
+  }
+}
+
+int32_t sparse_attn_keep_count(int32_t keep_bp, int32_t nkb) {
+  if (keep_bp < 1 || nkb < 1) return -1;
+  const int64_t k = ((int64_t)keep_bp * nkb + 9999) / 10000;
+  return (int32_t)(k < 1 ? 1 : (k > nkb ? nkb : k));
+}
+
+size_t sparse_attn_workspace_size(const sparse_attn_desc* desc, int32_t op, int32_t kmax) {
+  Shape s;
+  if (check_desc(desc, &s) != SA_OK) return 0;
+  switch (op) {
+    case SA_OP_SELECT: return sa::select_workspace_bytes(s);
+    case SA_OP_FWD:
+    case SA_OP_FWD_FP8: return kmax >= 1 ? fwd_workspace(s) : 0;
+    default: return 0;
+  }
+}
+
+int sparse_attn_select(const sparse_attn_desc* desc, const void* q, const void* k, int32_t mode,
+                       int64_t budget, int32_t* idx, int32_t* cnt, int32_t kmax, void* ws,
+                       size_t ws_bytes, void* stream) {
+  Shape s;
+  int st = check_desc(desc, &s);
+  if (st != SA_OK) return st;
+  if (!q || !k || !idx || !cnt || !ws) return SA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !strides_ok(desc->q_stride) || !strides_ok(desc->k_stride))
+    return SA_ERR_INVALID_ARG;
+  if (kmax < 1) return SA_ERR_INVALID_ARG;
+  if (mode == SA_SELECT_ROW_TOPK) {
+    if (budget < 1 || budget > s.nb || kmax < budget) return SA_ERR_INVALID_ARG;
+  } else if (mode == SA_SELECT_HEAD_TOPK) {
+    if (budget < s.nb || budget > (int64_t)s.nb * s.nb) return SA_ERR_INVALID_ARG;
+  } else {
+    return SA_ERR_INVALID_ARG;
+  }
+  if (ws_bytes < sa::select_workspace_bytes(s)) return SA_ERR_WORKSPACE;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (mode == SA_SELECT_ROW_TOPK)
+    return launch_status(sa::launch_select_row(s, q, to_strides(desc->q_stride), k,
+                                               to_strides(desc->k_stride), (int)budget, kmax,
+                                               idx, cnt, ws, hs));
+  const hipError_t e = sa::launch_select_head(s, q, to_strides(desc->q_stride), k,
+                                              to_strides(desc->k_stride), budget, kmax, idx,
+                                              cnt, ws, hs);
+  return e == hipErrorNotSupported ? SA_ERR_UNSUPPORTED : launch_status(e);
+}
+
+int sparse_attn_fwd(const sparse_attn_desc* desc, const void* q, const void* k, const void* v,
+                    const int32_t* idx, const int32_t* cnt, int32_t kmax, void* o, float* lse,
+                    void* ws, size_t ws_bytes, void* stream) {
+  Shape s;
+  int st = check_desc(desc, &s);
+  if (st != SA_OK) return st;
+  if (!q || !k || !v || !o || !ws) return SA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return SA_ERR_INVALID_ARG;
+  if (!strides_ok(desc->q_stride) || !strides_ok(desc->k_stride) ||
+      !strides_ok(desc->v_stride) || !strides_ok(desc->o_stride))
+    return SA_ERR_INVALID_ARG;
+  if ((st = check_lists(s, idx, cnt, kmax)) != SA_OK) return st;
+  if (ws_bytes < fwd_workspace(s)) return SA_ERR_WORKSPACE;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  sa::FwdArgs a{};
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.o = o;
+  a.lse = lse;
+  a.qs = to_strides(desc->q_stride);
+  a.ks = to_strides(desc->k_stride);
+  a.vs = to_strides(desc->v_stride);
+  a.os = to_strides(desc->o_stride);
+  a.idx = idx;
+  a.cnt = cnt;
+  a.kmax = kmax;
+  a.softmax_scale = effective_scale(desc);
+  hipError_t e = sa::launch_schedule(s, cnt, kmax, ws, &a.order, hs);
+  if (e != hipSuccess) return SA_ERR_LAUNCH;
+  return launch_status(sa::launch_fwd_bf16(s, a, hs));
+}
+
+int sparse_attn_quant_fp8(const sparse_attn_desc* desc, const void* x, const int64_t x_stride[3],
+                          uint8_t* x8, float* scale, void* stream) {
+  Shape s;
+  int st = check_desc(desc, &s);
+  if (st != SA_OK) return st;
+  if (!x || !x_stride || !x8 || !scale) return SA_ERR_INVALID_ARG;
+  if (!aligned16(x) || !aligned16(x8) || !strides_ok(x_stride)) return SA_ERR_INVALID_ARG;
+  return launch_status(
+      sa::launch_quant_fp8(s, x, to_strides(x_stride), x8, scale, static_cast<hipStream_t>(stream)));
+}
+
+int sparse_attn_fwd_fp8(const sparse_attn_desc* desc, const uint8_t* q8, const float* sq,
+                        const uint8_t* k8, const float* sk, const uint8_t* v8, const float* sv,
+                        const int32_t* idx, const int32_t* cnt, int32_t kmax, void* o, float* lse,
+                        void* ws, size_t ws_bytes, void* stream) {
+  Shape s;
+  int st = check_desc(desc, &s);
+  if (st != SA_OK) return st;
+  if (!q8 || !sq || !k8 || !sk || !v8 || !sv || !o || !ws) return SA_ERR_INVALID_ARG;
+  if (!aligned16(q8) || !aligned16(k8) || !aligned16(v8) || !aligned16(o))
+    return SA_ERR_INVALID_ARG;
+  if (!strides_ok(desc->o_stride)) return SA_ERR_INVALID_ARG;
+  if ((st = check_lists(s, idx, cnt, kmax)) != SA_OK) return st;
+  if (ws_bytes < fwd_workspace(s)) return SA_ERR_WORKSPACE;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  const int64_t tok = 128, head = (int64_t)s.N * tok, bat = head * s.H;
+  sa::FwdArgs a{};
+  a.q = q8;
+  a.k = k8;
+  a.v = v8;
+  a.o = o;
+  a.lse = lse;
+  a.qs = a.ks = a.vs = Strides{bat, head, tok};
+  a.os = to_strides(desc->o_stride);
+  a.idx = idx;
+  a.cnt = cnt;
+  a.sq = sq;
+  a.sk = sk;
+  a.sv = sv;
+  a.kmax = kmax;
+  a.softmax_scale = effective_scale(desc);
+  hipError_t e = sa::launch_schedule(s, cnt, kmax, ws, &a.order, hs);
+  if (e != hipSuccess) return SA_ERR_LAUNCH;
+  return launch_status(sa::launch_fwd_fp8(s, a, hs));
+}
+
+}  // extern "C"

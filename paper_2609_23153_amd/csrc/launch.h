@@ -1,0 +1,61 @@
+// Host-side launchers of the gfx950 kernels (internal to the library; the
+// public C ABI lives in include/sparse_attn.h).  Arguments have been checked
+// by the caller; every launcher only enqueues work on `stream`.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sa {
+
+struct Strides {
+  int64_t b, h, n;  // elements per batch, head, token
+};
+
+struct Shape {
+  int B, H, N, block, nb;  // nb = ceil(N / block) query blocks = key blocks
+};
+
+// ---- selection -----------------------------------------------------------
+// Workspace layout: qhat [B*H*nb*128] f64 | khat [same] | scores [B*H*nb*nb] f64
+size_t select_workspace_bytes(const Shape& s);
+hipError_t launch_select_row(const Shape& s, const void* q, Strides qs, const void* k,
+                             Strides ks, int topk, int kmax, int32_t* idx, int32_t* cnt,
+                             void* ws, hipStream_t stream);
+hipError_t launch_select_head(const Shape& s, const void* q, Strides qs, const void* k,
+                              Strides ks, int64_t budget, int kmax, int32_t* idx,
+                              int32_t* cnt, void* ws, hipStream_t stream);
+
+// ---- scheduling ----------------------------------------------------------
+size_t schedule_workspace_bytes(const Shape& s);
+// Writes the 64-row query tiles in launch order into the workspace and
+// returns a pointer to that list (int32 [B*H*ceil(N/64)]).
+hipError_t launch_schedule(const Shape& s, const int32_t* cnt, int kmax, void* ws,
+                           const int32_t** order, hipStream_t stream);
+
+// ---- forward -------------------------------------------------------------
+struct FwdArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  void* o;
+  float* lse;
+  Strides qs, ks, vs, os;
+  const int32_t* idx;
+  const int32_t* cnt;
+  const int32_t* order;  // launch order of query tiles (may be null: natural)
+  const float* sq;       // fp8 block scales (fp8 path only)
+  const float* sk;
+  const float* sv;
+  int kmax;
+  float softmax_scale;
+};
+hipError_t launch_fwd_bf16(const Shape& s, const FwdArgs& a, hipStream_t stream);
+hipError_t launch_fwd_fp8(const Shape& s, const FwdArgs& a, hipStream_t stream);
+
+// ---- fp8 quantisation ----------------------------------------------------
+hipError_t launch_quant_fp8(const Shape& s, const void* x, Strides xs, uint8_t* x8,
+                            float* scale, hipStream_t stream);
+
+}  // namespace sa

@@ -1,0 +1,63 @@
+"""Shared plumbing of the GPU parity tests: seeded inputs, oracle per head,
+error metrics.  (Not a test module.)"""
+import sys
+
+import numpy as np
+import torch
+
+import oracle as O
+
+# Parity bar: index lists bit-exact; bf16 outputs rel-L2 <= 1e-2 and max-abs
+# <= 2e-2 against the fp64 oracle; fp8 outputs rel-L2 <= 5e-2.
+BF16_REL_L2 = 1e-2
+BF16_MAX_ABS = 2e-2
+FP8_REL_L2 = 5e-2
+LSE_ABS = 2e-3
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def widen(t):
+    """bf16 CPU tensor -> float64 numpy (exact)."""
+    return t.to(torch.float64).numpy()
+
+
+def rel_l2(x, ref):
+    ref = np.asarray(ref, dtype=np.float64)
+    x = np.asarray(x, dtype=np.float64)
+    den = np.linalg.norm(ref)
+    return float(np.linalg.norm(x - ref) / (den if den > 0 else 1.0))
+
+
+def oracle_select(q, k, block, keep_bp, mode="row"):
+    """q, k: bf16 CPU [N, d] -> (idx, cnt) of the oracle."""
+    return O.select_head(widen(q), widen(k), block, keep_bp, mode)
+
+
+def oracle_attend(q, k, v, idx, cnt, block, tau, qblocks=None):
+    return O.sparse_attention(widen(q), widen(k), widen(v), idx, cnt, block, tau, qblocks)
+
+
+def check_out(o_gpu, lse_gpu, o_ref, lse_ref, rows=None, rel=BF16_REL_L2, mabs=BF16_MAX_ABS,
+              what=""):
+    """o_gpu [N, d] (any float dtype, CPU), lse_gpu [N] against the oracle."""
+    o = o_gpu.to(torch.float64).numpy()
+    lse = lse_gpu.to(torch.float64).numpy() if lse_gpu is not None else None
+    if rows is not None:
+        o, o_ref = o[rows], o_ref[rows]
+        lse = lse[rows] if lse is not None else None
+        lse_ref = lse_ref[rows]
+    err = rel_l2(o, o_ref)
+    mx = float(np.abs(o - o_ref).max()) if o.size else 0.0
+    say(f"  {what}: rel_l2={err:.3e} max_abs={mx:.3e}")
+    assert err <= rel, (what, err)
+    if mabs is not None:
+        assert mx <= mabs, (what, mx)
+    if lse is not None:
+        fin = np.isfinite(lse_ref)
+        assert np.array_equal(np.isneginf(lse), np.isneginf(lse_ref)), what
+        if fin.any():
+            assert np.abs(lse[fin] - lse_ref[fin]).max() <= LSE_ABS, what

@@ -1,0 +1,134 @@
+"""Host-side checks of the C ABI: the library loads, exports every function
+the header declares, and rejects invalid arguments before any HIP call (so
+these run without a GPU)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2609_23153_amd as sa
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sparse_attn.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sparse_attn_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    assert declared_functions() == sorted(sa.EXPORTED_SYMBOLS)
+
+
+def test_library_exports_every_declared_symbol():
+    out = subprocess.run(["nm", "-D", "--defined-only", sa.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT\s+(\w+)", out))
+    for name in declared_functions():
+        assert name in exported, name
+        assert hasattr(sa.library(), name)
+
+
+def test_version_status_keep_count():
+    assert sa.sparse_attn_version() == 100
+    assert sa.sparse_attn_status_str(0) == "ok"
+    assert sa.sparse_attn_status_str(-3) == "workspace too small"
+    assert sa.sparse_attn_status_str(12345) == "unknown status"
+    assert sa.sparse_attn_keep_count(1000, 64) == 7
+    assert sa.sparse_attn_keep_count(300, 1182) == 36
+    assert sa.sparse_attn_keep_count(10000, 591) == 591
+    assert sa.sparse_attn_keep_count(1, 10) == 1
+    assert sa.sparse_attn_keep_count(0, 10) == -1
+
+
+def desc(B=1, H=2, N=4096, d=128, block=64, scale=0.0):
+    ds = sa.SparseAttnDesc()
+    ds.batch, ds.heads, ds.seqlen, ds.head_dim, ds.block = B, H, N, d, block
+    st = (H * N * d, N * d, d)
+    for f in ("q_stride", "k_stride", "v_stride", "o_stride"):
+        getattr(ds, f)[:] = st
+    ds.softmax_scale = scale
+    return ds
+
+
+def test_workspace_size_formula():
+    lib = sa.library()
+    ds = desc(B=1, H=40, N=75600)
+    nb = 1182
+    assert lib.sparse_attn_workspace_size(ctypes.byref(ds), 0, 36) == \
+        40 * nb * 128 * 8 * 2 + 40 * nb * nb * 8
+    assert lib.sparse_attn_workspace_size(ctypes.byref(ds), 1, 36) > 0
+    assert lib.sparse_attn_workspace_size(ctypes.byref(ds), 1, 0) == 0
+    assert lib.sparse_attn_workspace_size(ctypes.byref(ds), 7, 36) == 0
+    assert lib.sparse_attn_workspace_size(ctypes.byref(desc(d=64)), 0, 1) == 0
+    assert lib.sparse_attn_workspace_size(None, 0, 1) == 0
+
+
+# Fake, aligned, non-null device addresses: every call below must fail its
+# host-side checks, so nothing is ever dereferenced or launched.
+P = ctypes.c_void_p(1 << 20)
+MIS = ctypes.c_void_p((1 << 20) + 2)
+WS = 1 << 40
+
+
+@pytest.mark.parametrize("case,expect", [
+    (dict(d=64), -2), (dict(block=32), -2), (dict(block=256), -2), (dict(N=0), -1),
+    (dict(B=0), -1), (dict(H=-1), -1), (dict(scale=-1.0), -1), (dict(scale=float("nan")), -1),
+    (dict(N=64 * 4097), -2),
+])
+def test_select_rejects_bad_descriptors(case, expect):
+    lib = sa.library()
+    ds = desc(**case)
+    st = lib.sparse_attn_select(ctypes.byref(ds), P, P, 0, 7, P, P, 7, P, WS, None)
+    assert st == expect
+
+
+def test_select_rejects_bad_arguments():
+    lib = sa.library()
+    ds = desc()
+    call = lambda *a: lib.sparse_attn_select(ctypes.byref(ds), *a)
+    assert call(None, P, 0, 7, P, P, 7, P, WS, None) == -1          # null q
+    assert call(P, P, 0, 7, None, P, 7, P, WS, None) == -1          # null idx
+    assert call(MIS, P, 0, 7, P, P, 7, P, WS, None) == -1           # misaligned q
+    assert call(P, P, 0, 0, P, P, 7, P, WS, None) == -1             # topk 0
+    assert call(P, P, 0, 65, P, P, 65, P, WS, None) == -1           # topk > nkb
+    assert call(P, P, 0, 7, P, P, 6, P, WS, None) == -1             # kmax < topk
+    assert call(P, P, 9, 7, P, P, 7, P, WS, None) == -1             # bad mode
+    assert call(P, P, 1, 63, P, P, 7, P, WS, None) == -1            # head budget < nqb
+    assert call(P, P, 1, 64 * 64 + 1, P, P, 7, P, WS, None) == -1   # head budget > nqb*nkb
+    assert call(P, P, 0, 7, P, P, 7, P, 100, None) == -3            # workspace too small
+    ds.q_stride[2] = 130                                            # stride not multiple of 8
+    assert call(P, P, 0, 7, P, P, 7, P, WS, None) == -1
+
+
+def test_fwd_rejects_bad_arguments():
+    lib = sa.library()
+    ds = desc()
+    call = lambda *a: lib.sparse_attn_fwd(ctypes.byref(ds), *a)
+    assert call(None, P, P, P, P, 7, P, None, P, WS, None) == -1    # null q
+    assert call(P, P, P, None, P, 7, P, None, P, WS, None) == -1    # null idx
+    assert call(P, P, P, P, None, 7, P, None, P, WS, None) == -1    # null cnt
+    assert call(P, P, P, P, P, 0, P, None, P, WS, None) == -1       # kmax 0
+    assert call(P, P, P, P, P, 7, MIS, None, P, WS, None) == -1     # misaligned o
+    assert call(P, P, P, P, P, 7, P, None, P, 8, None) == -3        # workspace
+    ds.head_dim = 96
+    assert call(P, P, P, P, P, 7, P, None, P, WS, None) == -2
+
+
+def test_quant_and_fwd_fp8_reject_bad_arguments():
+    lib = sa.library()
+    ds = desc()
+    st3 = (ctypes.c_int64 * 3)(2 * 4096 * 128, 4096 * 128, 128)
+    assert lib.sparse_attn_quant_fp8(ctypes.byref(ds), None, st3, P, P, None) == -1
+    assert lib.sparse_attn_quant_fp8(ctypes.byref(ds), P, None, P, P, None) == -1
+    assert lib.sparse_attn_quant_fp8(ctypes.byref(ds), MIS, st3, P, P, None) == -1
+    bad = (ctypes.c_int64 * 3)(2 * 4096 * 128, 4096 * 128, 129)
+    assert lib.sparse_attn_quant_fp8(ctypes.byref(ds), P, bad, P, P, None) == -1
+    f = lambda *a: lib.sparse_attn_fwd_fp8(ctypes.byref(ds), *a)
+    assert f(P, None, P, P, P, P, P, P, 7, P, None, P, WS, None) == -1   # null sq
+    assert f(P, P, P, P, P, P, P, P, 0, P, None, P, WS, None) == -1      # kmax 0
+    assert f(P, P, P, P, P, P, P, P, 7, P, None, P, 4, None) == -3       # workspace

@@ -311,8 +311,9 @@ def test_fp8_scale_exponent_bruteforce():
     for a in vals:
         e = O.fp8_scale_exponent(float(a))
         brute = next(ee for ee in range(-200, 200) if a <= 448.0 * 2.0 ** ee)
-        assert e == brute, a
+        assert e == max(brute, -126), a
     assert O.fp8_scale_exponent(0.0) == 0
+    assert O.fp8_scale_exponent(1e-40) == -126          # clamped: 2^e stays a normal fp32
 
 
 def test_quantize_blocks_properties():
