@@ -1,0 +1,208 @@
+#!/usr/bin/env python3
+"""Benchmark of the block-sparse attention hot path on one MI355X.
+
+A step is one pass of the whole path over one layer's synthetic inputs, all
+resident in HBM before timing starts: block selection (pool + fp64 score +
+top-k), work scheduling, and the fused sparse forward, all in the HIP library.
+Default workload: the Wan2.1-T2V-14B 720P attention layer shape (B=1, H=40,
+L=75,600 tokens = 21x45x80 latent grid, d=128) at 97% block sparsity
+(64x64 blocks, 36 of 1182 key blocks kept per query block), bf16.
+
+Prints one JSON line.  `value` is the dense-equivalent TFLOP/s of the whole
+step (4*B*H*L^2*d flops of the dense attention the step replaces, divided by
+the step time); `roofline` reports the fused forward kernel's actual flops
+over the selected blocks against the bf16 MFMA peak, timed with HIP events on
+the stream the kernels run on; `cpu_baseline` times the fp64 CPU oracle on a
+bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+import torch  # noqa: E402
+
+METRIC = "ms/call + dense-equiv TFLOP/s and % MFMA peak, block-sparse attn @97%"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_FP8_TFLOPS = 5000.0    # MI355X dense fp8 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def parse_args():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="wan14b_720p")
+    ap.add_argument("--cpu-baseline", choices=["on", "off"], default="on")
+    ap.add_argument("--cpu-heads", type=int, default=2,
+                    help="heads of the workload the oracle runs for the CPU baseline")
+    ap.add_argument("--copy-calib", action="store_true",
+                    help="also time a plain 1 GiB device copy (HBM counter calibration)")
+    return ap.parse_args()
+
+
+def selected_flops(cnt, idx, N, block, d):
+    """Algorithmic flops of the fused forward: 4 * n_i * n_j * d over every
+    selected (query block i, key block j) pair (QK^T and PV, 2 flops/MAC)."""
+    nb = cnt.shape[-1]
+    sizes = np.full(nb, block, dtype=np.int64)
+    sizes[-1] = N - (nb - 1) * block
+    kmax = idx.shape[-1]
+    valid = np.arange(kmax)[None, None, None, :] < cnt[..., None]
+    nj = np.where(valid & (idx >= 0), sizes[np.clip(idx, 0, nb - 1)], 0).sum(-1)  # [B,H,nb]
+    return int(4 * d * (nj * sizes[None, None, :]).sum())
+
+
+def blas_threads():
+    """Threads of the BLAS that NumPy (the oracle) runs on."""
+    try:
+        from threadpoolctl import threadpool_info
+        n = [p["num_threads"] for p in threadpool_info() if p.get("user_api") == "blas"]
+        if n:
+            return int(max(n))
+    except Exception:
+        pass
+    return len(os.sched_getaffinity(0))
+
+
+def main():
+    args = parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import paper_2609_23153_amd as sa
+    import workloads as W
+
+    wl = W.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    B, H, N, d, block = wl.batch, wl.heads, wl.seqlen, wl.head_dim, wl.block
+    nb = -(-N // block)
+    k = sa.sparse_attn_keep_count(wl.keep_bp, nb)
+
+    q, kk, v = (t.to(dev) for t in W.make_inputs(wl))
+    idx = torch.empty(B, H, nb, k, dtype=torch.int32, device=dev)
+    cnt = torch.empty(B, H, nb, dtype=torch.int32, device=dev)
+    o = torch.empty_like(q)
+    lse = torch.empty(B, H, N, dtype=torch.float32, device=dev)
+    desc = sa.make_desc(q, kk, v, o, block=block)
+    ws_sel = torch.empty(sa.sparse_attn_workspace_size(desc, sa.SA_OP_SELECT, k),
+                         dtype=torch.uint8, device=dev)
+    ws_sch = torch.empty(sa.sparse_attn_workspace_size(desc, sa.SA_OP_SCHEDULE, k),
+                         dtype=torch.uint8, device=dev)
+    order = torch.empty(sa.sparse_attn_num_tiles(desc), dtype=torch.int32, device=dev)
+    torch.cuda.synchronize()
+
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+
+    def step(e=None):
+        if e:
+            e[0].record()
+        sa.sparse_attn_select(q, kk, k, block=block, idx=idx, cnt=cnt, ws=ws_sel)
+        if e:
+            e[1].record()
+        sa.sparse_attn_schedule(cnt, N, k, block=block, order=order, ws=ws_sch)
+        if e:
+            e[2].record()
+        sa.sparse_attn_fwd(q, kk, v, idx, cnt, block=block, order=order, o=o, lse=lse)
+        if e:
+            e[3].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(ev[s])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    sel_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    sch_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    fwd_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in ev]))
+
+    flops = selected_flops(cnt.cpu().numpy(), idx.cpu().numpy(), N, block, d)
+    dense = 4 * B * H * N * N * d
+    fwd_tflops = flops / (fwd_ms * 1e-3) / 1e12
+    sel_bytes = 2 * B * H * N * d * 2 + B * H * nb * (k + 1) * 4
+    out = {
+        "metric": METRIC,
+        "value": round(dense / (ms_step * 1e-3) / 1e12, 2),
+        "unit": "dense-equiv TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": wl.name, "batch": B, "heads": H, "seqlen": N, "grid": list(wl.grid),
+            "head_dim": d, "block": block, "keep_blocks": k, "key_blocks": nb,
+            "sparsity": round(1 - k / nb, 4), "generator": wl.gen,
+        },
+        "ms_per_call": {"select": round(sel_ms, 4), "schedule": round(sch_ms, 4),
+                        "fwd": round(fwd_ms, 4)},
+        "fwd_actual_tflops": round(fwd_tflops, 2),
+        "fwd_dense_equiv_tflops": round(dense / (fwd_ms * 1e-3) / 1e12, 2),
+        "fwd_mfma_frac": round(fwd_tflops / PEAK_BF16_TFLOPS, 4),
+        "select_gbs": round(sel_bytes / (sel_ms * 1e-3) / 1e9, 1),
+        "roofline": {
+            "kernel": "fwd_bf16_kernel", "bound": "mfma",
+            "achieved": round(fwd_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(fwd_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+            "flops_per_launch": flops,
+        },
+    }
+
+    if args.copy_calib:
+        a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        bb = torch.empty_like(a)
+        for _ in range(3):
+            bb.copy_(a)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(5):
+            bb.copy_(a)
+        e1.record()
+        torch.cuda.synchronize()
+        out["copy_calib"] = {"bytes_each_way": 1 << 30, "ms": e0.elapsed_time(e1) / 5}
+
+    if args.cpu_baseline == "on":
+        import oracle as O
+        tau = W.softmax_scale(d)
+        sample = sorted({0, H - 1})[:max(1, args.cpu_heads)]
+        heads_data = [[t.to(torch.float64).numpy() for t in W.make_head(wl, 0, h)]
+                      for h in sample]
+        t0 = time.perf_counter()
+        for qf, kf, vf in heads_data:
+            ri, rc = O.select_head(qf, kf, block, wl.keep_bp)
+            O.sparse_attention(qf, kf, vf, ri, rc, block, tau)
+        secs = time.perf_counter() - t0
+        per_call = secs * (B * H) / len(sample)
+        out["cpu_baseline"] = {
+            "value": round(dense / per_call / 1e12, 6),
+            "unit": "dense-equiv TFLOP/s",
+            "ms_per_call": round(per_call * 1e3, 1),
+            "cores": blas_threads(),
+            "kind": "oracle",
+            "sample": f"fp64 NumPy oracle, select + attention of heads {sample} of {H} "
+                      f"({secs:.1f} s), scaled x{B * H / len(sample):g} to the full layer",
+        }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

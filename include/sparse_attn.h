@@ -53,8 +53,8 @@ enum {
   SA_SELECT_HEAD_TOPK = 1 /* ragged: `budget` (query, key) block pairs per head */
 };
 
-/* Workspace consumers (first argument of sparse_attn_workspace_size). */
-enum { SA_OP_SELECT = 0, SA_OP_FWD = 1, SA_OP_FWD_FP8 = 2 };
+/* Workspace consumers (second argument of sparse_attn_workspace_size). */
+enum { SA_OP_SELECT = 0, SA_OP_SCHEDULE = 1 };
 
 /*
  * Problem descriptor (host struct).
@@ -90,7 +90,7 @@ int32_t sparse_attn_keep_count(int32_t keep_bp, int32_t nkb);
 
 /* Bytes of device workspace that `op` needs for this problem; `kmax` is the
  * row stride of the index list (ignored for SA_OP_SELECT).  Returns 0 for an
- * invalid descriptor. */
+ * invalid descriptor or op. */
 size_t sparse_attn_workspace_size(const sparse_attn_desc* desc, int32_t op, int32_t kmax);
 
 /*
@@ -116,6 +116,25 @@ int sparse_attn_select(const sparse_attn_desc* desc, const void* q, const void* 
                        int32_t mode, int64_t budget, int32_t* idx, int32_t* cnt,
                        int32_t kmax, void* ws, size_t ws_bytes, void* stream);
 
+/* Number of 64-row query tiles, B * H * ceil(L / 64): the length of the
+ * launch order written by sparse_attn_schedule.  -1 for an invalid descriptor. */
+int64_t sparse_attn_num_tiles(const sparse_attn_desc* desc);
+
+/*
+ * Work scheduling for the fused forward (ragged per-query-block work, the
+ * selection lists of §2 Eq. comp-sparse being of unequal length in general).
+ * Writes the launch order of the B*H*ceil(L/64) query tiles (tile t = (b*H +
+ * h) * ceil(L/64) + row/64): tiles sorted by cost class floor(log2(key tiles))
+ * descending (longest first; stable, so equal-cost tiles keep raster order),
+ * then interleaved so that each XCD of the device receives runs of
+ * consecutive tiles.  Every tile appears exactly once.
+ *  cnt     int32 [B][H][nqb] list lengths (clamped to [0, kmax])
+ *  order   int32 [sparse_attn_num_tiles(desc)] out
+ *  ws      ws_bytes >= sparse_attn_workspace_size(SA_OP_SCHEDULE)
+ */
+int sparse_attn_schedule(const sparse_attn_desc* desc, const int32_t* cnt, int32_t kmax,
+                         int32_t* order, void* ws, size_t ws_bytes, void* stream);
+
 /*
  * Sparse branch O_s = A_M(Q, K, V) (paper §2 Eq. comp-sparse, §4.1), bf16.
  * For query block i with key-block list S_i = idx[b][h][i][0 .. cnt-1] and
@@ -125,14 +144,16 @@ int sparse_attn_select(const sparse_attn_desc* desc, const void* q, const void* 
  * List entries outside [0, nkb) are skipped and cnt is clamped to [0, kmax];
  * a query block with no valid entry gets O = 0 and LSE = -inf.
  *  q, k, v  bf16 via desc strides;  o  bf16 out via desc->o_stride
- *  idx/cnt  as written by sparse_attn_select (any ascending or not, duplicates
- *           are the caller's error: a duplicated block is counted twice)
+ *  idx/cnt  int32 [B][H][nqb][kmax] and [B][H][nqb], e.g. from
+ *           sparse_attn_select; entries need not be ascending, but a block
+ *           listed twice is attended twice (a caller error)
+ *  order    launch order from sparse_attn_schedule for the same cnt, or NULL
+ *           for plain raster order (results are identical either way)
  *  lse      fp32 [B][H][L] out, contiguous; may be NULL
- *  ws       ws_bytes >= sparse_attn_workspace_size(SA_OP_FWD, kmax)
  */
 int sparse_attn_fwd(const sparse_attn_desc* desc, const void* q, const void* k,
                     const void* v, const int32_t* idx, const int32_t* cnt, int32_t kmax,
-                    void* o, float* lse, void* ws, size_t ws_bytes, void* stream);
+                    const int32_t* order, void* o, float* lse, void* stream);
 
 /*
  * FP8 E4M3 (OCP e4m3fn) operand quantisation with one power-of-two scale per
@@ -154,13 +175,13 @@ int sparse_attn_quant_fp8(const sparse_attn_desc* desc, const void* x, const int
  * the fp8 matrix cores; the probabilities are rounded to e4m3 for the PV
  * product.  q8, k8, v8 are contiguous [B][H][L][d] e4m3 and sq, sk, sv are
  * [B][H][nb] power-of-two scales, both as written by sparse_attn_quant_fp8.
- * o, lse, idx, cnt, kmax and the workspace are as for sparse_attn_fwd
- * (ws_bytes >= sparse_attn_workspace_size(SA_OP_FWD_FP8, kmax)).
+ * o (via desc->o_stride), lse, idx, cnt, kmax and order are as for
+ * sparse_attn_fwd.
  */
 int sparse_attn_fwd_fp8(const sparse_attn_desc* desc, const uint8_t* q8, const float* sq,
                         const uint8_t* k8, const float* sk, const uint8_t* v8, const float* sv,
-                        const int32_t* idx, const int32_t* cnt, int32_t kmax, void* o,
-                        float* lse, void* ws, size_t ws_bytes, void* stream);
+                        const int32_t* idx, const int32_t* cnt, int32_t kmax,
+                        const int32_t* order, void* o, float* lse, void* stream);
 
 #ifdef __cplusplus
 }

@@ -15,22 +15,22 @@ import torch
 
 __all__ = [
     "LIB_PATH", "SparseAttnError", "SA_SELECT_ROW_TOPK", "SA_SELECT_HEAD_TOPK",
-    "SA_OP_SELECT", "SA_OP_FWD", "SA_OP_FWD_FP8", "library", "sparse_attn_version",
+    "SA_OP_SELECT", "SA_OP_SCHEDULE", "library", "sparse_attn_version",
     "sparse_attn_status_str", "sparse_attn_keep_count", "sparse_attn_workspace_size",
-    "sparse_attn_select", "sparse_attn_fwd", "sparse_attn_quant_fp8", "sparse_attn_fwd_fp8",
-    "make_desc", "EXPORTED_SYMBOLS",
+    "sparse_attn_num_tiles", "sparse_attn_select", "sparse_attn_schedule", "sparse_attn_fwd",
+    "sparse_attn_quant_fp8", "sparse_attn_fwd_fp8", "make_desc", "EXPORTED_SYMBOLS",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsparseattn.so")
 
 SA_SELECT_ROW_TOPK = 0
 SA_SELECT_HEAD_TOPK = 1
-SA_OP_SELECT, SA_OP_FWD, SA_OP_FWD_FP8 = 0, 1, 2
+SA_OP_SELECT, SA_OP_SCHEDULE = 0, 1
 
 EXPORTED_SYMBOLS = (
     "sparse_attn_version", "sparse_attn_status_str", "sparse_attn_keep_count",
-    "sparse_attn_workspace_size", "sparse_attn_select", "sparse_attn_fwd",
-    "sparse_attn_quant_fp8", "sparse_attn_fwd_fp8",
+    "sparse_attn_workspace_size", "sparse_attn_num_tiles", "sparse_attn_select",
+    "sparse_attn_schedule", "sparse_attn_fwd", "sparse_attn_quant_fp8", "sparse_attn_fwd_fp8",
 )
 
 
@@ -69,15 +69,17 @@ def library() -> ctypes.CDLL:
             "sparse_attn_status_str": (ctypes.c_char_p, [ctypes.c_int]),
             "sparse_attn_keep_count": (ctypes.c_int32, [ctypes.c_int32, ctypes.c_int32]),
             "sparse_attn_workspace_size": (ctypes.c_size_t, [D, ctypes.c_int32, ctypes.c_int32]),
+            "sparse_attn_num_tiles": (ctypes.c_int64, [D]),
             "sparse_attn_select": (ctypes.c_int, [D, _P, _P, ctypes.c_int32, ctypes.c_int64,
                                                   _P, _P, ctypes.c_int32, _P, ctypes.c_size_t, _P]),
-            "sparse_attn_fwd": (ctypes.c_int, [D, _P, _P, _P, _P, _P, ctypes.c_int32, _P, _P,
-                                               _P, ctypes.c_size_t, _P]),
+            "sparse_attn_schedule": (ctypes.c_int, [D, _P, ctypes.c_int32, _P, _P,
+                                                    ctypes.c_size_t, _P]),
+            "sparse_attn_fwd": (ctypes.c_int, [D, _P, _P, _P, _P, _P, ctypes.c_int32, _P, _P, _P,
+                                               _P]),
             "sparse_attn_quant_fp8": (ctypes.c_int, [D, _P, ctypes.POINTER(ctypes.c_int64),
                                                      _P, _P, _P]),
             "sparse_attn_fwd_fp8": (ctypes.c_int, [D, _P, _P, _P, _P, _P, _P, _P, _P,
-                                                   ctypes.c_int32, _P, _P, _P, ctypes.c_size_t,
-                                                   _P]),
+                                                   ctypes.c_int32, _P, _P, _P, _P]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(lib, name)
@@ -114,6 +116,13 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None else None
 
 
+def _dense(t, name, dtype=torch.int32):
+    """Index lists, counts and launch orders are dense C arrays at the ABI."""
+    if t is not None and (not t.is_contiguous() or t.dtype != dtype):
+        raise ValueError(f"{name} must be a contiguous {dtype} tensor")
+    return t
+
+
 def _check(status, what):
     if status != 0:
         raise SparseAttnError(status, what)
@@ -140,6 +149,10 @@ def sparse_attn_workspace_size(desc: SparseAttnDesc, op: int, kmax: int = 1) -> 
     return library().sparse_attn_workspace_size(ctypes.byref(desc), op, kmax)
 
 
+def sparse_attn_num_tiles(desc: SparseAttnDesc) -> int:
+    return library().sparse_attn_num_tiles(ctypes.byref(desc))
+
+
 def _workspace(desc, op, kmax, device):
     n = sparse_attn_workspace_size(desc, op, kmax)
     if n == 0:
@@ -160,6 +173,7 @@ def sparse_attn_select(q, k, budget: int, block: int = 64, mode: int = SA_SELECT
         idx = torch.empty(B, H, nb, kmax, dtype=torch.int32, device=q.device)
     if cnt is None:
         cnt = torch.empty(B, H, nb, dtype=torch.int32, device=q.device)
+    _dense(idx, "idx"), _dense(cnt, "cnt")
     if ws is None:
         ws = _workspace(desc, SA_OP_SELECT, kmax, q.device)
     st = library().sparse_attn_select(ctypes.byref(desc), _ptr(q), _ptr(k), mode, budget,
@@ -169,23 +183,44 @@ def sparse_attn_select(q, k, budget: int, block: int = 64, mode: int = SA_SELECT
     return idx, cnt
 
 
+def sparse_attn_schedule(cnt, seqlen: int, kmax: int, block: int = 64, order=None, ws=None):
+    """Launch order of the 64-row query tiles for the lists' lengths ``cnt``
+    [B, H, nb].  Returns int32 [B * H * ceil(seqlen / 64)]."""
+    B, H, _ = cnt.shape
+    _dense(cnt, "cnt")
+    _dense(order, "order")
+    desc = SparseAttnDesc()
+    desc.batch, desc.heads, desc.seqlen, desc.head_dim, desc.block = B, H, seqlen, 128, block
+    n = sparse_attn_num_tiles(desc)
+    if n < 0:
+        raise SparseAttnError(-2, "sparse_attn_num_tiles")
+    if order is None:
+        order = torch.empty(n, dtype=torch.int32, device=cnt.device)
+    if ws is None:
+        ws = _workspace(desc, SA_OP_SCHEDULE, kmax, cnt.device)
+    st = library().sparse_attn_schedule(ctypes.byref(desc), _ptr(cnt), kmax, _ptr(order),
+                                        _ptr(ws), ws.numel(), _stream(cnt))
+    _check(st, "sparse_attn_schedule")
+    return order
+
+
 def sparse_attn_fwd(q, k, v, idx, cnt, block: int = 64, softmax_scale: float = 0.0,
-                    with_lse: bool = True, o=None, lse=None, ws=None):
+                    with_lse: bool = True, order=None, o=None, lse=None):
     """Block-sparse attention forward on bf16 q, k, v [B, H, N, 128] with the
-    lists from sparse_attn_select.  Returns (o bf16 [B, H, N, 128], lse fp32
+    lists from sparse_attn_select (and optionally the launch order from
+    sparse_attn_schedule).  Returns (o bf16 [B, H, N, 128], lse fp32
     [B, H, N] or None)."""
     B, H, N, _ = q.shape
     kmax = idx.shape[-1]
+    _dense(idx, "idx"), _dense(cnt, "cnt"), _dense(order, "order")
     if o is None:
         o = torch.empty_like(q, memory_format=torch.contiguous_format)
     if with_lse and lse is None:
         lse = torch.empty(B, H, N, dtype=torch.float32, device=q.device)
     desc = make_desc(q, k, v, o, block=block, softmax_scale=softmax_scale)
-    if ws is None:
-        ws = _workspace(desc, SA_OP_FWD, kmax, q.device)
     st = library().sparse_attn_fwd(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(idx),
-                                   _ptr(cnt), kmax, _ptr(o), _ptr(lse if with_lse else None),
-                                   _ptr(ws), ws.numel(), _stream(q))
+                                   _ptr(cnt), kmax, _ptr(order), _ptr(o),
+                                   _ptr(lse if with_lse else None), _stream(q))
     _check(st, "sparse_attn_fwd")
     return o, (lse if with_lse else None)
 
@@ -207,23 +242,26 @@ def sparse_attn_quant_fp8(x, block: int = 64, x8=None, scale=None):
 
 
 def sparse_attn_fwd_fp8(q8, sq, k8, sk, v8, sv, idx, cnt, block: int = 64,
-                        softmax_scale: float = 0.0, with_lse: bool = True, o=None, lse=None,
-                        ws=None):
+                        softmax_scale: float = 0.0, with_lse: bool = True, order=None, o=None,
+                        lse=None):
     """Block-sparse attention forward on e4m3 operands from
     sparse_attn_quant_fp8.  Returns (o bf16 [B, H, N, 128], lse or None)."""
     B, H, N, d = q8.shape
     kmax = idx.shape[-1]
+    _dense(idx, "idx"), _dense(cnt, "cnt"), _dense(order, "order")
+    for name, t in (("q8", q8), ("k8", k8), ("v8", v8)):
+        _dense(t, name, torch.uint8)
+    for name, t in (("sq", sq), ("sk", sk), ("sv", sv)):
+        _dense(t, name, torch.float32)
     if o is None:
         o = torch.empty(B, H, N, d, dtype=torch.bfloat16, device=q8.device)
     if with_lse and lse is None:
         lse = torch.empty(B, H, N, dtype=torch.float32, device=q8.device)
     desc = make_desc(o, o=o, block=block, softmax_scale=softmax_scale)
-    if ws is None:
-        ws = _workspace(desc, SA_OP_FWD_FP8, kmax, q8.device)
     st = library().sparse_attn_fwd_fp8(ctypes.byref(desc), _ptr(q8), _ptr(sq), _ptr(k8),
                                        _ptr(sk), _ptr(v8), _ptr(sv), _ptr(idx), _ptr(cnt), kmax,
-                                       _ptr(o), _ptr(lse if with_lse else None), _ptr(ws),
-                                       ws.numel(), _stream(q8))
+                                       _ptr(order), _ptr(o), _ptr(lse if with_lse else None),
+                                       _stream(q8))
     _check(st, "sparse_attn_fwd_fp8")
     return o, (lse if with_lse else None)
 

@@ -47,8 +47,6 @@ float effective_scale(const sparse_attn_desc* d) {
 
 int launch_status(hipError_t e) { return e == hipSuccess ? SA_OK : SA_ERR_LAUNCH; }
 
-size_t fwd_workspace(const Shape& s) { return sa::schedule_workspace_bytes(s); }
-
 int check_lists(const Shape& s, const int32_t* idx, const int32_t* cnt, int32_t kmax) {
   if (!idx || !cnt) return SA_ERR_INVALID_ARG;
   if (kmax < 1 || kmax > (1 << 16)) return SA_ERR_INVALID_ARG;
@@ -84,10 +82,27 @@ size_t sparse_attn_workspace_size(const sparse_attn_desc* desc, int32_t op, int3
   if (check_desc(desc, &s) != SA_OK) return 0;
   switch (op) {
     case SA_OP_SELECT: return sa::select_workspace_bytes(s);
-    case SA_OP_FWD:
-    case SA_OP_FWD_FP8: return kmax >= 1 ? fwd_workspace(s) : 0;
+    case SA_OP_SCHEDULE: return kmax >= 1 ? sa::schedule_workspace_bytes(s) : 0;
     default: return 0;
   }
+}
+
+int64_t sparse_attn_num_tiles(const sparse_attn_desc* desc) {
+  Shape s;
+  if (check_desc(desc, &s) != SA_OK) return -1;
+  return sa::num_query_tiles(s);
+}
+
+int sparse_attn_schedule(const sparse_attn_desc* desc, const int32_t* cnt, int32_t kmax,
+                         int32_t* order, void* ws, size_t ws_bytes, void* stream) {
+  Shape s;
+  int st = check_desc(desc, &s);
+  if (st != SA_OK) return st;
+  if (!order || !ws) return SA_ERR_INVALID_ARG;
+  if ((st = check_lists(s, cnt, cnt, kmax)) != SA_OK) return st;
+  if (ws_bytes < sa::schedule_workspace_bytes(s)) return SA_ERR_WORKSPACE;
+  return launch_status(
+      sa::launch_schedule(s, cnt, kmax, order, ws, static_cast<hipStream_t>(stream)));
 }
 
 int sparse_attn_select(const sparse_attn_desc* desc, const void* q, const void* k, int32_t mode,
@@ -120,19 +135,17 @@ int sparse_attn_select(const sparse_attn_desc* desc, const void* q, const void* 
 }
 
 int sparse_attn_fwd(const sparse_attn_desc* desc, const void* q, const void* k, const void* v,
-                    const int32_t* idx, const int32_t* cnt, int32_t kmax, void* o, float* lse,
-                    void* ws, size_t ws_bytes, void* stream) {
+                    const int32_t* idx, const int32_t* cnt, int32_t kmax, const int32_t* order,
+                    void* o, float* lse, void* stream) {
   Shape s;
   int st = check_desc(desc, &s);
   if (st != SA_OK) return st;
-  if (!q || !k || !v || !o || !ws) return SA_ERR_INVALID_ARG;
+  if (!q || !k || !v || !o) return SA_ERR_INVALID_ARG;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return SA_ERR_INVALID_ARG;
   if (!strides_ok(desc->q_stride) || !strides_ok(desc->k_stride) ||
       !strides_ok(desc->v_stride) || !strides_ok(desc->o_stride))
     return SA_ERR_INVALID_ARG;
   if ((st = check_lists(s, idx, cnt, kmax)) != SA_OK) return st;
-  if (ws_bytes < fwd_workspace(s)) return SA_ERR_WORKSPACE;
-  hipStream_t hs = static_cast<hipStream_t>(stream);
   sa::FwdArgs a{};
   a.q = q;
   a.k = k;
@@ -145,11 +158,10 @@ int sparse_attn_fwd(const sparse_attn_desc* desc, const void* q, const void* k, 
   a.os = to_strides(desc->o_stride);
   a.idx = idx;
   a.cnt = cnt;
+  a.order = order;
   a.kmax = kmax;
   a.softmax_scale = effective_scale(desc);
-  hipError_t e = sa::launch_schedule(s, cnt, kmax, ws, &a.order, hs);
-  if (e != hipSuccess) return SA_ERR_LAUNCH;
-  return launch_status(sa::launch_fwd_bf16(s, a, hs));
+  return launch_status(sa::launch_fwd_bf16(s, a, static_cast<hipStream_t>(stream)));
 }
 
 int sparse_attn_quant_fp8(const sparse_attn_desc* desc, const void* x, const int64_t x_stride[3],
@@ -165,18 +177,16 @@ int sparse_attn_quant_fp8(const sparse_attn_desc* desc, const void* x, const int
 
 int sparse_attn_fwd_fp8(const sparse_attn_desc* desc, const uint8_t* q8, const float* sq,
                         const uint8_t* k8, const float* sk, const uint8_t* v8, const float* sv,
-                        const int32_t* idx, const int32_t* cnt, int32_t kmax, void* o, float* lse,
-                        void* ws, size_t ws_bytes, void* stream) {
+                        const int32_t* idx, const int32_t* cnt, int32_t kmax,
+                        const int32_t* order, void* o, float* lse, void* stream) {
   Shape s;
   int st = check_desc(desc, &s);
   if (st != SA_OK) return st;
-  if (!q8 || !sq || !k8 || !sk || !v8 || !sv || !o || !ws) return SA_ERR_INVALID_ARG;
+  if (!q8 || !sq || !k8 || !sk || !v8 || !sv || !o) return SA_ERR_INVALID_ARG;
   if (!aligned16(q8) || !aligned16(k8) || !aligned16(v8) || !aligned16(o))
     return SA_ERR_INVALID_ARG;
   if (!strides_ok(desc->o_stride)) return SA_ERR_INVALID_ARG;
   if ((st = check_lists(s, idx, cnt, kmax)) != SA_OK) return st;
-  if (ws_bytes < fwd_workspace(s)) return SA_ERR_WORKSPACE;
-  hipStream_t hs = static_cast<hipStream_t>(stream);
   const int64_t tok = 128, head = (int64_t)s.N * tok, bat = head * s.H;
   sa::FwdArgs a{};
   a.q = q8;
@@ -191,11 +201,10 @@ int sparse_attn_fwd_fp8(const sparse_attn_desc* desc, const uint8_t* q8, const f
   a.sq = sq;
   a.sk = sk;
   a.sv = sv;
+  a.order = order;
   a.kmax = kmax;
   a.softmax_scale = effective_scale(desc);
-  hipError_t e = sa::launch_schedule(s, cnt, kmax, ws, &a.order, hs);
-  if (e != hipSuccess) return SA_ERR_LAUNCH;
-  return launch_status(sa::launch_fwd_fp8(s, a, hs));
+  return launch_status(sa::launch_fwd_fp8(s, a, static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

@@ -29,10 +29,10 @@ hipError_t launch_select_head(const Shape& s, const void* q, Strides qs, const v
 
 // ---- scheduling ----------------------------------------------------------
 size_t schedule_workspace_bytes(const Shape& s);
-// Writes the 64-row query tiles in launch order into the workspace and
-// returns a pointer to that list (int32 [B*H*ceil(N/64)]).
-hipError_t launch_schedule(const Shape& s, const int32_t* cnt, int kmax, void* ws,
-                           const int32_t** order, hipStream_t stream);
+int64_t num_query_tiles(const Shape& s);
+// Writes the launch order of the 64-row query tiles (int32 [B*H*ceil(N/64)]).
+hipError_t launch_schedule(const Shape& s, const int32_t* cnt, int kmax, int32_t* order,
+                           void* ws, hipStream_t stream);
 
 // ---- forward -------------------------------------------------------------
 struct FwdArgs {

@@ -101,20 +101,21 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* 
 
 }  // namespace
 
-size_t schedule_workspace_bytes(const Shape& s) {
-  const size_t G = (size_t)s.B * s.H * ((s.N + kTile - 1) / kTile);
-  return 2 * G * sizeof(int32_t) + 256;
+int64_t num_query_tiles(const Shape& s) {
+  return (int64_t)s.B * s.H * ((s.N + kTile - 1) / kTile);
 }
 
-hipError_t launch_schedule(const Shape& s, const int32_t* cnt, int kmax, void* ws,
-                           const int32_t** order, hipStream_t stream) {
+size_t schedule_workspace_bytes(const Shape& s) {
+  return (size_t)num_query_tiles(s) * sizeof(int32_t);
+}
+
+hipError_t launch_schedule(const Shape& s, const int32_t* cnt, int kmax, int32_t* order,
+                           void* ws, hipStream_t stream) {
   const int ntiles = (s.N + kTile - 1) / kTile;
-  const int G = s.B * s.H * ntiles;
+  const int G = (int)num_query_tiles(s);
   int32_t* list = static_cast<int32_t*>(ws);
-  int32_t* ord = list + G;
   schedule_kernel<<<1, kSchedThreads, 0, stream>>>(cnt, kmax, s.nb, ntiles, s.block, G, list,
-                                                   ord);
-  *order = ord;
+                                                   order);
   return hipGetLastError();
 }
 

@@ -61,7 +61,7 @@ def test_workspace_size_formula():
     nb = 1182
     assert lib.sparse_attn_workspace_size(ctypes.byref(ds), 0, 36) == \
         40 * nb * 128 * 8 * 2 + 40 * nb * nb * 8
-    assert lib.sparse_attn_workspace_size(ctypes.byref(ds), 1, 36) > 0
+    assert lib.sparse_attn_workspace_size(ctypes.byref(ds), 1, 36) == 40 * 1182 * 4
     assert lib.sparse_attn_workspace_size(ctypes.byref(ds), 1, 0) == 0
     assert lib.sparse_attn_workspace_size(ctypes.byref(ds), 7, 36) == 0
     assert lib.sparse_attn_workspace_size(ctypes.byref(desc(d=64)), 0, 1) == 0
@@ -109,14 +109,30 @@ def test_fwd_rejects_bad_arguments():
     lib = sa.library()
     ds = desc()
     call = lambda *a: lib.sparse_attn_fwd(ctypes.byref(ds), *a)
-    assert call(None, P, P, P, P, 7, P, None, P, WS, None) == -1    # null q
-    assert call(P, P, P, None, P, 7, P, None, P, WS, None) == -1    # null idx
-    assert call(P, P, P, P, None, 7, P, None, P, WS, None) == -1    # null cnt
-    assert call(P, P, P, P, P, 0, P, None, P, WS, None) == -1       # kmax 0
-    assert call(P, P, P, P, P, 7, MIS, None, P, WS, None) == -1     # misaligned o
-    assert call(P, P, P, P, P, 7, P, None, P, 8, None) == -3        # workspace
+    assert call(None, P, P, P, P, 7, None, P, None, None) == -1     # null q
+    assert call(P, P, P, None, P, 7, None, P, None, None) == -1     # null idx
+    assert call(P, P, P, P, None, 7, None, P, None, None) == -1     # null cnt
+    assert call(P, P, P, P, P, 0, None, P, None, None) == -1        # kmax 0
+    assert call(P, P, P, P, P, 7, None, MIS, None, None) == -1      # misaligned o
+    assert call(P, P, P, P, P, 7, None, None, None, None) == -1     # null o
+    ds.v_stride[1] = 12                                              # stride not multiple of 8
+    assert call(P, P, P, P, P, 7, None, P, None, None) == -1
     ds.head_dim = 96
-    assert call(P, P, P, P, P, 7, P, None, P, WS, None) == -2
+    assert call(P, P, P, P, P, 7, None, P, None, None) == -2
+
+
+def test_schedule_rejects_bad_arguments():
+    lib = sa.library()
+    ds = desc(B=2, H=3, N=1000)
+    assert lib.sparse_attn_num_tiles(ctypes.byref(ds)) == 2 * 3 * 16
+    assert lib.sparse_attn_num_tiles(ctypes.byref(desc(block=96))) == -1
+    need = lib.sparse_attn_workspace_size(ctypes.byref(ds), 1, 7)
+    assert need == 2 * 3 * 16 * 4
+    call = lambda *a: lib.sparse_attn_schedule(ctypes.byref(ds), *a)
+    assert call(None, 7, P, P, need, None) == -1                    # null cnt
+    assert call(P, 7, None, P, need, None) == -1                    # null order
+    assert call(P, 0, P, P, need, None) == -1                       # kmax 0
+    assert call(P, 7, P, P, need - 1, None) == -3                   # workspace
 
 
 def test_quant_and_fwd_fp8_reject_bad_arguments():
@@ -129,6 +145,7 @@ def test_quant_and_fwd_fp8_reject_bad_arguments():
     bad = (ctypes.c_int64 * 3)(2 * 4096 * 128, 4096 * 128, 129)
     assert lib.sparse_attn_quant_fp8(ctypes.byref(ds), P, bad, P, P, None) == -1
     f = lambda *a: lib.sparse_attn_fwd_fp8(ctypes.byref(ds), *a)
-    assert f(P, None, P, P, P, P, P, P, 7, P, None, P, WS, None) == -1   # null sq
-    assert f(P, P, P, P, P, P, P, P, 0, P, None, P, WS, None) == -1      # kmax 0
-    assert f(P, P, P, P, P, P, P, P, 7, P, None, P, 4, None) == -3       # workspace
+    assert f(P, None, P, P, P, P, P, P, 7, None, P, None, None) == -1    # null sq
+    assert f(P, P, P, P, P, P, P, P, 0, None, P, None, None) == -1       # kmax 0
+    assert f(P, P, P, P, P, P, None, P, 7, None, P, None, None) == -1    # null idx
+    assert f(P, P, MIS, P, P, P, P, P, 7, None, P, None, None) == -1     # misaligned k8

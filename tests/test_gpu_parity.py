@@ -9,6 +9,7 @@ import oracle as O
 import paper_2609_23153_amd as sa
 import workloads as W
 from gpu_helpers import check_out, oracle_attend, oracle_select, say, widen
+from oracle.schedule import launch_order
 
 pytestmark = pytest.mark.gpu
 
@@ -100,9 +101,15 @@ def test_select_kmax_padding():
 
 
 # --------------------------------------------------------------------- fwd
-def fwd_and_check(q, k, v, idx, cnt, block, what, qblocks=None, heads=None):
+def fwd_and_check(q, k, v, idx, cnt, block, what, qblocks=None, heads=None, schedule=True):
     qd, kd, vd = to_dev(q, k, v)
-    o, lse = sa.sparse_attn_fwd(qd, kd, vd, idx, cnt, block=block)
+    order = None
+    if schedule:
+        order = sa.sparse_attn_schedule(cnt, q.shape[2], idx.shape[-1], block=block)
+        torch.cuda.synchronize()
+        ref = launch_order(cnt.cpu().numpy(), idx.shape[-1], q.shape[2], block)
+        assert np.array_equal(order.cpu().numpy(), ref), what
+    o, lse = sa.sparse_attn_fwd(qd, kd, vd, idx, cnt, block=block, order=order)
     torch.cuda.synchronize()
     o, lse = o.cpu(), lse.cpu()
     idx_c, cnt_c = idx.cpu().numpy(), cnt.cpu().numpy()
@@ -119,11 +126,30 @@ def fwd_and_check(q, k, v, idx, cnt, block, what, qblocks=None, heads=None):
     return o, lse
 
 
-def test_fwd_tiny():
+@pytest.mark.parametrize("schedule", [True, False])
+def test_fwd_tiny(schedule):
     wl = W.WORKLOADS["tiny"]
     q, k, v = W.make_inputs(wl)
     idx, cnt = select_and_check(q, k, wl.block, wl.keep_bp, "tiny")
-    fwd_and_check(q, k, v, idx, cnt, wl.block, "tiny fwd")
+    fwd_and_check(q, k, v, idx, cnt, wl.block, "tiny fwd", schedule=schedule)
+
+
+def test_schedule_large_ragged_matches_definition():
+    # 3 x 40 heads x 1182 blocks of ragged lengths: several XCD groups and a
+    # partial tail group
+    rng = np.random.default_rng(21)
+    cnt = rng.integers(0, 300, size=(3, 40, 1182)).astype(np.int32)
+    cnt[0, 0, :50] = 0
+    cntd = torch.from_numpy(cnt).to(DEV)
+    order = sa.sparse_attn_schedule(cntd, 75600, 250, block=64)
+    torch.cuda.synchronize()
+    ref = launch_order(cnt, 250, 75600, 64)
+    assert np.array_equal(order.cpu().numpy(), ref)
+    order = sa.sparse_attn_schedule(cntd[:, :, :591].contiguous(), 75600, 250, block=128)
+    with pytest.raises(ValueError):
+        sa.sparse_attn_schedule(cntd[:, :, :591], 75600, 250, block=128)
+    torch.cuda.synchronize()
+    assert np.array_equal(order.cpu().numpy(), launch_order(cnt[:, :, :591], 250, 75600, 128))
 
 
 def test_fwd_wan13b_sampled_heads():
@@ -202,7 +228,8 @@ def test_wan14b_full_size_sampled():
     nb = O.block_count(wl.seqlen, wl.block)
     kk = O.keep_count(wl.keep_bp, nb)
     idx, cnt = sa.sparse_attn_select(qd, kd, kk)
-    o, lse = sa.sparse_attn_fwd(qd, kd, vd, idx, cnt)
+    order = sa.sparse_attn_schedule(cnt, wl.seqlen, kk)
+    o, lse = sa.sparse_attn_fwd(qd, kd, vd, idx, cnt, order=order)
     torch.cuda.synchronize()
     idx_c, cnt_c = idx.cpu().numpy(), cnt.cpu().numpy()
     rng = np.random.default_rng(14)

@@ -352,3 +352,22 @@ def test_widen_bf16_matches_library():
     x = torch.randn(1000).to(torch.bfloat16)
     np.testing.assert_array_equal(O.widen_bf16(x.view(torch.int16).numpy().view(np.uint16)),
                                   x.to(torch.float64).numpy())
+
+
+def test_launch_order_definition_small_cases():
+    from oracle.schedule import launch_order
+    # uniform lists and fewer tiles than one XCD group: identity order
+    cnt = np.full((1, 2, 10), 3)
+    assert launch_order(cnt, 3, 640, 64).tolist() == list(range(20))
+    # ragged: costlier tiles first, raster order within a class
+    cnt = np.array([[[1, 4, 0, 2]]])
+    # classes: cost 1 -> 1, 4 -> 3, 0 -> 0, 2 -> 2
+    assert launch_order(cnt, 9, 256, 64).tolist() == [1, 3, 0, 2]
+    # block 128: one list per two 64-row tiles, cost doubled; cnt clamped to kmax
+    cnt = np.array([[[5, 1]]])
+    assert launch_order(cnt, 2, 256, 128).tolist() == [0, 1, 2, 3]
+    # XCD interleave over one full group of 512 uniform tiles
+    cnt = np.full((1, 1, 512), 1)
+    o = launch_order(cnt, 1, 512 * 64, 64)
+    assert sorted(o.tolist()) == list(range(512))
+    assert o[:9].tolist() == [0, 64, 128, 192, 256, 320, 384, 448, 1]
