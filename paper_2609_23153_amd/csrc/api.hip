@@ -41,6 +41,12 @@ int check_desc(const sparse_attn_desc* d, Shape* s) {
 
 Strides to_strides(const int64_t st[3]) { return Strides{st[0], st[1], st[2]}; }
 
+// The kernels address one head's rows with 32-bit byte offsets, up to the
+// last row of the last (padded) 64-token tile.
+bool offsets_fit(const Shape& s, const int64_t st[3], int elem_bytes) {
+  return ((int64_t)s.N + 64) * st[2] * elem_bytes + 256 < ((int64_t)1 << 32);
+}
+
 float effective_scale(const sparse_attn_desc* d) {
   return d->softmax_scale > 0.f ? d->softmax_scale : (float)(1.0 / sqrt((double)d->head_dim));
 }
@@ -146,6 +152,9 @@ int sparse_attn_fwd(const sparse_attn_desc* desc, const void* q, const void* k, 
       !strides_ok(desc->v_stride) || !strides_ok(desc->o_stride))
     return SA_ERR_INVALID_ARG;
   if ((st = check_lists(s, idx, cnt, kmax)) != SA_OK) return st;
+  if (!offsets_fit(s, desc->q_stride, 2) || !offsets_fit(s, desc->k_stride, 2) ||
+      !offsets_fit(s, desc->v_stride, 2))
+    return SA_ERR_UNSUPPORTED;
   sa::FwdArgs a{};
   a.q = q;
   a.k = k;

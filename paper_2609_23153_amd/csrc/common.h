@@ -17,6 +17,24 @@ constexpr int kHeadDim = 128;   // d handled by every kernel
 constexpr int kWave = 64;       // CDNA wavefront width
 constexpr int kTile = 64;       // query rows / keys per fwd tile
 
+// Buffer resource over `bytes` bytes from `base`: loads at offsets past the
+// end return zero (the hardware range check), without branches.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                           0x00020000);
+}
+__device__ __forceinline__ u32x4 buf_ld16(__amdgpu_buffer_rsrc_t r, uint32_t off,
+                                          uint32_t soff = 0) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, soff, 0));
+}
+
+// max of x over the lane pair (l, l ^ 32), through v_permlane32_swap.
+__device__ __forceinline__ float pair_max32(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto sw = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+}
+
 // 16-byte global load / store (dwordx4) of raw bits.
 __device__ __forceinline__ u32x4 ld16(const void* p) {
   return *reinterpret_cast<const u32x4*>(p);

@@ -4,16 +4,21 @@
 // Eq. comp-sparse, §4.1): exact softmax attention of each 64-row query tile
 // over the union of the key blocks its query block selected.
 //
-// One workgroup = 4 wavefronts = one 64-row query tile.  Every selected key
-// block is walked as 64-key tiles that are staged in LDS (double-buffered,
-// K row-major, V transposed so that the PV product reads keys contiguously).
-// Wave w owns query rows 32*(w&1)..+31 and keys 32*(w>>1)..+31 of every tile:
-//   S^T (32 keys x 32 queries) = K_half . Q_half^T  -- 8 x v_mfma_f32_32x32x16_bf16
-//   online softmax in fp32 registers (exp2 with tau*log2(e) folded in)
-//   O^T (128 x 32)          += V_half^T . P^T       -- 8 x v_mfma_f32_32x32x16_bf16
-// Computing S transposed puts all 16 scores of a lane in one query column,
-// so the row statistics are per-lane scalars and the probabilities already
-// sit in the B-operand layout of the PV product (no LDS round trip for P).
+// One workgroup = 4 wavefronts = one 64-row query tile; two workgroups share
+// a CU.  Every selected key block is walked as 64-key tiles:
+//  * K and V tiles go straight from HBM/L2 into LDS with buffer_load ... lds
+//    (no staging registers, no VALU), double-buffered, rows past the sequence
+//    end reading zero through the buffer range check.  Both tiles are stored
+//    row-major with a 16-byte-chunk XOR swizzle chosen on the global side.
+//  * Wave w owns query rows 32*(w&1)..+31 and keys 32*(w>>1)..+31 of a tile:
+//      S^T (32 keys x 32 queries) = K_half . Q_half^T   8 x v_mfma_f32_32x32x16_bf16
+//      O^T (128 x 32)          += V_half^T . P^T       8 x v_mfma_f32_32x32x16_bf16
+//    Computing S transposed leaves all 16 scores of a lane in one query
+//    column: row statistics are per-lane scalars and the probabilities are
+//    already in the B-operand layout of the PV product.  The V^T A-operand is
+//    read from the row-major V tile with ds_read_b64_tr_b16.
+//  * Online softmax in fp32 registers with exp2 (tau*log2(e) folded into one
+//    FMA) and a lazily raised reference max.
 // The two key-half waves of a row-half keep separate softmax states that are
 // merged through LDS at the end.
 #include "common.h"
@@ -23,11 +28,19 @@ namespace sa {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kKRow = kHeadDim + 8;  // LDS K row stride (bf16): 272 B, 16-B aligned
-constexpr int kVRow = kTile + 4;     // LDS V^T row stride (bf16): 136 B, 8-B aligned
-constexpr int kKBuf = kTile * kKRow;
-constexpr int kVBuf = kHeadDim * kVRow;
-constexpr int kLdsElems = 2 * kKBuf + 2 * kVBuf;  // 69632 bytes
+constexpr int kRowBytes = kHeadDim * 2;            // 256 B per bf16 row
+constexpr int kTileBytes = kTile * kRowBytes;      // 16 KB per K or V tile
+constexpr int kBufBytes = 2 * kTileBytes;          // K + V: 32 KB, two such buffers
+constexpr float kLazy = 8.f;  // log2 headroom before the accumulator is rescaled
+
+// 16-byte-chunk swizzles (row = row within the tile): conflict-free for the
+// K A-operand reads (32 rows, one chunk) and the V transpose reads (4 rows x
+// 4 chunks per half-wave).
+__device__ __forceinline__ int swz_k(int row, int chunk) { return chunk ^ (row & 15); }
+__device__ __forceinline__ int swz_v(int row, int chunk) { return chunk ^ ((row & 3) << 2); }
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((__vector_size__(4 * sizeof(short)))) short i16x4;
 
 struct Params {
   const uint16_t* q;
@@ -66,61 +79,58 @@ __device__ __forceinline__ int next_tile(const int32_t* list, int n, int total, 
   return total;
 }
 
-struct TileRegs {
-  u32x4 k[4];
-  u32x4 v[4];
+// Per-lane global byte offsets (loop invariant) of the 16-byte chunks this
+// lane moves into LDS: wave w, instruction i covers tile rows 16w+4i .. +3,
+// lane l writes LDS chunk slot l%16 of row 16w+4i+l/16 and so fetches the
+// logical chunk that the swizzle places there.
+struct DmaOffsets {
+  uint32_t k[4];
+  uint32_t v[4];
 };
 
-// Global -> registers for one 64-key tile; rows past N read as zero.
-__device__ __forceinline__ void load_tile(TileRegs& r, const uint16_t* kb, const uint16_t* vb,
-                                          const Params& p, int start) {
-  const int t = threadIdx.x;
-  const int chunk = t & 15;
-  const u32x4 zero = {0u, 0u, 0u, 0u};
+__device__ __forceinline__ DmaOffsets dma_offsets(uint32_t kst, uint32_t vst) {
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  DmaOffsets o;
 #pragma unroll
-  for (int m = 0; m < 4; ++m) {
-    const int row = start + (t >> 4) + 16 * m;
-    r.k[m] = row < p.N ? ld16(kb + (int64_t)row * p.ks.n + chunk * 8) : zero;
+  for (int i = 0; i < 4; ++i) {
+    const int row = 16 * w + 4 * i + (l >> 4);
+    o.k[i] = (uint32_t)row * kst + (uint32_t)swz_k(row, l & 15) * 16u;
+    o.v[i] = (uint32_t)row * vst + (uint32_t)swz_v(row, l & 15) * 16u;
   }
-  const int kq = t >> 4;
-#pragma unroll
-  for (int m = 0; m < 4; ++m) {
-    const int row = start + 4 * kq + m;
-    r.v[m] = row < p.N ? ld16(vb + (int64_t)row * p.vs.n + chunk * 8) : zero;
-  }
+  return o;
 }
 
-// Registers -> LDS buffer: K row-major, V transposed (4-key chunks per d row).
-__device__ __forceinline__ void store_tile(const TileRegs& r, uint16_t* ks, uint16_t* vt) {
-  const int t = threadIdx.x;
-  const int chunk = t & 15;
+// Issue the global -> LDS copies of one K/V tile into the buffer `dst`.
+// Completion is tracked by vmcnt.
+__device__ __forceinline__ void dma_tile(uint8_t* dst, __amdgpu_buffer_rsrc_t kr,
+                                         __amdgpu_buffer_rsrc_t vr, const DmaOffsets& o,
+                                         uint32_t ksoff, uint32_t vsoff) {
+  const int w = threadIdx.x >> 6;
+  uint8_t* kb = dst + (16 * w) * kRowBytes;
+  uint8_t* vb = kb + kTileBytes;
 #pragma unroll
-  for (int m = 0; m < 4; ++m) {
-    const int row = (t >> 4) + 16 * m;
-    st16(ks + row * kKRow + chunk * 8, r.k[m]);
-  }
-  const int kq = t >> 4;
+  for (int i = 0; i < 4; ++i)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_void*)(kb + 4 * i * kRowBytes), 16, o.k[i],
+                                             ksoff, 0, 0);
 #pragma unroll
-  for (int x = 0; x < 4; ++x) {
-    // even channel d = 8*chunk + 2x (low halves), odd channel d + 1 (high halves)
-    u32x2 ev, od;
-    ev[0] = (r.v[0][x] & 0xffffu) | (r.v[1][x] << 16);
-    ev[1] = (r.v[2][x] & 0xffffu) | (r.v[3][x] << 16);
-    od[0] = (r.v[0][x] >> 16) | (r.v[1][x] & 0xffff0000u);
-    od[1] = (r.v[2][x] >> 16) | (r.v[3][x] & 0xffff0000u);
-    const int d = chunk * 8 + 2 * x;
-    *reinterpret_cast<u32x2*>(vt + d * kVRow + kq * 4) = ev;
-    *reinterpret_cast<u32x2*>(vt + (d + 1) * kVRow + kq * 4) = od;
-  }
+  for (int i = 0; i < 4; ++i)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_void*)(vb + 4 * i * kRowBytes), 16, o.v[i],
+                                             vsoff, 0, 0);
+}
+
+__device__ __forceinline__ void wait_dma() {
+  // vmcnt(0); expcnt and lgkmcnt left at their maxima (no wait).
+  __builtin_amdgcn_s_waitcnt(0x0F70);
 }
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
 __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
-  __shared__ __attribute__((aligned(16))) uint16_t lds[kLdsElems];
-  // buffer x: K at lds + x * kKBuf, V^T at lds + 2 * kKBuf + x * kVBuf
-  auto ks_buf = [&](int x) { return lds + x * kKBuf; };
-  auto vt_buf = [&](int x) { return lds + 2 * kKBuf + x * kVBuf; };
+  // Two distinct LDS objects (rather than one array indexed by a buffer
+  // number) let the compiler prove that the reads of one buffer do not alias
+  // the copies in flight into the other, so it does not wait for them.
+  __shared__ __attribute__((aligned(1024))) uint8_t lds0[kBufBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t lds1[kBufBytes];
 
   const int item = p.order ? p.order[blockIdx.x] : (int)blockIdx.x;
   const int bh = item / p.ntiles;
@@ -137,18 +147,24 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
   const int rh = wave & 1, kh = wave >> 1;
   const int g = lane >> 5, l32 = lane & 31;
 
-  const uint16_t* kbase = p.k + b * p.ks.b + h * p.ks.h;
-  const uint16_t* vbase = p.v + b * p.vs.b + h * p.vs.h;
+  // Per-head buffer resources covering rows [0, N): rows past N read zero.
+  const uint32_t kst = (uint32_t)p.ks.n * 2, vst = (uint32_t)p.vs.n * 2, qst = (uint32_t)p.qs.n * 2;
+  const auto kr = make_rsrc(p.k + b * p.ks.b + h * p.ks.h, (uint32_t)(p.N - 1) * kst + 256u);
+  const auto vr = make_rsrc(p.v + b * p.vs.b + h * p.vs.h, (uint32_t)(p.N - 1) * vst + 256u);
+  const DmaOffsets dofs = dma_offsets(kst, vst);
+
+  int start = 0;
+  int n = next_tile(list, 0, total, spb, p.block, p.nb, p.N, &start);
+  if (n < total) dma_tile(lds0, kr, vr, dofs, (uint32_t)start * kst, (uint32_t)start * vst);
 
   // Q fragment (B operand of K.Q^T): query row l32 of this row-half,
   // channels 16*ks + 8*g .. +7.
   bf16x8 qf[8];
   {
-    const int row = q0 + rh * 32 + l32;
-    const uint16_t* qp = p.q + b * p.qs.b + h * p.qs.h + (int64_t)row * p.qs.n + g * 8;
-    const u32x4 zero = {0u, 0u, 0u, 0u};
+    const auto qr = make_rsrc(p.q + b * p.qs.b + h * p.qs.h, (uint32_t)(p.N - 1) * qst + 256u);
+    const uint32_t off = (uint32_t)(q0 + rh * 32 + l32) * qst + g * 16;
 #pragma unroll
-    for (int s = 0; s < 8; ++s) qf[s] = as_bf16x8(row < p.N ? ld16(qp + s * 16) : zero);
+    for (int s = 0; s < 8; ++s) qf[s] = as_bf16x8(buf_ld16(qr, off + s * 32));
   }
 
   f32x16 acc[4];
@@ -156,32 +172,46 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
   for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[dt][r] = 0.f;
-  float m2 = -INFINITY;  // running max of tau*log2(e)*logit for this lane's query
-  float lsum = 0.f;      // partial sum of exp2 over this lane's keys
+  // Reference max (log2 domain, tau*log2(e)*logit) of this lane's query: the
+  // accumulator holds sum 2^(x - m2) v.  It is raised only when a tile's max
+  // exceeds it by more than kLazy, so most tiles skip the rescale; the
+  // probabilities stay <= 2^kLazy.  Lanes l and l^32 share one query and one m2.
+  float m2 = -INFINITY;
+  float lsum = 0.f;  // partial sum of 2^(x - m2) over this lane's keys
 
-  int start = 0;
-  int n = next_tile(list, 0, total, spb, p.block, p.nb, p.N, &start);
-  TileRegs regs;
-  if (n < total) {
-    load_tile(regs, kbase, vbase, p, start);
-    store_tile(regs, ks_buf(0), vt_buf(0));
-  }
+  // LDS read addresses (bytes, relative to a buffer):
+  //  K A-operand: row kh*32 + l32, logical chunk 2*ks + g
+  //  V^T A-operand (transpose read): lane 16G + 4e + q supplies the 8-byte
+  //  chunk of key kh*32 + 16*cs + 8*hf + 4*(G>>1) + e at channels
+  //  32*dt + 16*(G&1) + 4*q .. +3; lane l then receives channel 32*dt + (l&31)
+  //  of keys kh*32 + 16*cs + 8*hf + 4*g + {0..3}.
+  const int krow = kh * 32 + l32;
+  const int G = lane >> 4, e4 = (lane >> 2) & 3, q4 = lane & 3;
+  const int vrow0 = kh * 32 + 4 * (G >> 1) + e4;  // + 16*cs + 8*hf (keeps row & 3)
+
+  wait_dma();
   __syncthreads();
 
-  int buf = 0;
-  while (n < total) {
-    int nstart = 0;
+  // One 64-key tile: compute from `cur` while the next tile streams into `nxt`.
+  auto step = [&](const uint8_t* cur, uint8_t* nxt) {
+    // Prefetch the next tile into the other buffer.  Past the last tile the
+    // start lies beyond the buffer range: the copies then read zeros without
+    // touching memory, and the loop body has no branches around in-flight loads.
+    int nstart = p.N;
     const int nn = next_tile(list, n + 1, total, spb, p.block, p.nb, p.N, &nstart);
-    if (nn < total) load_tile(regs, kbase, vbase, p, nstart);
+    dma_tile(nxt, kr, vr, dofs, (uint32_t)nstart * kst, (uint32_t)nstart * vst);
+
+    const uint8_t* kt = cur;
+    const uint8_t* vt = cur + kTileBytes;
 
     // ---- S^T = K_half . Q^T ------------------------------------------------
     f32x16 s;
 #pragma unroll
     for (int r = 0; r < 16; ++r) s[r] = 0.f;
-    const uint16_t* krow = ks_buf(buf) + (kh * 32 + l32) * kKRow + g * 8;
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) {
-      const bf16x8 kf = as_bf16x8(*reinterpret_cast<const u32x4*>(krow + ks * 16));
+      const bf16x8 kf = as_bf16x8(*reinterpret_cast<const u32x4*>(
+          kt + krow * kRowBytes + swz_k(krow, 2 * ks + g) * 16));
       s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s, 0, 0, 0);
     }
     // lane holds keys kh*32 + 8*(r>>2) + 4*g + (r&3) of query l32
@@ -197,26 +227,27 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
     float mx = s[0];
 #pragma unroll
     for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-    const float mnew = fmaxf(m2, mx * p.scale_log2);
-    const float msafe = mnew == -INFINITY ? 0.f : mnew;
-    const float alpha = __builtin_amdgcn_exp2f(m2 - msafe);
+    mx *= p.scale_log2;
+    if (__any(mx > m2 + kLazy)) {  // wave-uniform: raise the reference max
+      const float mnew = fmaxf(m2, pair_max32(mx));
+      const float alpha = __builtin_amdgcn_exp2f(m2 - (mnew == -INFINITY ? 0.f : mnew));
+      lsum *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[dt][r] *= alpha;
+      m2 = mnew;
+    }
+    const float msafe = m2 == -INFINITY ? 0.f : m2;
     float pv[16];
-    float psum = 0.f;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       pv[r] = __builtin_amdgcn_exp2f(fmaf(s[r], p.scale_log2, -msafe));
-      psum += pv[r];
+      lsum += pv[r];
     }
-    lsum = lsum * alpha + psum;
-    m2 = mnew;
-#pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[dt][r] *= alpha;
 
-    // P^T as B operand: k-step c uses registers 8c .. 8c+7 (keys
-    // 16c + 4g + {0..3} and 16c + 8 + 4g + {0..3} of the half).
+    // P^T as B operand: k-step cs uses registers 8cs .. 8cs+7 (keys
+    // 16cs + 4g + {0..3} and 16cs + 8 + 4g + {0..3} of the half).
     bf16x8 pk[2];
 #pragma unroll
     for (int cs = 0; cs < 2; ++cs)
@@ -224,29 +255,41 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
       for (int e = 0; e < 8; ++e) pk[cs][e] = (__bf16)pv[8 * cs + e];
 
     // ---- O^T += V_half^T . P^T -------------------------------------------
-    const uint16_t* vrow = vt_buf(buf) + l32 * kVRow + (kh * 8 + g) * 4;
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) {
+      const int lc = 4 * dt + 2 * (G & 1) + (q4 >> 1);  // logical 16-B chunk
+      const int half = (q4 & 1) * 8;
 #pragma unroll
       for (int cs = 0; cs < 2; ++cs) {
-        const uint16_t* vp = vrow + dt * 32 * kVRow + cs * 16;
-        const u32x2 lo = *reinterpret_cast<const u32x2*>(vp);
-        const u32x2 hi = *reinterpret_cast<const u32x2*>(vp + 8);
-        const u32x4 vv = {lo[0], lo[1], hi[0], hi[1]};
+        u32x4 vv;
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          const int row = vrow0 + 16 * cs + 8 * hf;
+          const i16x4 t = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) i16x4*)(vt + row * kRowBytes +
+                                                         swz_v(row, lc) * 16 + half));
+          const u32x2 tw = __builtin_bit_cast(u32x2, t);
+          vv[2 * hf] = tw[0];
+          vv[2 * hf + 1] = tw[1];
+        }
         acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv), pk[cs], acc[dt], 0, 0, 0);
       }
     }
 
-    if (nn < total) store_tile(regs, ks_buf(buf ^ 1), vt_buf(buf ^ 1));
+    wait_dma();
     __syncthreads();
-    buf ^= 1;
     n = nn;
     start = nstart;
+  };
+  while (n < total) {
+    step(lds0, lds1);
+    if (n >= total) break;
+    step(lds1, lds0);
   }
 
   // ---- merge the two key halves, normalise, store ------------------------
   lsum += __shfl_xor(lsum, 32, kWave);
-  float* mrg = reinterpret_cast<float*>(lds) + rh * (66 * kWave);
+  float* mrg = reinterpret_cast<float*>(rh ? lds1 : lds0);  // 66 x 64 floats per row-half
   if (kh == 1) {
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)

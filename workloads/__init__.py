@@ -12,11 +12,14 @@ t-major (x fastest), as a video DiT lays out its spatiotemporal tokens.
 Generators (recipes are stated in words in the design notes as well):
 
 ``normal``      Q, K, V ~ N(0, 1).
-``positional``  a smooth 3D positional signal shared by Q and K of one head,
-                P[n, c] = sum_{m<8} A[m, c] sin(w_m . (t, y, x)_n + phi[m, c]),
-                A ~ N(0, 1/8), each axis frequency of w_m ~ U[0, pi/4] rad per
-                grid step, phi ~ U[0, 2 pi); Q = P + 0.5 N(0,1), K = P + 0.5
-                N(0,1) (independent noise), V ~ N(0, 1).
+``positional``  a smooth 3D positional signal shared by Q and K of one head:
+                every channel is one random sinusoid over the grid,
+                P[n, c] = sqrt(2) sin(w_c . (t, y, x)_n + phi_c), with
+                w_c ~ N(0, 0.25^2 I) rad per grid step and phi_c ~ U[0, 2 pi),
+                so that P_t . P_u ~ sum_c cos(w_c . (p_t - p_u)) decays with 3D
+                grid distance (length scale ~4 steps) like the local attention
+                of a video DiT; Q = P + 0.5 N(0,1), K = P + 0.5 N(0,1)
+                (independent noise), V ~ N(0, 1).
 ``outliers``    ``positional`` plus 5 (head, channel) pairs in Q and 5 in K
                 (0.1% of the H*d = 5120 pairs of a 40-head layer, rounded)
                 multiplied by 20 on every token.
@@ -105,12 +108,9 @@ def _coords(grid):
 
 
 def _positional(grid, d, g):
-    a = torch.randn(8, d, generator=g, dtype=torch.float64) / math.sqrt(8.0)
-    w = torch.rand(8, 3, generator=g, dtype=torch.float64) * (math.pi / 4)
-    phi = torch.rand(8, d, generator=g, dtype=torch.float64) * (2 * math.pi)
-    theta = _coords(grid) @ w.T                                    # [N, 8]
-    # sin(theta + phi) = sin(theta) cos(phi) + cos(theta) sin(phi)
-    return torch.sin(theta) @ (a * torch.cos(phi)) + torch.cos(theta) @ (a * torch.sin(phi))
+    w = torch.randn(d, 3, generator=g, dtype=torch.float64) * 0.25
+    phi = torch.rand(d, generator=g, dtype=torch.float64) * (2 * math.pi)
+    return math.sqrt(2.0) * torch.sin(_coords(grid) @ w.T + phi)        # [N, d]
 
 
 def _locality(grid, d, g):
