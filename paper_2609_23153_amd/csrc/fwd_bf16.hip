@@ -153,8 +153,12 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
   const auto vr = make_rsrc(p.v + b * p.vs.b + h * p.vs.h, (uint32_t)(p.N - 1) * vst + 256u);
   const DmaOffsets dofs = dma_offsets(kst, vst);
 
-  int start = 0;
+  // Tile cursor: n / start = tile being computed, nn / nstart = the next valid
+  // tile (total / N when none).  The list entry of the tile after nn is read
+  // one step ahead, alongside that step's copies, so no step waits on it.
+  int start = p.N, nstart = p.N;
   int n = next_tile(list, 0, total, spb, p.block, p.nb, p.N, &start);
+  int nn = next_tile(list, n + 1, total, spb, p.block, p.nb, p.N, &nstart);
   if (n < total) dma_tile(lds0, kr, vr, dofs, (uint32_t)start * kst, (uint32_t)start * vst);
 
   // Q fragment (B operand of K.Q^T): query row l32 of this row-half,
@@ -197,9 +201,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
     // Prefetch the next tile into the other buffer.  Past the last tile the
     // start lies beyond the buffer range: the copies then read zeros without
     // touching memory, and the loop body has no branches around in-flight loads.
-    int nstart = p.N;
-    const int nn = next_tile(list, n + 1, total, spb, p.block, p.nb, p.N, &nstart);
     dma_tile(nxt, kr, vr, dofs, (uint32_t)nstart * kst, (uint32_t)nstart * vst);
+    const int ahead = nn + 1;  // tile after the prefetched one
+    const int pre = list[min(ahead / spb, p.kmax - 1)];
 
     const uint8_t* kt = cur;
     const uint8_t* vt = cur + kTileBytes;
@@ -280,6 +284,18 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
     __syncthreads();
     n = nn;
     start = nstart;
+    nn = total;
+    nstart = p.N;
+    if (ahead < total) {
+      const int j = __builtin_amdgcn_readfirstlane(pre);
+      const int st = j * p.block + (ahead % spb) * kTile;
+      if (j >= 0 && j < p.nb && st < p.N) {
+        nn = ahead;
+        nstart = st;
+      } else {
+        nn = next_tile(list, ahead + 1, total, spb, p.block, p.nb, p.N, &nstart);
+      }
+    }
   };
   while (n < total) {
     step(lds0, lds1);
