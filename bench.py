@@ -44,6 +44,8 @@ def parse_args():
     ap.add_argument("--cpu-baseline", choices=["on", "off"], default="on")
     ap.add_argument("--cpu-heads", type=int, default=2,
                     help="heads of the workload the oracle runs for the CPU baseline")
+    ap.add_argument("--fp8", choices=["on", "off"], default="on",
+                    help="also time the fp8 path on the outlier workload of the same shape")
     ap.add_argument("--copy-calib", action="store_true",
                     help="also time a plain 1 GiB device copy (HBM counter calibration)")
     return ap.parse_args()
@@ -71,6 +73,72 @@ def blas_threads():
     except Exception:
         pass
     return len(os.sched_getaffinity(0))
+
+
+def bench_fp8(args, sa, W, dev):
+    """fp8 pass at the same shape on the outlier workload: bf16 selection,
+    e4m3 quantisation of Q, K, V, scheduling, fp8 fused forward."""
+    wl = W.WORKLOADS["wan14b_720p_fp8"]
+    B, H, N, d, block = wl.batch, wl.heads, wl.seqlen, wl.head_dim, wl.block
+    nb = -(-N // block)
+    k = sa.sparse_attn_keep_count(wl.keep_bp, nb)
+    q, kk, v = (t.to(dev) for t in W.make_inputs(wl))
+    idx = torch.empty(B, H, nb, k, dtype=torch.int32, device=dev)
+    cnt = torch.empty(B, H, nb, dtype=torch.int32, device=dev)
+    o = torch.empty_like(q)
+    lse = torch.empty(B, H, N, dtype=torch.float32, device=dev)
+    x8 = [torch.empty(B, H, N, d, dtype=torch.uint8, device=dev) for _ in range(3)]
+    sc = [torch.empty(B, H, nb, dtype=torch.float32, device=dev) for _ in range(3)]
+    desc = sa.make_desc(q, kk, v, o, block=block)
+    ws_sel = torch.empty(sa.sparse_attn_workspace_size(desc, sa.SA_OP_SELECT, k),
+                         dtype=torch.uint8, device=dev)
+    ws_sch = torch.empty(sa.sparse_attn_workspace_size(desc, sa.SA_OP_SCHEDULE, k),
+                         dtype=torch.uint8, device=dev)
+    order = torch.empty(sa.sparse_attn_num_tiles(desc), dtype=torch.int32, device=dev)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+
+    def step(e=None):
+        if e:
+            e[0].record()
+        sa.sparse_attn_select(q, kk, k, block=block, idx=idx, cnt=cnt, ws=ws_sel)
+        if e:
+            e[1].record()
+        for t, a8, s8 in zip((q, kk, v), x8, sc):
+            sa.sparse_attn_quant_fp8(t, block=block, x8=a8, scale=s8)
+        if e:
+            e[2].record()
+        sa.sparse_attn_schedule(cnt, N, k, block=block, order=order, ws=ws_sch)
+        if e:
+            e[3].record()
+        sa.sparse_attn_fwd_fp8(x8[0], sc[0], x8[1], sc[1], x8[2], sc[2], idx, cnt, block=block,
+                               order=order, o=o, lse=lse)
+        if e:
+            e[4].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(ev[s])
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    ms = [float(np.mean([e[i].elapsed_time(e[i + 1]) for e in ev])) for i in range(4)]
+    flops = selected_flops(cnt.cpu().numpy(), idx.cpu().numpy(), N, block, d)
+    dense = 4 * B * H * N * N * d
+    tf = flops / (ms[3] * 1e-3) / 1e12
+    qbytes = 3 * (B * H * N * d * 3 + B * H * nb * 4)   # bf16 in, e4m3 out, scales
+    return {
+        "workload": wl.name, "dtype": "fp8-e4m3", "ms_per_step": round(ms_step, 4),
+        "dense_equiv_tflops_step": round(dense / (ms_step * 1e-3) / 1e12, 2),
+        "ms_per_call": {"select": round(ms[0], 4), "quant_qkv": round(ms[1], 4),
+                        "schedule": round(ms[2], 4), "fwd_fp8": round(ms[3], 4)},
+        "fwd_actual_tflops": round(tf, 2), "fwd_mfma_frac": round(tf / PEAK_FP8_TFLOPS, 4),
+        "quant_gbs": round(qbytes / (ms[1] * 1e-3) / 1e9, 1),
+        "roofline": {"kernel": "fwd_fp8_kernel", "bound": "mfma", "achieved": round(tf, 2),
+                     "peak": PEAK_FP8_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tf / PEAK_FP8_TFLOPS, 4), "flops_per_launch": flops},
+    }
 
 
 def main():
@@ -165,6 +233,9 @@ def main():
             "flops_per_launch": flops,
         },
     }
+
+    if args.fp8 == "on":
+        out["fp8"] = bench_fp8(args, sa, W, dev)
 
     if args.copy_calib:
         a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)

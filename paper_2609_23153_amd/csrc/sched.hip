@@ -38,6 +38,10 @@ __device__ __forceinline__ int slot_to_pos(int b, int G) {
   return (r / kRun) * group + x * kRun + (r % kRun);
 }
 
+// Classes of up to this many tiles are kept in LDS (one byte each) between
+// the histogram and the scatter pass; larger launches recompute them.
+constexpr int kClassCache = 64 * 1024;
+
 __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* __restrict__ cnt,
                                                                  int kmax, int nb, int ntiles,
                                                                  int block, int G,
@@ -46,8 +50,10 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* 
   __shared__ int hist[kClasses];
   __shared__ int base[kClasses];
   __shared__ int wave_cnt[kSchedThreads / kWave][kClasses];
+  __shared__ uint8_t cls_cache[kClassCache];
   const int t = threadIdx.x, lane = t & (kWave - 1), wave = t / kWave;
   const int spb = block / kTile;
+  const bool cached = G <= kClassCache;
   if (t < kClasses) hist[t] = 0;
   __syncthreads();
 
@@ -57,7 +63,12 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* 
     return cost_class(min(max(c, 0), kmax) * spb);
   };
 
-  for (int it = t; it < G; it += kSchedThreads) atomicAdd(&hist[cls_of(it)], 1);
+  // Histogram pass: the loads of all items are independent, so they overlap.
+  for (int it = t; it < G; it += kSchedThreads) {
+    const int c = cls_of(it);
+    if (cached) cls_cache[it] = (uint8_t)c;
+    atomicAdd(&hist[c], 1);
+  }
   __syncthreads();
   if (t == 0) {
     int acc = 0;
@@ -71,7 +82,7 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* 
   const uint64_t below = lanes_below_mask();
   for (int c0 = 0; c0 < G; c0 += kSchedThreads) {
     const int it = c0 + t;
-    const int cls = it < G ? cls_of(it) : -1;
+    const int cls = it < G ? (cached ? (int)cls_cache[it] : cls_of(it)) : -1;
     int rank = 0;
 #pragma unroll
     for (int c = 0; c < kClasses; ++c) {

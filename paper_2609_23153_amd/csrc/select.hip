@@ -59,9 +59,19 @@ __global__ __launch_bounds__(kPoolThreads) void pool_kernel(
   }
 }
 
-// fp64 score GEMM: one 64x64 tile of S = qhat khat^T / (n_i n_j) per workgroup.
+// fp64 score GEMM on the matrix cores: one 64x64 tile of
+// S = qhat khat^T / (n_i n_j) per workgroup of 4 waves, each wave a 32x32
+// quarter as 2x2 v_mfma_f64_16x16x4f64 tiles.  qhat and khat are staged
+// through LDS in 32-deep slices, [row][k] with a row stride of 34 doubles
+// (conflict-free both for the row-contiguous stores and for the operand
+// reads, 16 rows x 2 depths per half-wave).  The results are fp64 roundings
+// of the dot products in an order that differs from the oracle's only in the
+// last bits.
 constexpr int kSTile = 64;
-constexpr int kSK = 32;  // depth staged per step
+constexpr int kSDepth = 32;
+constexpr int kSStride = 34;
+typedef __attribute__((__vector_size__(4 * sizeof(double)))) double f64x4;
+
 __global__ __launch_bounds__(256) void score_kernel(const double* __restrict__ qhat,
                                                    const double* __restrict__ khat, int N,
                                                    int block, int nb,
@@ -70,52 +80,54 @@ __global__ __launch_bounds__(256) void score_kernel(const double* __restrict__ q
   const int i0 = blockIdx.y * kSTile, j0 = blockIdx.x * kSTile;
   const double* qb = qhat + (int64_t)bh * nb * kHeadDim;
   const double* kb = khat + (int64_t)bh * nb * kHeadDim;
-  __shared__ double As[kSK][kSTile + 1];
-  __shared__ double Bs[kSK][kSTile + 1];
-  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-  double acc[4][4];
+  __shared__ double As[kSTile * kSStride];
+  __shared__ double Bs[kSTile * kSStride];
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const int wr = (w >> 1) * 32, wc = (w & 1) * 32;  // this wave's 32x32 quarter
+  // 16x16x4 f64 operands: A lane l holds A[l%16][l/16], B lane l holds B[l/16][l%16];
+  // D lane l holds D[l/16 + 4r][l%16], r = 0..3.
+  const int li = l & 15, lk = l >> 4;
+  f64x4 acc[2][2];
 #pragma unroll
-  for (int r = 0; r < 4; ++r)
+  for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int c = 0; c < 4; ++c) acc[r][c] = 0.0;
+    for (int c = 0; c < 2; ++c) acc[a][c] = (f64x4){0.0, 0.0, 0.0, 0.0};
 
-  const int lr = threadIdx.x >> 2;       // tile row loaded by this thread
-  const int lk = (threadIdx.x & 3) * 8;  // 8 consecutive depth values
-  for (int k0 = 0; k0 < kHeadDim; k0 += kSK) {
-    const bool qa = i0 + lr < nb, ka = j0 + lr < nb;
+  for (int k0 = 0; k0 < kHeadDim; k0 += kSDepth) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      As[lk + e][lr] = qa ? qb[(int64_t)(i0 + lr) * kHeadDim + k0 + lk + e] : 0.0;
-      Bs[lk + e][lr] = ka ? kb[(int64_t)(j0 + lr) * kHeadDim + k0 + lk + e] : 0.0;
+    for (int m = 0; m < kSTile * kSDepth / 256; ++m) {
+      const int e = threadIdx.x + 256 * m;
+      const int r = e / kSDepth, c = e - r * kSDepth;
+      As[r * kSStride + c] = i0 + r < nb ? qb[(int64_t)(i0 + r) * kHeadDim + k0 + c] : 0.0;
+      Bs[r * kSStride + c] = j0 + r < nb ? kb[(int64_t)(j0 + r) * kHeadDim + k0 + c] : 0.0;
     }
     __syncthreads();
-#pragma unroll 8
-    for (int kk = 0; kk < kSK; ++kk) {
-      double a[4], bv[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) a[r] = As[kk][ty + 16 * r];
-#pragma unroll
-      for (int c = 0; c < 4; ++c) bv[c] = Bs[kk][tx + 16 * c];
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-#pragma unroll
-        for (int c = 0; c < 4; ++c) acc[r][c] = fma(a[r], bv[c], acc[r][c]);
+    for (int kk = 0; kk < kSDepth; kk += 4) {
+      const double a0 = As[(wr + li) * kSStride + kk + lk];
+      const double a1 = As[(wr + 16 + li) * kSStride + kk + lk];
+      const double b0 = Bs[(wc + li) * kSStride + kk + lk];
+      const double b1 = Bs[(wc + 16 + li) * kSStride + kk + lk];
+      acc[0][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b0, acc[0][0], 0, 0, 0);
+      acc[0][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b1, acc[0][1], 0, 0, 0);
+      acc[1][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b0, acc[1][0], 0, 0, 0);
+      acc[1][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b1, acc[1][1], 0, 0, 0);
     }
     __syncthreads();
   }
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int i = i0 + ty + 16 * r;
-    if (i >= nb) continue;
-    const int n_i = min(block, N - i * block);
+  for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int j = j0 + tx + 16 * c;
-      if (j >= nb) continue;
-      const int n_j = min(block, N - j * block);
-      scores[((int64_t)bh * nb + i) * nb + j] = acc[r][c] / (double)(n_i * n_j);
-    }
-  }
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int i = i0 + wr + 16 * a + lk + 4 * r;
+        const int j = j0 + wc + 16 * c + li;
+        if (i < nb && j < nb) {
+          const int n_i = min(block, N - i * block), n_j = min(block, N - j * block);
+          scores[((int64_t)bh * nb + i) * nb + j] = acc[a][c][r] / (double)(n_i * n_j);
+        }
+      }
 }
 
 // Order-preserving map of a double to uint64 (larger score -> larger key);
@@ -164,10 +176,10 @@ __device__ __forceinline__ uint64_t kth_largest(const uint64_t (&key)[KPL], cons
   uint64_t prefix = mx & ~((2ull << top) - 1ull);  // bits above `top` are common
   for (int bit = top; bit >= 0; --bit) {
     const uint64_t cand = prefix | (1ull << bit);
+    // count over the wave with ballots: scalar popcounts, no cross-lane shuffles
     int c = 0;
 #pragma unroll
-    for (int t = 0; t < KPL; ++t) c += (valid[t] && key[t] >= cand) ? 1 : 0;
-    c = wave_sum(c);
+    for (int t = 0; t < KPL; ++t) c += __popcll(__ballot(valid[t] && key[t] >= cand));
     if (c >= k) {
       prefix = cand;
       if (c == k) break;
@@ -196,8 +208,8 @@ __global__ __launch_bounds__(256) void topk_row_kernel(const double* __restrict_
   const uint64_t thr = kth_largest<KPL>(key, valid, k);
   int gt = 0;
 #pragma unroll
-  for (int t = 0; t < KPL; ++t) gt += (valid[t] && key[t] > thr) ? 1 : 0;
-  const int need_eq = k - wave_sum(gt);  // ties at the threshold, lowest index first
+  for (int t = 0; t < KPL; ++t) gt += __popcll(__ballot(valid[t] && key[t] > thr));
+  const int need_eq = k - gt;  // ties at the threshold, lowest index first
 
   const uint64_t below = lanes_below_mask();
   int32_t* out = idx + (int64_t)row * kmax;
