@@ -35,6 +35,31 @@ __device__ __forceinline__ float pair_max32(float x) {
   return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
 }
 
+// Global -> LDS copy of 16 bytes per lane (buffer_load_dwordx4 ... lds): lane
+// l's bytes land at LDS byte address lds_addr + 16*l; rows past the resource
+// range land as zeros.  Issued from inline asm so that the compiler does not
+// track it: callers wait (vmcnt) and synchronise explicitly.  The compiler's
+// own waits stay correct (they can only become more conservative), and the
+// memory clobber keeps program order for every memory access around it.
+__device__ __forceinline__ void dma16(uint32_t lds_addr, __amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                      uint32_t soff) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :: "s"(lds_addr), "v"(voff), "s"(r), "s"(soff)
+               : "memory", "m0");
+}
+
+// LDS byte address of a __shared__ pointer.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// Workgroup barrier for pipelined LDS staging: unlike __syncthreads() it has
+// no release fence, which would wait for every load in flight (vmcnt(0)),
+// including global->LDS copies meant to stay in flight across the barrier.
+// The caller waits explicitly for the copies the next step reads; the memory
+// clobber keeps the compiler from moving memory accesses across.
+__device__ __forceinline__ void barrier_keep_loads() { asm volatile("s_barrier" ::: "memory"); }
+
 // 16-byte global load / store (dwordx4) of raw bits.
 __device__ __forceinline__ u32x4 ld16(const void* p) {
   return *reinterpret_cast<const u32x4*>(p);

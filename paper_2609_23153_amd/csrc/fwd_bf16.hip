@@ -7,9 +7,13 @@
 // One workgroup = 4 wavefronts = one 64-row query tile; two workgroups share
 // a CU.  Every selected key block is walked as 64-key tiles:
 //  * K and V tiles go straight from HBM/L2 into LDS with buffer_load ... lds
-//    (no staging registers, no VALU), double-buffered, rows past the sequence
-//    end reading zero through the buffer range check.  Both tiles are stored
-//    row-major with a 16-byte-chunk XOR swizzle chosen on the global side.
+//    (no staging registers, no VALU), rows past the sequence end reading zero
+//    through the buffer range check.  K is triple-buffered and V double-
+//    buffered: step n issues V(n+1) and K(n+2), so a K tile has two steps and
+//    a V tile almost two to arrive (tiles that miss L2 come from the MALL or
+//    HBM with about a step of latency).  80 KB of LDS per workgroup, two
+//    workgroups per CU.  Both tiles are stored row-major with a 16-byte-chunk
+//    XOR swizzle chosen on the global side.
 //  * Wave w owns query rows 32*(w&1)..+31 and keys 32*(w>>1)..+31 of a tile:
 //      S^T (32 keys x 32 queries) = K_half . Q_half^T   8 x v_mfma_f32_32x32x16_bf16
 //      O^T (128 x 32)          += V_half^T . P^T       8 x v_mfma_f32_32x32x16_bf16
@@ -30,7 +34,7 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kRowBytes = kHeadDim * 2;            // 256 B per bf16 row
 constexpr int kTileBytes = kTile * kRowBytes;      // 16 KB per K or V tile
-constexpr int kBufBytes = 2 * kTileBytes;          // K + V: 32 KB, two such buffers
+
 constexpr float kLazy = 8.f;  // log2 headroom before the accumulator is rescaled
 
 // 16-byte-chunk swizzles (row = row within the tile): conflict-free for the
@@ -58,8 +62,10 @@ struct Params {
 
 // Start row of the n-th 64-key tile of a query block's list, or -1 when the
 // list entry is out of range or the sub-tile lies past the sequence end.
-__device__ __forceinline__ int tile_start(const int32_t* list, int n, int spb, int block,
-                                          int nb, int N) {
+typedef const __attribute__((address_space(4))) int32_t* list_ptr;
+
+__device__ __forceinline__ int tile_start(list_ptr list, int n, int spb, int block, int nb,
+                                          int N) {
   const int e = n / spb;
   const int j = list[e];
   if (j < 0 || j >= nb) return -1;
@@ -67,8 +73,8 @@ __device__ __forceinline__ int tile_start(const int32_t* list, int n, int spb, i
   return st < N ? st : -1;
 }
 
-__device__ __forceinline__ int next_tile(const int32_t* list, int n, int total, int spb,
-                                         int block, int nb, int N, int* start) {
+__device__ __forceinline__ int next_tile(list_ptr list, int n, int total, int spb, int block,
+                                         int nb, int N, int* start) {
   for (; n < total; ++n) {
     const int st = tile_start(list, n, spb, block, nb, N);
     if (st >= 0) {
@@ -100,37 +106,31 @@ __device__ __forceinline__ DmaOffsets dma_offsets(uint32_t kst, uint32_t vst) {
   return o;
 }
 
-// Issue the global -> LDS copies of one K/V tile into the buffer `dst`.
-// Completion is tracked by vmcnt.
-__device__ __forceinline__ void dma_tile(uint8_t* dst, __amdgpu_buffer_rsrc_t kr,
-                                         __amdgpu_buffer_rsrc_t vr, const DmaOffsets& o,
-                                         uint32_t ksoff, uint32_t vsoff) {
-  const int w = threadIdx.x >> 6;
-  uint8_t* kb = dst + (16 * w) * kRowBytes;
-  uint8_t* vb = kb + kTileBytes;
+// Issue the global -> LDS copies of one K or V tile (4 instructions per
+// wave, each 4 rows); completion is tracked by vmcnt, which the caller waits.
+__device__ __forceinline__ void dma_tile(uint8_t* dst, __amdgpu_buffer_rsrc_t r,
+                                         const uint32_t (&off)[4], uint32_t soff) {
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const uint32_t base = lds_addr(dst) + (uint32_t)(16 * w) * kRowBytes;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_void*)(kb + 4 * i * kRowBytes), 16, o.k[i],
-                                             ksoff, 0, 0);
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_void*)(vb + 4 * i * kRowBytes), 16, o.v[i],
-                                             vsoff, 0, 0);
+  for (int i = 0; i < 4; ++i) dma16(base + 4 * i * kRowBytes, r, off[i], soff);
 }
 
-__device__ __forceinline__ void wait_dma() {
-  // vmcnt(0); expcnt and lgkmcnt left at their maxima (no wait).
-  __builtin_amdgcn_s_waitcnt(0x0F70);
-}
+// vmcnt(n) with expcnt and lgkmcnt left at their maxima (no wait on them).
+__device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+__device__ __forceinline__ void wait_vm4() { __builtin_amdgcn_s_waitcnt(0x0F74); }
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
 __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
-  // Two distinct LDS objects (rather than one array indexed by a buffer
-  // number) let the compiler prove that the reads of one buffer do not alias
-  // the copies in flight into the other, so it does not wait for them.
-  __shared__ __attribute__((aligned(1024))) uint8_t lds0[kBufBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t lds1[kBufBytes];
+  // Distinct LDS objects per buffer (rather than one array indexed by a
+  // buffer number) let the compiler prove that the reads of one buffer do not
+  // alias the copies in flight into another, so it does not wait for them.
+  __shared__ __attribute__((aligned(1024))) uint8_t kb0[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t kb1[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t kb2[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t vb0[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t vb1[kTileBytes];
 
   const int item = p.order ? p.order[blockIdx.x] : (int)blockIdx.x;
   const int bh = item / p.ntiles;
@@ -139,9 +139,11 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
   const int q0 = qt * kTile;
   const int iblk = q0 / p.block;
   const int spb = p.block / kTile;
-  const int32_t* list = p.idx + ((int64_t)bh * p.nb + iblk) * p.kmax;
   const int c = min(max(p.cnt[(int64_t)bh * p.nb + iblk], 0), p.kmax);
   const int total = c * spb;
+  // The list is read-only here: reading it through the constant address space
+  // makes the uniform reads scalar loads (s_load), which vmcnt does not count.
+  const list_ptr list = (list_ptr)(p.idx + ((int64_t)bh * p.nb + iblk) * p.kmax);
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int rh = wave & 1, kh = wave >> 1;
@@ -153,13 +155,14 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
   const auto vr = make_rsrc(p.v + b * p.vs.b + h * p.vs.h, (uint32_t)(p.N - 1) * vst + 256u);
   const DmaOffsets dofs = dma_offsets(kst, vst);
 
-  // Tile cursor: n / start = tile being computed, nn / nstart = the next valid
-  // tile (total / N when none).  The list entry of the tile after nn is read
-  // one step ahead, alongside that step's copies, so no step waits on it.
-  int start = p.N, nstart = p.N;
+  // Tile cursor: n / start = tile being computed; n1 / s1 and n2 / s2 = the
+  // next two valid tiles (total / N when none).  The list entry of the tile
+  // after n2 is read one step ahead, before that step's copies, so no step
+  // waits on it.
+  int start = p.N, s1 = p.N, s2 = p.N;
   int n = next_tile(list, 0, total, spb, p.block, p.nb, p.N, &start);
-  int nn = next_tile(list, n + 1, total, spb, p.block, p.nb, p.N, &nstart);
-  if (n < total) dma_tile(lds0, kr, vr, dofs, (uint32_t)start * kst, (uint32_t)start * vst);
+  int n1 = next_tile(list, n + 1, total, spb, p.block, p.nb, p.N, &s1);
+  int n2 = next_tile(list, n1 + 1, total, spb, p.block, p.nb, p.N, &s2);
 
   // Q fragment (B operand of K.Q^T): query row l32 of this row-half,
   // channels 16*ks + 8*g .. +7.
@@ -169,6 +172,11 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
     const uint32_t off = (uint32_t)(q0 + rh * 32 + l32) * qst + g * 16;
 #pragma unroll
     for (int s = 0; s < 8; ++s) qf[s] = as_bf16x8(buf_ld16(qr, off + s * 32));
+  }
+  if (n < total) {
+    dma_tile(kb0, kr, dofs.k, (uint32_t)start * kst);
+    dma_tile(vb0, vr, dofs.v, (uint32_t)start * vst);
+    dma_tile(kb1, kr, dofs.k, (uint32_t)s1 * kst);
   }
 
   f32x16 acc[4];
@@ -193,20 +201,24 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
   const int G = lane >> 4, e4 = (lane >> 2) & 3, q4 = lane & 3;
   const int vrow0 = kh * 32 + 4 * (G >> 1) + e4;  // + 16*cs + 8*hf (keeps row & 3)
 
-  wait_dma();
-  __syncthreads();
+  wait_vm0();  // Q, K(0), V(0), K(1) landed
+  barrier_keep_loads();
 
-  // One 64-key tile: compute from `cur` while the next tile streams into `nxt`.
-  auto step = [&](const uint8_t* cur, uint8_t* nxt) {
-    // Prefetch the next tile into the other buffer.  Past the last tile the
-    // start lies beyond the buffer range: the copies then read zeros without
-    // touching memory, and the loop body has no branches around in-flight loads.
-    dma_tile(nxt, kr, vr, dofs, (uint32_t)nstart * kst, (uint32_t)nstart * vst);
-    const int ahead = nn + 1;  // tile after the prefetched one
+  // One 64-key tile: compute from K buffer `kc` and V buffer `vc` while V(n+1)
+  // streams into `vn` and K(n+2) into `kn2`.  Past the last tile the starts
+  // lie beyond the buffer range: the copies then read zeros without touching
+  // memory, and the loop body has no branches around in-flight loads.
+  auto step = [&](const uint8_t* kc, uint8_t* kn2, const uint8_t* vc, uint8_t* vn) {
+    // tile after the last one in flight; its list entry is a scalar load, so
+    // that no vector load follows the copies and vmcnt(4) below means "all
+    // but K(n+2)"
+    const int ahead = n2 + 1;
     const int pre = list[min(ahead / spb, p.kmax - 1)];
+    dma_tile(vn, vr, dofs.v, (uint32_t)s1 * vst);
+    dma_tile(kn2, kr, dofs.k, (uint32_t)s2 * kst);
 
-    const uint8_t* kt = cur;
-    const uint8_t* vt = cur + kTileBytes;
+    const uint8_t* kt = kc;
+    const uint8_t* vt = vc;
 
     // ---- S^T = K_half . Q^T ------------------------------------------------
     f32x16 s;
@@ -280,44 +292,60 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
       }
     }
 
-    wait_dma();
-    __syncthreads();
-    n = nn;
-    start = nstart;
-    nn = total;
-    nstart = p.N;
+    wait_vm4();  // everything but K(n+2): V(n+1) and K(n+1) have landed
+    barrier_keep_loads();
+    n = n1;
+    start = s1;
+    n1 = n2;
+    s1 = s2;
+    n2 = total;
+    s2 = p.N;
     if (ahead < total) {
       const int j = __builtin_amdgcn_readfirstlane(pre);
       const int st = j * p.block + (ahead % spb) * kTile;
       if (j >= 0 && j < p.nb && st < p.N) {
-        nn = ahead;
-        nstart = st;
+        n2 = ahead;
+        s2 = st;
       } else {
-        nn = next_tile(list, ahead + 1, total, spb, p.block, p.nb, p.N, &nstart);
+        n2 = next_tile(list, ahead + 1, total, spb, p.block, p.nb, p.N, &s2);
       }
     }
   };
+  // step n reads K[n%3], V[n%2] and fills K[(n+2)%3], V[(n+1)%2]
   while (n < total) {
-    step(lds0, lds1);
+    step(kb0, kb2, vb0, vb1);
     if (n >= total) break;
-    step(lds1, lds0);
+    step(kb1, kb0, vb1, vb0);
+    if (n >= total) break;
+    step(kb2, kb1, vb0, vb1);
+    if (n >= total) break;
+    step(kb0, kb2, vb1, vb0);
+    if (n >= total) break;
+    step(kb1, kb0, vb0, vb1);
+    if (n >= total) break;
+    step(kb2, kb1, vb1, vb0);
   }
+  wait_vm0();
+  __syncthreads();
 
   // ---- merge the two key halves, normalise, store ------------------------
   lsum += __shfl_xor(lsum, 32, kWave);
-  float* mrg = reinterpret_cast<float*>(rh ? lds1 : lds0);  // 66 x 64 floats per row-half
+  // per row-half: 64 x 64 accumulator floats in kb0 / kb1 (16 KB each), the
+  // max and sum (2 x 64 floats) in vb0
+  float* mrg = reinterpret_cast<float*>(rh ? kb1 : kb0);
+  float* mls = reinterpret_cast<float*>(vb0) + rh * 2 * kWave;
   if (kh == 1) {
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mrg[(dt * 16 + r) * kWave + lane] = acc[dt][r];
-    mrg[64 * kWave + lane] = m2;
-    mrg[65 * kWave + lane] = lsum;
+    mls[lane] = m2;
+    mls[kWave + lane] = lsum;
   }
   __syncthreads();
   if (kh == 0) {
-    const float m_o = mrg[64 * kWave + lane];
-    const float l_o = mrg[65 * kWave + lane];
+    const float m_o = mls[lane];
+    const float l_o = mls[kWave + lane];
     const float mm = fmaxf(m2, m_o);
     const float ms = mm == -INFINITY ? 0.f : mm;
     const float a0 = __builtin_amdgcn_exp2f(m2 - ms);
