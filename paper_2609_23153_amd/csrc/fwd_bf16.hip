@@ -6,14 +6,15 @@
 //
 // One workgroup = 4 wavefronts = one 64-row query tile; two workgroups share
 // a CU.  Every selected key block is walked as 64-key tiles:
-//  * K and V tiles go straight from HBM/L2 into LDS with buffer_load ... lds
-//    (no staging registers, no VALU), rows past the sequence end reading zero
-//    through the buffer range check.  K is triple-buffered and V double-
-//    buffered: step n issues V(n+1) and K(n+2), so a K tile has two steps and
-//    a V tile almost two to arrive (tiles that miss L2 come from the MALL or
-//    HBM with about a step of latency).  80 KB of LDS per workgroup, two
-//    workgroups per CU.  Both tiles are stored row-major with a 16-byte-chunk
-//    XOR swizzle chosen on the global side.
+//  * K and V tiles go straight from L2 into LDS with buffer_load ... lds (no
+//    staging registers, no VALU), rows past the sequence end reading zero
+//    through the buffer range check.  Both are stored row-major with a
+//    16-byte-chunk XOR swizzle chosen on the global side.
+//  * Each step first reads its whole K and V fragments from LDS into
+//    registers; after one barrier both buffers are free and immediately
+//    receive K(n+3) and V(n+2).  A K tile thus has three steps and a V tile
+//    two to arrive, from 80 KB of LDS per workgroup (K triple-, V double-
+//    buffered): enough bytes in flight to cover L2 latency under load.
 //  * Wave w owns query rows 32*(w&1)..+31 and keys 32*(w>>1)..+31 of a tile:
 //      S^T (32 keys x 32 queries) = K_half . Q_half^T   8 x v_mfma_f32_32x32x16_bf16
 //      O^T (128 x 32)          += V_half^T . P^T       8 x v_mfma_f32_32x32x16_bf16
@@ -116,16 +117,17 @@ __device__ __forceinline__ void dma_tile(uint8_t* dst, __amdgpu_buffer_rsrc_t r,
   for (int i = 0; i < 4; ++i) dma16(base + 4 * i * kRowBytes, r, off[i], soff);
 }
 
-// vmcnt(n) with expcnt and lgkmcnt left at their maxima (no wait on them).
+// s_waitcnt with the other counters at their maxima (no wait on them).
 __device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
-__device__ __forceinline__ void wait_vm4() { __builtin_amdgcn_s_waitcnt(0x0F74); }
+__device__ __forceinline__ void wait_vm12() { __builtin_amdgcn_s_waitcnt(0x0F7C); }
+__device__ __forceinline__ void wait_vm16() { __builtin_amdgcn_s_waitcnt(0x4F70); }
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
 __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
   // Distinct LDS objects per buffer (rather than one array indexed by a
-  // buffer number) let the compiler prove that the reads of one buffer do not
-  // alias the copies in flight into another, so it does not wait for them.
+  // buffer number) keep every access at a constant base.
   __shared__ __attribute__((aligned(1024))) uint8_t kb0[kTileBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t kb1[kTileBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t kb2[kTileBytes];
@@ -155,29 +157,55 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
   const auto vr = make_rsrc(p.v + b * p.vs.b + h * p.vs.h, (uint32_t)(p.N - 1) * vst + 256u);
   const DmaOffsets dofs = dma_offsets(kst, vst);
 
-  // Tile cursor: n / start = tile being computed; n1 / s1 and n2 / s2 = the
-  // next two valid tiles (total / N when none).  The list entry of the tile
-  // after n2 is read one step ahead, before that step's copies, so no step
-  // waits on it.
-  int start = p.N, s1 = p.N, s2 = p.N;
-  int n = next_tile(list, 0, total, spb, p.block, p.nb, p.N, &start);
+  // Tile cursor: n / s0 = tile being computed, n1..n3 / s1..s3 = the next
+  // three valid tiles (total / N when there are none).  The list entry after n3 is read one step ahead.
+  int s0 = p.N, s1 = p.N, s2 = p.N, s3 = p.N;
+  int n = next_tile(list, 0, total, spb, p.block, p.nb, p.N, &s0);
   int n1 = next_tile(list, n + 1, total, spb, p.block, p.nb, p.N, &s1);
   int n2 = next_tile(list, n1 + 1, total, spb, p.block, p.nb, p.N, &s2);
+  int n3 = next_tile(list, n2 + 1, total, spb, p.block, p.nb, p.N, &s3);
+
+  // Prologue.  The Q tile is staged through kb2 (same swizzle as K), then
+  // K(0), V(0), K(1), V(1) are issued; once every wave holds its Q fragment,
+  // kb2 receives K(2).  Past the end of the list the starts equal N and the
+  // copies read zeros without touching memory, so every step issues the same
+  // number of copies and the vmcnt arithmetic below is uniform.
+  {
+    const auto qr = make_rsrc(p.q + b * p.qs.b + h * p.qs.h, (uint32_t)(p.N - 1) * qst + 256u);
+    const DmaOffsets qofs = dma_offsets(qst, qst);
+    dma_tile(kb2, qr, qofs.k, (uint32_t)q0 * qst);
+  }
+  dma_tile(kb0, kr, dofs.k, (uint32_t)s0 * kst);
+  dma_tile(vb0, vr, dofs.v, (uint32_t)s0 * vst);
+  dma_tile(kb1, kr, dofs.k, (uint32_t)s1 * kst);
+  dma_tile(vb1, vr, dofs.v, (uint32_t)s1 * vst);
+  wait_vm16();  // this wave's rows of Q have landed
+  barrier_keep_loads();
+
+  // LDS read addresses (bytes, relative to a buffer):
+  //  Q B-operand / K A-operand: row rh*32 + l32 / kh*32 + l32, logical chunk
+  //  2*ks + g.
+  //  V^T A-operand (transpose read): lane 16G + 4e + q supplies the 8-byte
+  //  chunk of key kh*32 + 16*cs + 8*hf + 4*(G>>1) + e at channels
+  //  32*dt + 16*(G&1) + 4*q .. +3; lane l then receives channel 32*dt + (l&31)
+  //  of keys kh*32 + 16*cs + 8*hf + 4*g + {0..3}.
+  const int krow = kh * 32 + l32;
+  const int G = lane >> 4, e4 = (lane >> 2) & 3, q4 = lane & 3;
+  const int vrow0 = kh * 32 + 4 * (G >> 1) + e4;  // + 16*cs + 8*hf (keeps row & 3)
 
   // Q fragment (B operand of K.Q^T): query row l32 of this row-half,
   // channels 16*ks + 8*g .. +7.
   bf16x8 qf[8];
   {
-    const auto qr = make_rsrc(p.q + b * p.qs.b + h * p.qs.h, (uint32_t)(p.N - 1) * qst + 256u);
-    const uint32_t off = (uint32_t)(q0 + rh * 32 + l32) * qst + g * 16;
+    const int qrow = rh * 32 + l32;
 #pragma unroll
-    for (int s = 0; s < 8; ++s) qf[s] = as_bf16x8(buf_ld16(qr, off + s * 32));
+    for (int ks = 0; ks < 8; ++ks)
+      qf[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(kb2 + qrow * kRowBytes +
+                                                         swz_k(qrow, 2 * ks + g) * 16));
   }
-  if (n < total) {
-    dma_tile(kb0, kr, dofs.k, (uint32_t)start * kst);
-    dma_tile(vb0, vr, dofs.v, (uint32_t)start * vst);
-    dma_tile(kb1, kr, dofs.k, (uint32_t)s1 * kst);
-  }
+  wait_lgkm0();
+  barrier_keep_loads();
+  dma_tile(kb2, kr, dofs.k, (uint32_t)s2 * kst);
 
   f32x16 acc[4];
 #pragma unroll
@@ -191,50 +219,55 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
   float m2 = -INFINITY;
   float lsum = 0.f;  // partial sum of 2^(x - m2) over this lane's keys
 
-  // LDS read addresses (bytes, relative to a buffer):
-  //  K A-operand: row kh*32 + l32, logical chunk 2*ks + g
-  //  V^T A-operand (transpose read): lane 16G + 4e + q supplies the 8-byte
-  //  chunk of key kh*32 + 16*cs + 8*hf + 4*(G>>1) + e at channels
-  //  32*dt + 16*(G&1) + 4*q .. +3; lane l then receives channel 32*dt + (l&31)
-  //  of keys kh*32 + 16*cs + 8*hf + 4*g + {0..3}.
-  const int krow = kh * 32 + l32;
-  const int G = lane >> 4, e4 = (lane >> 2) & 3, q4 = lane & 3;
-  const int vrow0 = kh * 32 + 4 * (G >> 1) + e4;  // + 16*cs + 8*hf (keeps row & 3)
-
-  wait_vm0();  // Q, K(0), V(0), K(1) landed
+  wait_vm12();  // K(0), V(0) landed (K(1), V(1), K(2) may still fly)
   barrier_keep_loads();
 
-  // One 64-key tile: compute from K buffer `kc` and V buffer `vc` while V(n+1)
-  // streams into `vn` and K(n+2) into `kn2`.  Past the last tile the starts
-  // lie beyond the buffer range: the copies then read zeros without touching
-  // memory, and the loop body has no branches around in-flight loads.
-  auto step = [&](const uint8_t* kc, uint8_t* kn2, const uint8_t* vc, uint8_t* vn) {
-    // tile after the last one in flight; its list entry is a scalar load, so
-    // that no vector load follows the copies and vmcnt(4) below means "all
-    // but K(n+2)"
-    const int ahead = n2 + 1;
+  // One 64-key tile, computed from K buffer `kc` and V buffer `vc`, which
+  // then receive K(n+3) and V(n+2).
+  auto step = [&](uint8_t* kc, uint8_t* vc) {
+    bf16x8 kf[8];
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks)
+      kf[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(kc + krow * kRowBytes +
+                                                         swz_k(krow, 2 * ks + g) * 16));
+    u32x4 vf[8];  // V^T fragments, [2*dt + cs]
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+      const int lc = 4 * dt + 2 * (G & 1) + (q4 >> 1);  // logical 16-B chunk
+      const int half = (q4 & 1) * 8;
+#pragma unroll
+      for (int cs = 0; cs < 2; ++cs)
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          const int row = vrow0 + 16 * cs + 8 * hf;
+          const i16x4 t = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) i16x4*)(vc + row * kRowBytes +
+                                                         swz_v(row, lc) * 16 + half));
+          const u32x2 tw = __builtin_bit_cast(u32x2, t);
+          vf[2 * dt + cs][2 * hf] = tw[0];
+          vf[2 * dt + cs][2 * hf + 1] = tw[1];
+        }
+    }
+    // list entry of the tile after n3 (a scalar load, waited below)
+    const int ahead = n3 + 1;
     const int pre = list[min(ahead / spb, p.kmax - 1)];
-    dma_tile(vn, vr, dofs.v, (uint32_t)s1 * vst);
-    dma_tile(kn2, kr, dofs.k, (uint32_t)s2 * kst);
-
-    const uint8_t* kt = kc;
-    const uint8_t* vt = vc;
+    wait_lgkm0();
+    barrier_keep_loads();  // every wave holds its fragments: kc and vc are free
+    dma_tile(vc, vr, dofs.v, (uint32_t)s2 * vst);
+    dma_tile(kc, kr, dofs.k, (uint32_t)s3 * kst);
 
     // ---- S^T = K_half . Q^T ------------------------------------------------
     f32x16 s;
 #pragma unroll
     for (int r = 0; r < 16; ++r) s[r] = 0.f;
 #pragma unroll
-    for (int ks = 0; ks < 8; ++ks) {
-      const bf16x8 kf = as_bf16x8(*reinterpret_cast<const u32x4*>(
-          kt + krow * kRowBytes + swz_k(krow, 2 * ks + g) * 16));
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s, 0, 0, 0);
-    }
+    for (int ks = 0; ks < 8; ++ks)
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], qf[ks], s, 0, 0, 0);
     // lane holds keys kh*32 + 8*(r>>2) + 4*g + (r&3) of query l32
-    if (start + kTile > p.N) {
+    if (s0 + kTile > p.N) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int key = start + kh * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
+        const int key = s0 + kh * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
         if (key >= p.N) s[r] = -INFINITY;
       }
     }
@@ -272,58 +305,49 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
 
     // ---- O^T += V_half^T . P^T -------------------------------------------
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt) {
-      const int lc = 4 * dt + 2 * (G & 1) + (q4 >> 1);  // logical 16-B chunk
-      const int half = (q4 & 1) * 8;
+    for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-      for (int cs = 0; cs < 2; ++cs) {
-        u32x4 vv;
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-          const int row = vrow0 + 16 * cs + 8 * hf;
-          const i16x4 t = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (__attribute__((address_space(3))) i16x4*)(vt + row * kRowBytes +
-                                                         swz_v(row, lc) * 16 + half));
-          const u32x2 tw = __builtin_bit_cast(u32x2, t);
-          vv[2 * hf] = tw[0];
-          vv[2 * hf + 1] = tw[1];
-        }
-        acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv), pk[cs], acc[dt], 0, 0, 0);
-      }
-    }
+      for (int cs = 0; cs < 2; ++cs)
+        acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf[2 * dt + cs]), pk[cs],
+                                                          acc[dt], 0, 0, 0);
 
-    wait_vm4();  // everything but K(n+2): V(n+1) and K(n+1) have landed
-    barrier_keep_loads();
+    // advance the cursor
     n = n1;
-    start = s1;
     n1 = n2;
+    n2 = n3;
+    s0 = s1;
     s1 = s2;
-    n2 = total;
-    s2 = p.N;
+    s2 = s3;
+    s3 = p.N;
+    n3 = total;
     if (ahead < total) {
       const int j = __builtin_amdgcn_readfirstlane(pre);
       const int st = j * p.block + (ahead % spb) * kTile;
       if (j >= 0 && j < p.nb && st < p.N) {
-        n2 = ahead;
-        s2 = st;
+        n3 = ahead;
+        s3 = st;
       } else {
-        n2 = next_tile(list, ahead + 1, total, spb, p.block, p.nb, p.N, &s2);
+        n3 = next_tile(list, ahead + 1, total, spb, p.block, p.nb, p.N, &s3);
       }
     }
+    // keep the whole tile's work ahead of the wait
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vm12();  // K(n+1), V(n+1) landed; K(n+2), V(n+2), K(n+3) may fly
+    barrier_keep_loads();
   };
-  // step n reads K[n%3], V[n%2] and fills K[(n+2)%3], V[(n+1)%2]
+  // step n reads and refills K[n%3], V[n%2]
   while (n < total) {
-    step(kb0, kb2, vb0, vb1);
+    step(kb0, vb0);
     if (n >= total) break;
-    step(kb1, kb0, vb1, vb0);
+    step(kb1, vb1);
     if (n >= total) break;
-    step(kb2, kb1, vb0, vb1);
+    step(kb2, vb0);
     if (n >= total) break;
-    step(kb0, kb2, vb1, vb0);
+    step(kb0, vb1);
     if (n >= total) break;
-    step(kb1, kb0, vb0, vb1);
+    step(kb1, vb0);
     if (n >= total) break;
-    step(kb2, kb1, vb1, vb0);
+    step(kb2, vb1);
   }
   wait_vm0();
   __syncthreads();
