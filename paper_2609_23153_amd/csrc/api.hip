@@ -30,7 +30,9 @@ int check_desc(const sparse_attn_desc* d, Shape* s) {
   if (d->block != 64 && d->block != 128) return SA_ERR_UNSUPPORTED;
   const int64_t nb = (d->seqlen + (int64_t)d->block - 1) / d->block;
   if (nb > kMaxBlocks) return SA_ERR_UNSUPPORTED;
-  if ((int64_t)d->batch * d->heads * nb > (int64_t)1 << 30) return SA_ERR_UNSUPPORTED;
+  // query tiles (and so launch slots) must fit the 32-bit tile index
+  const int64_t ntiles = (d->seqlen + 63) / 64;
+  if ((int64_t)d->batch * d->heads * ntiles > (int64_t)1 << 30) return SA_ERR_UNSUPPORTED;
   s->B = d->batch;
   s->H = d->heads;
   s->N = d->seqlen;

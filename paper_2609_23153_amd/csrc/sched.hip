@@ -9,18 +9,23 @@
 //  * locality: within a class, tiles stay in raster order, and blockIdx is
 //    remapped so that each XCD (blockIdx % 8 on MI355X) receives runs of
 //    consecutive tiles, whose key-block lists overlap and share that XCD's L2.
-// The cost classes are floor(log2(key tiles)) so the sort is a 16-bucket
-// stable partition computed by one workgroup.
+// The cost classes are floor(log2(key tiles)), so the sort is a 16-bucket
+// stable partition (a counting sort), done by three small launches over
+// chunks of 1024 tiles: class counts per chunk, one exclusive scan of the
+// counts (classes descending, chunks ascending), and a scatter that writes
+// every tile straight into its launch slot.
 #include "common.h"
 #include "launch.h"
 
 namespace sa {
 namespace {
 
-constexpr int kSchedThreads = 1024;
 constexpr int kClasses = 16;
 constexpr int kXcds = 8;
-constexpr int kRun = 64;  // consecutive list positions handed to one XCD
+constexpr int kRun = 64;           // consecutive list positions handed to one XCD
+constexpr int kChunk = 1024;       // tiles per counting / scatter workgroup
+constexpr int kSortThreads = 256;  // 4 waves x 4 rounds of 64 tiles
+constexpr int kScanThreads = 1024;
 
 __device__ __forceinline__ int cost_class(int tiles) {
   // 0 for empty tiles; otherwise 1 + floor(log2(tiles)), capped.  Larger = costlier.
@@ -29,85 +34,146 @@ __device__ __forceinline__ int cost_class(int tiles) {
   return c < kClasses ? c : kClasses - 1;
 }
 
-// Position in the cost-sorted list that launch slot `b` (of G) takes.
-__device__ __forceinline__ int slot_to_pos(int b, int G) {
-  const int group = kXcds * kRun;
-  const int full = (G / group) * group;
-  if (b >= full) return b;
-  const int x = b % kXcds, r = b / kXcds;
-  return (r / kRun) * group + x * kRun + (r % kRun);
+struct SchedArgs {
+  const int32_t* cnt;
+  int kmax, nb, ntiles, block, G, chunks;
+};
+
+__device__ __forceinline__ int class_of(const SchedArgs& a, int item) {
+  const int bh = item / a.ntiles, qt = item - bh * a.ntiles;
+  const int c = a.cnt[(int64_t)bh * a.nb + (qt * kTile) / a.block];
+  return cost_class(min(max(c, 0), a.kmax) * (a.block / kTile));
 }
 
-// Classes of up to this many tiles are kept in LDS (one byte each) between
-// the histogram and the scatter pass; larger launches recompute them.
-constexpr int kClassCache = 64 * 1024;
+// Launch slot that takes sorted position `pos` (of G): the inverse of the
+// interleave that gives XCD x (slot % 8) runs of kRun consecutive positions;
+// the positions of the last partial group keep their own slot.
+__device__ __forceinline__ int pos_to_slot(int pos, int G) {
+  const int group = kXcds * kRun;
+  const int full = (G / group) * group;
+  if (pos >= full) return pos;
+  const int g = pos / group, rem = pos - g * group;
+  const int x = rem / kRun, rr = rem - x * kRun;
+  return (g * kRun + rr) * kXcds + x;
+}
 
-__global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* __restrict__ cnt,
-                                                                 int kmax, int nb, int ntiles,
-                                                                 int block, int G,
-                                                                 int32_t* __restrict__ list,
-                                                                 int32_t* __restrict__ order) {
-  __shared__ int hist[kClasses];
-  __shared__ int base[kClasses];
-  __shared__ int wave_cnt[kSchedThreads / kWave][kClasses];
-  __shared__ uint8_t cls_cache[kClassCache];
+// counts[chunk][c] = tiles of class c in the chunk.
+__global__ __launch_bounds__(kSortThreads) void sched_count_kernel(SchedArgs a,
+                                                                   int32_t* __restrict__ counts) {
+  __shared__ int wave_cnt[kSortThreads / kWave][kClasses];
   const int t = threadIdx.x, lane = t & (kWave - 1), wave = t / kWave;
-  const int spb = block / kTile;
-  const bool cached = G <= kClassCache;
-  if (t < kClasses) hist[t] = 0;
-  __syncthreads();
-
-  auto cls_of = [&](int item) {
-    const int bh = item / ntiles, qt = item - bh * ntiles;
-    const int c = cnt[(int64_t)bh * nb + (qt * kTile) / block];
-    return cost_class(min(max(c, 0), kmax) * spb);
-  };
-
-  // Histogram pass: the loads of all items are independent, so they overlap.
-  for (int it = t; it < G; it += kSchedThreads) {
-    const int c = cls_of(it);
-    if (cached) cls_cache[it] = (uint8_t)c;
-    atomicAdd(&hist[c], 1);
-  }
-  __syncthreads();
-  if (t == 0) {
-    int acc = 0;
-    for (int c = kClasses - 1; c >= 0; --c) {  // costliest class first
-      base[c] = acc;
-      acc += hist[c];
-    }
-  }
-  __syncthreads();
-
-  const uint64_t below = lanes_below_mask();
-  for (int c0 = 0; c0 < G; c0 += kSchedThreads) {
-    const int it = c0 + t;
-    const int cls = it < G ? (cached ? (int)cls_cache[it] : cls_of(it)) : -1;
-    int rank = 0;
+  int mine = 0;  // lane c of each wave keeps the wave's count of class c
+#pragma unroll
+  for (int m = 0; m < kChunk / kSortThreads; ++m) {
+    const int it = blockIdx.x * kChunk + m * kSortThreads + t;
+    const int cls = it < a.G ? class_of(a, it) : -1;
 #pragma unroll
     for (int c = 0; c < kClasses; ++c) {
-      const uint64_t m = __ballot(cls == c);
-      if (cls == c) rank = __popcll(m & below);
-      if (lane == 0) wave_cnt[wave][c] = __popcll(m);
+      const int n = __popcll(__ballot(cls == c));
+      if (lane == c) mine += n;
     }
+  }
+  if (lane < kClasses) wave_cnt[wave][lane] = mine;
+  __syncthreads();
+  if (t < kClasses) {
+    int tot = 0;
+#pragma unroll
+    for (int w = 0; w < kSortThreads / kWave; ++w) tot += wave_cnt[w][t];
+    counts[(int64_t)blockIdx.x * kClasses + t] = tot;
+  }
+}
+
+// In place: counts[chunk][c] becomes the number of class-c tiles in earlier
+// chunks; counts[chunks][c] receives the first sorted position of class c
+// (classes in descending order).  One workgroup.
+__global__ __launch_bounds__(kScanThreads) void sched_scan_kernel(int chunks,
+                                                                  int32_t* __restrict__ counts) {
+  __shared__ int wsum[kScanThreads / kWave][kClasses];
+  __shared__ int carry[kClasses];
+  const int t = threadIdx.x, lane = t & (kWave - 1), wave = t / kWave;
+  if (t < kClasses) carry[t] = 0;
+  __syncthreads();
+  for (int ch0 = 0; ch0 < chunks; ch0 += kScanThreads) {
+    const int ch = ch0 + t;
+    int v[kClasses], incl[kClasses];
+#pragma unroll
+    for (int c = 0; c < kClasses; ++c) {
+      v[c] = ch < chunks ? counts[(int64_t)ch * kClasses + c] : 0;
+      incl[c] = v[c];
+    }
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1)
+#pragma unroll
+      for (int c = 0; c < kClasses; ++c) {
+        const int y = __shfl_up(incl[c], o, kWave);
+        if (lane >= o) incl[c] += y;
+      }
+    if (lane == kWave - 1)
+#pragma unroll
+      for (int c = 0; c < kClasses; ++c) wsum[wave][c] = incl[c];
     __syncthreads();
-    if (cls >= 0) {
-      int pos = base[cls] + rank;
-      for (int w = 0; w < wave; ++w) pos += wave_cnt[w][cls];
-      list[pos] = it;
+    if (ch < chunks) {
+#pragma unroll
+      for (int c = 0; c < kClasses; ++c) {
+        int before = carry[c];
+        for (int w = 0; w < wave; ++w) before += wsum[w][c];
+        counts[(int64_t)ch * kClasses + c] = before + incl[c] - v[c];
+      }
     }
     __syncthreads();
     if (t < kClasses) {
       int tot = 0;
-      for (int w = 0; w < kSchedThreads / kWave; ++w) tot += wave_cnt[w][t];
-      base[t] += tot;
+      for (int w = 0; w < kScanThreads / kWave; ++w) tot += wsum[w][t];
+      carry[t] += tot;
     }
     __syncthreads();
   }
-  // list[] is complete; every thread of this single workgroup can read it now.
-  __threadfence_block();
-  __syncthreads();
-  for (int b = t; b < G; b += kSchedThreads) order[b] = list[slot_to_pos(b, G)];
+  if (t == 0) {
+    int acc = 0;
+    for (int c = kClasses - 1; c >= 0; --c) {  // costliest class first
+      counts[(int64_t)chunks * kClasses + c] = acc;
+      acc += carry[c];
+    }
+  }
+}
+
+// Each tile's sorted position = class start + class-c tiles in earlier chunks
+// + class-c tiles before it in this chunk; written to order[slot(position)].
+__global__ __launch_bounds__(kSortThreads) void sched_scatter_kernel(
+    SchedArgs a, const int32_t* __restrict__ counts, int32_t* __restrict__ order) {
+  __shared__ int run[kClasses];
+  __shared__ int wave_cnt[kSortThreads / kWave][kClasses];
+  const int t = threadIdx.x, lane = t & (kWave - 1), wave = t / kWave;
+  if (t < kClasses)
+    run[t] = counts[(int64_t)a.chunks * kClasses + t] +
+             counts[(int64_t)blockIdx.x * kClasses + t];
+  const uint64_t below = lanes_below_mask();
+  for (int m = 0; m < kChunk / kSortThreads; ++m) {
+    // tiles of round m in index order: wave w holds the w-th 64 of them
+    const int it = blockIdx.x * kChunk + m * kSortThreads + t;
+    const int cls = it < a.G ? class_of(a, it) : -1;
+    int rank = 0;
+#pragma unroll
+    for (int c = 0; c < kClasses; ++c) {
+      const uint64_t msk = __ballot(cls == c);
+      if (cls == c) rank = __popcll(msk & below);
+      if (lane == c) wave_cnt[wave][c] = __popcll(msk);
+    }
+    __syncthreads();
+    if (cls >= 0) {
+      int pos = run[cls] + rank;
+      for (int w = 0; w < wave; ++w) pos += wave_cnt[w][cls];
+      order[pos_to_slot(pos, a.G)] = it;
+    }
+    __syncthreads();
+    if (t < kClasses) {
+      int tot = 0;
+#pragma unroll
+      for (int w = 0; w < kSortThreads / kWave; ++w) tot += wave_cnt[w][t];
+      run[t] += tot;
+    }
+    __syncthreads();
+  }
 }
 
 }  // namespace
@@ -117,16 +183,28 @@ int64_t num_query_tiles(const Shape& s) {
 }
 
 size_t schedule_workspace_bytes(const Shape& s) {
-  return (size_t)num_query_tiles(s) * sizeof(int32_t);
+  const int64_t chunks = (num_query_tiles(s) + kChunk - 1) / kChunk;
+  return (size_t)(chunks + 1) * kClasses * sizeof(int32_t);
 }
 
 hipError_t launch_schedule(const Shape& s, const int32_t* cnt, int kmax, int32_t* order,
                            void* ws, hipStream_t stream) {
-  const int ntiles = (s.N + kTile - 1) / kTile;
-  const int G = (int)num_query_tiles(s);
-  int32_t* list = static_cast<int32_t*>(ws);
-  schedule_kernel<<<1, kSchedThreads, 0, stream>>>(cnt, kmax, s.nb, ntiles, s.block, G, list,
-                                                   order);
+  SchedArgs a;
+  a.cnt = cnt;
+  a.kmax = kmax;
+  a.nb = s.nb;
+  a.ntiles = (s.N + kTile - 1) / kTile;
+  a.block = s.block;
+  a.G = (int)num_query_tiles(s);
+  a.chunks = (a.G + kChunk - 1) / kChunk;
+  int32_t* counts = static_cast<int32_t*>(ws);
+  sched_count_kernel<<<a.chunks, kSortThreads, 0, stream>>>(a, counts);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  sched_scan_kernel<<<1, kScanThreads, 0, stream>>>(a.chunks, counts);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  sched_scatter_kernel<<<a.chunks, kSortThreads, 0, stream>>>(a, counts, order);
   return hipGetLastError();
 }
 

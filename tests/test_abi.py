@@ -61,11 +61,21 @@ def test_workspace_size_formula():
     nb = 1182
     assert lib.sparse_attn_workspace_size(ctypes.byref(ds), 0, 36) == \
         40 * nb * 128 * 8 * 2 + 40 * nb * nb * 8
-    assert lib.sparse_attn_workspace_size(ctypes.byref(ds), 1, 36) == 40 * 1182 * 4
+    # scheduler: 16 class counters per chunk of 1024 query tiles, plus one row
+    assert lib.sparse_attn_workspace_size(ctypes.byref(ds), 1, 36) == (47 + 1) * 16 * 4
     assert lib.sparse_attn_workspace_size(ctypes.byref(ds), 1, 0) == 0
     assert lib.sparse_attn_workspace_size(ctypes.byref(ds), 7, 36) == 0
     assert lib.sparse_attn_workspace_size(ctypes.byref(desc(d=64)), 0, 1) == 0
     assert lib.sparse_attn_workspace_size(None, 0, 1) == 0
+
+
+def test_tile_count_limit():
+    # B*H*ceil(L/64) query tiles must stay <= 2^30 (32-bit tile indices), also
+    # when B*H*nkb does (block 128 halves nkb but not the 64-row tiles)
+    lib = sa.library()
+    assert lib.sparse_attn_num_tiles(ctypes.byref(desc(H=131072, N=524288, block=128))) == \
+        131072 * 8192
+    assert lib.sparse_attn_num_tiles(ctypes.byref(desc(H=131073, N=524288, block=128))) == -1
 
 
 # Fake, aligned, non-null device addresses: every call below must fail its
@@ -127,7 +137,7 @@ def test_schedule_rejects_bad_arguments():
     assert lib.sparse_attn_num_tiles(ctypes.byref(ds)) == 2 * 3 * 16
     assert lib.sparse_attn_num_tiles(ctypes.byref(desc(block=96))) == -1
     need = lib.sparse_attn_workspace_size(ctypes.byref(ds), 1, 7)
-    assert need == 2 * 3 * 16 * 4
+    assert need == (1 + 1) * 16 * 4                                   # one chunk of 96 tiles
     call = lambda *a: lib.sparse_attn_schedule(ctypes.byref(ds), *a)
     assert call(None, 7, P, P, need, None) == -1                    # null cnt
     assert call(P, 7, None, P, need, None) == -1                    # null order

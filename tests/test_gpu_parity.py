@@ -79,6 +79,23 @@ def test_select_ties_and_signed_zeros():
     select_and_check(q2, k2, 64, 5000, "duplicate-block ties")
 
 
+def test_select_low_word_ties():
+    """Block scores that agree in the high 32 bits of their fp64 order keys
+    and differ only in the low bits (relative gaps ~4e-9), with exact ties
+    among them: the top-k must still follow the full fp64 order."""
+    nb, block = 16, 64
+    q = torch.zeros(1, 1, nb * block, 128)
+    q[..., 0] = 1.0                          # score_ij = mean of k[:, 0] over block j
+    k = torch.zeros(1, 1, nb * block, 128)
+    k[0, 0, :, 0] = 2.0 ** 14
+    for j in range(nb):
+        rank = (7 * j) % nb // 2             # pairs of blocks share a rank: exact ties
+        k[0, 0, j * block, 0] = rank * 2.0 ** -8
+    q, k = q.to(torch.bfloat16), k.to(torch.bfloat16)
+    for keep in (1000, 2500, 5000, 7000):
+        select_and_check(q, k, block, keep, f"low-word ties keep={keep}")
+
+
 @pytest.mark.parametrize("N,block,keep_bp", [(4096, 128, 1000), (777, 64, 3000),
                                              (64, 64, 100), (8200, 128, 10000)])
 def test_select_shapes(N, block, keep_bp):
