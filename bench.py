@@ -18,6 +18,7 @@ bounded sample of the same workload.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -33,6 +34,31 @@ METRIC = "ms/call + dense-equiv TFLOP/s and % MFMA peak, block-sparse attn @97%"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_FP8_TFLOPS = 5000.0    # MI355X dense fp8 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "fwd_bf16_wan14b_720p_hbm_traffic.txt")
+FWD_BF16_SOURCES = ("fwd_bf16.hip", "common.h", "launch.h")
+
+
+def measured_traffic(workload):
+    """HBM bytes per launch of fwd_bf16_kernel from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE summary (copy-calibrated), or None when that
+    summary does not cover this workload or the kernel sources have changed
+    since the counters were taken."""
+    if workload != "wan14b_720p" or not os.path.exists(TRAFFIC_PROFILE):
+        return None
+    kv = {}
+    for line in open(TRAFFIC_PROFILE):
+        if not line.startswith("#") and ":" in line:
+            key, val = line.split(":", 1)
+            kv[key.strip()] = val.strip()
+    h = hashlib.sha256()
+    for f in FWD_BF16_SOURCES:
+        with open(os.path.join(ROOT, "paper_2609_23153_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    if kv.get("fwd_bf16_source_sha256") != h.hexdigest():
+        return None
+    return int(float(kv["traffic_bytes_per_launch"]))
 
 
 def parse_args():
@@ -137,7 +163,8 @@ def bench_fp8(args, sa, W, dev):
         "quant_gbs": round(qbytes / (ms[1] * 1e-3) / 1e9, 1),
         "roofline": {"kernel": "fwd_fp8_kernel", "bound": "mfma", "achieved": round(tf, 2),
                      "peak": PEAK_FP8_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(tf / PEAK_FP8_TFLOPS, 4), "flops_per_launch": flops},
+                     "frac": round(tf / PEAK_FP8_TFLOPS, 4), "traffic": None,
+                     "flops_per_launch": flops},
     }
 
 
@@ -229,8 +256,11 @@ def main():
         "roofline": {
             "kernel": "fwd_bf16_kernel", "bound": "mfma",
             "achieved": round(fwd_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-            "frac": round(fwd_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+            "frac": round(fwd_tflops / PEAK_BF16_TFLOPS, 4),
+            "traffic": measured_traffic(wl.name),
             "flops_per_launch": flops,
+            "algorithmic_bytes_per_launch": 4 * B * H * N * d * 2 + B * H * N * 4
+                                            + B * H * nb * (k + 1) * 4,
         },
     }
 
