@@ -115,18 +115,29 @@ def select_row_topk(scores: np.ndarray, k: int) -> np.ndarray:
     return np.stack([topk_ascending(scores[i], k) for i in range(nqb)]).astype(np.int32)
 
 
-def select_head_topk(scores: np.ndarray, keep_bp: int):
+def head_pair_budget(keep_bp: int, nqb: int, nkb: int) -> int:
+    """Pairs kept per head by the ragged selection: ceil(keep_bp * nqb * nkb
+    / 10000) in integers, clamped to [nqb, nqb * nkb] (every query block keeps
+    at least its best key block)."""
+    total = -(-keep_bp * nqb * nkb // 10000)
+    return int(min(max(total, nqb), nqb * nkb))
+
+
+def select_head_topk(scores: np.ndarray, keep_bp: int = None, kmax: int = None,
+                     budget: int = None):
     """Ragged selection over a whole head (a reading for ragged per-query-block
     work; the paper only fixes sparsity as a global block fraction, §2).
 
-    K = ceil(keep_bp * nqb * nkb / 10000) pairs are kept, clamped to
-    [nqb, nqb*nkb]: first every query block's best key block, then the
-    remaining K - nqb pairs by (score desc, i asc, j asc) among pairs not yet
-    taken.  Returns (idx [nqb, kmax] padded with -1, cnt [nqb]) where kmax is
+    K pairs are kept (``budget``, else head_pair_budget(keep_bp, ...)): first
+    every query block's best key block, then the remaining K - nqb pairs by
+    (score desc, i asc, j asc) among pairs not yet taken.  With ``kmax`` given
+    (the fixed row stride of an index list), a row that would keep more than
+    kmax pairs keeps only its kmax best by (score desc, j asc).  Returns
+    (idx [nqb, w] padded with -1, cnt [nqb]) where w is kmax if given, else
     the largest cnt."""
     nqb, nkb = scores.shape
-    total = -(-keep_bp * nqb * nkb // 10000)
-    total = int(min(max(total, nqb), nqb * nkb))
+    total = budget if budget is not None else head_pair_budget(keep_bp, nqb, nkb)
+    assert nqb <= total <= nqb * nkb
     taken = np.zeros((nqb, nkb), dtype=bool)
     for i in range(nqb):
         taken[i, topk_ascending(scores[i], 1)[0]] = True
@@ -140,9 +151,17 @@ def select_head_topk(scores: np.ndarray, keep_bp: int):
         if not taken[ii[p], jj[p]]:
             taken[ii[p], jj[p]] = True
             need -= 1
+    if kmax is not None:
+        for i in range(nqb):
+            sel = np.nonzero(taken[i])[0]
+            if sel.size > kmax:
+                # the kmax best of the row's kept pairs, (score desc, j asc)
+                best = sel[np.lexsort((sel, -scores[i, sel]))[:kmax]]
+                taken[i] = False
+                taken[i, best] = True
     cnt = taken.sum(axis=1).astype(np.int32)
-    kmax = int(cnt.max())
-    idx = np.full((nqb, kmax), -1, dtype=np.int32)
+    width = kmax if kmax is not None else int(cnt.max())
+    idx = np.full((nqb, width), -1, dtype=np.int32)
     for i in range(nqb):
         sel = np.nonzero(taken[i])[0]
         idx[i, :sel.size] = sel

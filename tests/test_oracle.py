@@ -153,6 +153,32 @@ def test_head_topk_invariants():
     assert max(key(p) for p in extra) < min(key(p) for p in unchosen)
 
 
+def test_head_topk_rows_are_row_prefixes_and_cap():
+    """Each row's ragged selection is the row's own top-cnt_i under
+    (score desc, j asc) -- the property the GPU path reduces the mode to --
+    and a row stride kmax keeps the kmax best of a longer row."""
+    rng = np.random.default_rng(11)
+    for trial in range(20):
+        nqb, nkb = rng.integers(2, 9), rng.integers(2, 11)
+        s = rng.integers(-4, 5, size=(nqb, nkb)).astype(np.float64)   # many ties
+        budget = int(rng.integers(nqb, nqb * nkb + 1))
+        idx, cnt = O.select_head_topk(s, budget=budget)
+        assert cnt.sum() == budget
+        for i in range(nqb):
+            assert idx[i, :cnt[i]].tolist() == O.topk_ascending(s[i], int(cnt[i])).tolist()
+        kmax = int(rng.integers(1, nkb + 1))
+        ci, cc = O.select_head_topk(s, budget=budget, kmax=kmax)
+        assert ci.shape == (nqb, kmax)
+        assert cc.tolist() == np.minimum(cnt, kmax).tolist()
+        for i in range(nqb):
+            assert ci[i, :cc[i]].tolist() == O.topk_ascending(s[i], int(cc[i])).tolist()
+            assert (ci[i, cc[i]:] == -1).all()
+    # budget from a keep ratio
+    assert O.head_pair_budget(3000, 7, 9) == 19
+    assert O.head_pair_budget(1, 7, 9) == 7
+    assert O.head_pair_budget(10000, 7, 9) == 63
+
+
 # ----------------------------------------------------------------- attention
 def _dense_sdpa(q, k, v, tau):
     qt, kt, vt = (torch.from_numpy(x)[None, None] for x in (q, k, v))
