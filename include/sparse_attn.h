@@ -105,8 +105,10 @@ size_t sparse_attn_workspace_size(const sparse_attn_desc* desc, int32_t op, int3
  *          SA_SELECT_HEAD_TOPK: per (batch, head), `budget` block pairs in
  *          total (nqb <= budget <= nqb * nkb): every query block first keeps
  *          its best key block, then the remaining pairs go by (score desc,
- *          query block asc, key block asc); a row keeps at most kmax blocks
- *          (kmax >= 1), pairs beyond that are dropped.
+ *          query block asc, key block asc).  A row that would keep more than
+ *          kmax blocks (kmax >= 1, the list stride) keeps its kmax best by
+ *          (score desc, key block asc); the pairs so dropped are not
+ *          replaced, so cnt then sums to less than budget.
  *  idx     int32 [B][H][nqb][kmax] out: kept key-block indices, strictly
  *          ascending in the first cnt entries, -1 after them
  *  cnt     int32 [B][H][nqb] out: number of kept blocks per query block

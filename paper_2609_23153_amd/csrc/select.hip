@@ -1,8 +1,8 @@
 // Block selection M_phi on gfx950 (paper §2 Eq. comp-sparse; selection kept
 // in BF16 inputs per §4.3): mean-pooled block scores and per-query-block
-// top-k with ties to the lower block index.
+// top-k with ties to the lower block index, or the ragged whole-head variant.
 //
-// Three launches:
+// Launches:
 //   pool   : Q and K streamed once from HBM; per block, the fp64 sum of the
 //            bf16 token vectors (exact for bf16 inputs whose exponents span
 //            fewer than ~38 binades, so it does not depend on summation order)
@@ -12,6 +12,9 @@
 //            order-preserving 64-bit keys (high word first, then the low word
 //            of the keys tied there) finds the k-th largest score, then
 //            ballots emit the kept block indices in ascending order.
+//   whole-head mode: row bests, an 8-pass radix select of the global
+//            threshold key per head, per-row counts and a scan, then the row
+//            top-k with a per-row k (see the comment above head_init_kernel).
 #include "common.h"
 #include "launch.h"
 
@@ -226,12 +229,14 @@ __device__ __forceinline__ uint32_t kth_largest32(const uint32_t (&v)[KPL], cons
 // tie with it there take part in the search over the low 32 bits.
 template <int KPL>
 __global__ __launch_bounds__(256) void topk_row_kernel(const double* __restrict__ scores,
-                                                       int nb, int rows, int k, int kmax,
-                                                       int32_t* __restrict__ idx,
+                                                       int nb, int rows, int k_all, int kmax,
+                                                       bool k_per_row, int32_t* __restrict__ idx,
                                                        int32_t* __restrict__ cnt) {
   const int lane = threadIdx.x & (kWave - 1);
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= rows) return;  // uniform per wave
+  // the row's k: one value for all rows, or (ragged mode) read from cnt
+  const int k = k_per_row ? __builtin_amdgcn_readfirstlane(cnt[row]) : k_all;
   const double* s = scores + (int64_t)row * nb;
   uint32_t hi[KPL], lo[KPL];
   bool valid[KPL];
@@ -290,17 +295,236 @@ __global__ __launch_bounds__(256) void topk_row_kernel(const double* __restrict_
 }
 
 template <int KPL>
-hipError_t launch_topk(const double* scores, int nb, int rows, int k, int kmax, int32_t* idx,
-                       int32_t* cnt, hipStream_t stream) {
-  topk_row_kernel<KPL><<<(rows + 3) / 4, 256, 0, stream>>>(scores, nb, rows, k, kmax, idx, cnt);
+hipError_t launch_topk(const double* scores, int nb, int rows, int k, int kmax, bool k_per_row,
+                       int32_t* idx, int32_t* cnt, hipStream_t stream) {
+  topk_row_kernel<KPL><<<(rows + 3) / 4, 256, 0, stream>>>(scores, nb, rows, k, kmax, k_per_row,
+                                                            idx, cnt);
   return hipGetLastError();
+}
+
+// Row top-k over the score matrix with the register tile that fits nb.
+hipError_t launch_topk_any(const double* scores, int nb, int rows, int k, int kmax,
+                           bool k_per_row, int32_t* idx, int32_t* cnt, hipStream_t stream) {
+  const int kpl = (nb + kWave - 1) / kWave;
+#define SA_TOPK(n) \
+  if (kpl <= n) return launch_topk<n>(scores, nb, rows, k, kmax, k_per_row, idx, cnt, stream);
+  SA_TOPK(1) SA_TOPK(2) SA_TOPK(4) SA_TOPK(8) SA_TOPK(12) SA_TOPK(16) SA_TOPK(20) SA_TOPK(24)
+  SA_TOPK(32)
+#undef SA_TOPK
+  return launch_topk<64>(scores, nb, rows, k, kmax, k_per_row, idx, cnt, stream);
+}
+
+// ---- whole-head ragged selection ------------------------------------------
+// Per (batch, head): every query block keeps its best key block; the other
+// (budget - nqb) pairs are the largest of the remaining ones under (score
+// desc, i asc, j asc).  Within a row, the pairs so kept are always a prefix of
+// the row's own order (score desc, j asc), so the mode reduces to a per-row
+// count c_i followed by the row top-k with k_i = min(c_i, kmax):
+//   top1   : each row's best key block (excluded from the global ranking)
+//   radix  : the (budget - nqb)-th largest order key T among the remaining
+//            pairs, by 8 passes of 8 bits (a 256-bin histogram, then one
+//            workgroup per head picks the digit), and the number r of pairs
+//            equal to T that are kept (those first in (i, j) order)
+//   counts : per row, remaining pairs with key > T and with key == T
+//   row k  : c_i = 1 + above_i + clamp(r - (ties in rows < i), 0, ties_i)
+struct HeadState {
+  unsigned long long prefix;  // radix prefix; T after the last pass
+  long long need;             // rank still to find among the keys == prefix
+  int none;                   // no pair beyond the row bests is kept
+  int pad[3];
+};
+constexpr int kBins = 256;
+
+struct HeadWs {
+  HeadState* st;    // [BH]
+  uint32_t* hist;   // [BH][256]
+  int32_t* top1;    // [rows]
+  int32_t* above;   // [rows]
+  int32_t* ties;    // [rows]
+};
+
+__global__ __launch_bounds__(kBins) void head_init_kernel(HeadWs w, long long rest) {
+  const int bh = blockIdx.x;
+  w.hist[bh * kBins + threadIdx.x] = 0u;
+  if (threadIdx.x == 0) {
+    w.st[bh].prefix = 0ull;
+    w.st[bh].need = rest;
+    w.st[bh].none = rest == 0;
+  }
+}
+
+// One wave per row: the largest key, lowest index first.
+__global__ __launch_bounds__(256) void row_top1_kernel(const double* __restrict__ scores, int nb,
+                                                       int rows, int32_t* __restrict__ top1) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const double* s = scores + (int64_t)row * nb;
+  uint64_t best = 0ull;  // below every finite score
+  int bj = nb;
+  for (int j = lane; j < nb; j += kWave) {
+    const uint64_t key = order_key(s[j]);
+    if (key > best) {  // ascending j within the lane: ties keep the first
+      best = key;
+      bj = j;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const uint64_t ok = __shfl_xor(best, o, kWave);
+    const int oj = __shfl_xor(bj, o, kWave);
+    if (ok > best || (ok == best && oj < bj)) {
+      best = ok;
+      bj = oj;
+    }
+  }
+  if (lane == 0) top1[row] = bj;
+}
+
+// Histogram of the next 8-bit digit (bits shift..shift+7) of the order keys
+// of the remaining pairs that match the prefix found so far.  Blocks of 4
+// rows; equal digits of a wave are counted with one ballot and one LDS add.
+__global__ __launch_bounds__(256) void head_hist_kernel(const double* __restrict__ scores, int nb,
+                                                        HeadWs w, int shift) {
+  __shared__ uint32_t h[kBins];
+  const int bh = blockIdx.y;
+  if (w.st[bh].none) return;  // uniform per workgroup
+  const uint64_t prefix = w.st[bh].prefix;
+  const uint64_t mask = shift == 56 ? 0ull : ~0ull << (shift + 8);
+  h[threadIdx.x] = 0u;
+  __syncthreads();
+  const int lane = threadIdx.x & (kWave - 1);
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (i < nb) {
+    const int64_t row = (int64_t)bh * nb + i;
+    const double* s = scores + row * nb;
+    const int skip = w.top1[row];
+    for (int j0 = 0; j0 < nb; j0 += kWave) {
+      const int j = j0 + lane;
+      bool act = false;
+      uint32_t bin = 0;
+      if (j < nb && j != skip) {
+        const uint64_t key = order_key(s[j]);
+        act = (key & mask) == (prefix & mask);
+        bin = (uint32_t)(key >> shift) & (kBins - 1);
+      }
+      uint64_t left = __ballot(act);
+      while (left) {
+        const int first = __ffsll((long long)left) - 1;
+        const uint32_t b = __shfl(bin, first, kWave);
+        const uint64_t same = __ballot(act && bin == b);
+        if (lane == first) atomicAdd(&h[b], (uint32_t)__popcll(same));
+        left &= ~same;
+        if (act && bin == b) act = false;
+      }
+    }
+  }
+  __syncthreads();
+  const uint32_t c = h[threadIdx.x];
+  if (c) atomicAdd(&w.hist[bh * kBins + threadIdx.x], c);
+}
+
+// One workgroup per head: the digit that holds the need-th largest key,
+// scanning bins from the top; clears the histogram for the next pass.
+__global__ __launch_bounds__(kBins) void head_radix_step_kernel(HeadWs w, int shift) {
+  __shared__ uint32_t wsum[kBins / kWave];
+  const int bh = blockIdx.x, t = threadIdx.x, lane = t & (kWave - 1), wave = t / kWave;
+  const int d = kBins - 1 - t;  // thread t holds bin d: t ascending = digit descending
+  const uint32_t c = w.hist[bh * kBins + d];
+  w.hist[bh * kBins + d] = 0u;
+  if (w.st[bh].none) return;  // uniform per workgroup
+  uint32_t incl = c;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const uint32_t y = __shfl_up(incl, o, kWave);
+    if (lane >= o) incl += y;
+  }
+  if (lane == kWave - 1) wsum[wave] = incl;
+  __syncthreads();
+  for (int v = 0; v < wave; ++v) incl += wsum[v];
+  const long long need = w.st[bh].need;
+  const long long excl = (long long)incl - c;  // keys in higher digits
+  __syncthreads();
+  if (c > 0 && excl < need && (long long)incl >= need) {
+    w.st[bh].prefix |= (unsigned long long)d << shift;
+    w.st[bh].need = need - excl;
+  }
+}
+
+// One wave per row: remaining pairs above and equal to the threshold key.
+__global__ __launch_bounds__(256) void head_count_kernel(const double* __restrict__ scores, int nb,
+                                                         int rows, HeadWs w) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int bh = row / nb;
+  int above = 0, ties = 0;
+  if (!w.st[bh].none) {
+    const uint64_t T = w.st[bh].prefix;
+    const double* s = scores + (int64_t)row * nb;
+    const int skip = w.top1[row];
+    for (int j0 = 0; j0 < nb; j0 += kWave) {
+      const int j = j0 + lane;
+      uint64_t key = 0ull;
+      if (j < nb && j != skip) key = order_key(s[j]);
+      above += __popcll(__ballot(key > T));
+      ties += __popcll(__ballot(key == T && key != 0ull));
+    }
+  }
+  if (lane == 0) {
+    w.above[row] = above;
+    w.ties[row] = ties;
+  }
+}
+
+// One workgroup per head: the ties at T are kept first in row order, so row i
+// keeps clamp(r - ties in earlier rows, 0, ties_i) of them.  Writes each row's
+// k = min(c_i, kmax) into cnt (read back by the row top-k).
+constexpr int kRowKThreads = 1024;
+__global__ __launch_bounds__(kRowKThreads) void head_rowk_kernel(int nb, int kmax, HeadWs w,
+                                                                 int32_t* __restrict__ cnt) {
+  __shared__ long long wsum[kRowKThreads / kWave];
+  __shared__ long long carry;
+  const int bh = blockIdx.x, t = threadIdx.x, lane = t & (kWave - 1), wave = t / kWave;
+  const long long r = w.st[bh].none ? 0 : w.st[bh].need;
+  if (t == 0) carry = 0;
+  __syncthreads();
+  for (int i0 = 0; i0 < nb; i0 += kRowKThreads) {
+    const int i = i0 + t;
+    const int64_t row = (int64_t)bh * nb + i;
+    const long long e = i < nb ? w.ties[row] : 0;
+    long long incl = e;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const long long y = __shfl_up(incl, o, kWave);
+      if (lane >= o) incl += y;
+    }
+    if (lane == kWave - 1) wsum[wave] = incl;
+    __syncthreads();
+    long long before = carry + incl - e;
+    for (int v = 0; v < wave; ++v) before += wsum[v];
+    if (i < nb) {
+      const long long take = min(max(r - before, 0ll), e);
+      const long long c = 1 + (long long)w.above[row] + take;
+      cnt[row] = (int32_t)min(c, (long long)kmax);
+    }
+    __syncthreads();
+    if (t == 0) {
+      long long tot = 0;
+      for (int v = 0; v < kRowKThreads / kWave; ++v) tot += wsum[v];
+      carry += tot;
+    }
+    __syncthreads();
+  }
 }
 
 }  // namespace
 
 size_t select_workspace_bytes(const Shape& s) {
   const size_t bh = (size_t)s.B * s.H;
-  return bh * s.nb * kHeadDim * sizeof(double) * 2 + bh * s.nb * s.nb * sizeof(double);
+  const size_t rows = bh * s.nb;
+  return bh * s.nb * kHeadDim * sizeof(double) * 2 + bh * s.nb * s.nb * sizeof(double) +
+         bh * sizeof(HeadState) + bh * kBins * sizeof(uint32_t) + 3 * rows * sizeof(int32_t);
 }
 
 static hipError_t launch_pool_score(const Shape& s, const void* q, Strides qs, const void* k,
@@ -329,22 +553,35 @@ hipError_t launch_select_row(const Shape& s, const void* q, Strides qs, const vo
   hipError_t e = launch_pool_score(s, q, qs, k, ks, ws, &scores, stream);
   if (e != hipSuccess) return e;
   const int rows = s.B * s.H * s.nb;
-  const int kpl = (s.nb + kWave - 1) / kWave;
-  if (kpl <= 1) return launch_topk<1>(scores, s.nb, rows, topk, kmax, idx, cnt, stream);
-  if (kpl <= 2) return launch_topk<2>(scores, s.nb, rows, topk, kmax, idx, cnt, stream);
-  if (kpl <= 4) return launch_topk<4>(scores, s.nb, rows, topk, kmax, idx, cnt, stream);
-  if (kpl <= 8) return launch_topk<8>(scores, s.nb, rows, topk, kmax, idx, cnt, stream);
-  if (kpl <= 12) return launch_topk<12>(scores, s.nb, rows, topk, kmax, idx, cnt, stream);
-  if (kpl <= 16) return launch_topk<16>(scores, s.nb, rows, topk, kmax, idx, cnt, stream);
-  if (kpl <= 20) return launch_topk<20>(scores, s.nb, rows, topk, kmax, idx, cnt, stream);
-  if (kpl <= 24) return launch_topk<24>(scores, s.nb, rows, topk, kmax, idx, cnt, stream);
-  if (kpl <= 32) return launch_topk<32>(scores, s.nb, rows, topk, kmax, idx, cnt, stream);
-  return launch_topk<64>(scores, s.nb, rows, topk, kmax, idx, cnt, stream);
+  return launch_topk_any(scores, s.nb, rows, topk, kmax, false, idx, cnt, stream);
 }
 
-hipError_t launch_select_head(const Shape&, const void*, Strides, const void*, Strides,
-                              int64_t, int, int32_t*, int32_t*, void*, hipStream_t) {
-  return hipErrorNotSupported;
+hipError_t launch_select_head(const Shape& s, const void* q, Strides qs, const void* k,
+                              Strides ks, int64_t budget, int kmax, int32_t* idx, int32_t* cnt,
+                              void* ws, hipStream_t stream) {
+  double* scores = nullptr;
+  hipError_t e = launch_pool_score(s, q, qs, k, ks, ws, &scores, stream);
+  if (e != hipSuccess) return e;
+  const int bh = s.B * s.H;
+  const int rows = bh * s.nb;
+  HeadWs w;
+  w.st = reinterpret_cast<HeadState*>(scores + (size_t)rows * s.nb);
+  w.hist = reinterpret_cast<uint32_t*>(w.st + bh);
+  w.top1 = reinterpret_cast<int32_t*>(w.hist + (size_t)bh * kBins);
+  w.above = w.top1 + rows;
+  w.ties = w.above + rows;
+  head_init_kernel<<<bh, kBins, 0, stream>>>(w, (long long)(budget - s.nb));
+  row_top1_kernel<<<(rows + 3) / 4, 256, 0, stream>>>(scores, s.nb, rows, w.top1);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  for (int shift = 56; shift >= 0; shift -= 8) {
+    head_hist_kernel<<<dim3((s.nb + 3) / 4, bh), 256, 0, stream>>>(scores, s.nb, w, shift);
+    head_radix_step_kernel<<<bh, kBins, 0, stream>>>(w, shift);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  head_count_kernel<<<(rows + 3) / 4, 256, 0, stream>>>(scores, s.nb, rows, w);
+  head_rowk_kernel<<<bh, kRowKThreads, 0, stream>>>(s.nb, kmax, w, cnt);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  return launch_topk_any(scores, s.nb, rows, 0, kmax, true, idx, cnt, stream);
 }
 
 }  // namespace sa

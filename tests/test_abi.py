@@ -59,8 +59,10 @@ def test_workspace_size_formula():
     lib = sa.library()
     ds = desc(B=1, H=40, N=75600)
     nb = 1182
+    # pooled q/k (fp64), scores (fp64), then the whole-head mode's state: per
+    # head 32 B of radix state and a 256-bin histogram, per row 3 int32
     assert lib.sparse_attn_workspace_size(ctypes.byref(ds), 0, 36) == \
-        40 * nb * 128 * 8 * 2 + 40 * nb * nb * 8
+        40 * nb * 128 * 8 * 2 + 40 * nb * nb * 8 + 40 * 32 + 40 * 256 * 4 + 3 * 40 * nb * 4
     # scheduler: 16 class counters per chunk of 1024 query tiles, plus one row
     assert lib.sparse_attn_workspace_size(ctypes.byref(ds), 1, 36) == (47 + 1) * 16 * 4
     assert lib.sparse_attn_workspace_size(ctypes.byref(ds), 1, 0) == 0
