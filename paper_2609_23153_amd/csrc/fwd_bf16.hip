@@ -23,7 +23,9 @@
 //    already in the B-operand layout of the PV product.  The V^T A-operand is
 //    read from the row-major V tile with ds_read_b64_tr_b16.
 //  * Online softmax in fp32 registers with exp2 (tau*log2(e) folded into one
-//    FMA) and a lazily raised reference max.
+//    FMA) and a lazily raised reference max: the common tile costs one FMA
+//    and one exp2 per score, a bf16 pack per pair and a v_dot2 per pair for
+//    the row sum; the max is only taken on the tiles that raise it.
 // The two key-half waves of a row-half keep separate softmax states that are
 // merged through LDS at the end.
 #include "common.h"
@@ -36,7 +38,11 @@ constexpr int kThreads = 256;
 constexpr int kRowBytes = kHeadDim * 2;            // 256 B per bf16 row
 constexpr int kTileBytes = kTile * kRowBytes;      // 16 KB per K or V tile
 
-constexpr float kLazy = 8.f;  // log2 headroom before the accumulator is rescaled
+// A tile's probabilities are taken against the running reference max as it
+// stands; only when a lane's tile sum of them exceeds this bound (or is not
+// finite) is the max raised and the tile recomputed, so every probability
+// stays <= kSumCap.
+constexpr float kSumCap = 4096.f;
 
 // 16-byte-chunk swizzles (row = row within the tile): conflict-free for the
 // K A-operand reads (32 rows, one chunk) and the V transpose reads (4 rows x
@@ -44,8 +50,8 @@ constexpr float kLazy = 8.f;  // log2 headroom before the accumulator is rescale
 __device__ __forceinline__ int swz_k(int row, int chunk) { return chunk ^ (row & 15); }
 __device__ __forceinline__ int swz_v(int row, int chunk) { return chunk ^ ((row & 3) << 2); }
 
-typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((__vector_size__(4 * sizeof(short)))) short i16x4;
+typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2;
 
 struct Params {
   const uint16_t* q;
@@ -119,20 +125,42 @@ __device__ __forceinline__ void dma_tile(uint8_t* dst, __amdgpu_buffer_rsrc_t r,
 
 // s_waitcnt with the other counters at their maxima (no wait on them).
 __device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
-__device__ __forceinline__ void wait_vm12() { __builtin_amdgcn_s_waitcnt(0x0F7C); }
+__device__ __forceinline__ void wait_vm8() { __builtin_amdgcn_s_waitcnt(0x0F78); }
 __device__ __forceinline__ void wait_vm16() { __builtin_amdgcn_s_waitcnt(0x4F70); }
 __device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+// Probabilities 2^(s*c - m) of a lane's 16 scores packed to bf16 as the PV
+// B operand (k-step cs in pk[cs]), and their sum over those bf16 values
+// (v_dot2 against (1, 1)), so numerator and normaliser see the same numbers.
+__device__ __forceinline__ float tile_probs(const f32x16& s, float c, float m, bf16x8 (&pk)[2]) {
+  const bf16x2 one = {(__bf16)1.f, (__bf16)1.f};
+  float ts = 0.f;
+#pragma unroll
+  for (int cs = 0; cs < 2; ++cs) {
+    u32x4 w;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float a = __builtin_amdgcn_exp2f(fmaf(s[8 * cs + 2 * e], c, -m));
+      const float b = __builtin_amdgcn_exp2f(fmaf(s[8 * cs + 2 * e + 1], c, -m));
+      const bf16x2 t = {(__bf16)a, (__bf16)b};
+      w[e] = __builtin_bit_cast(uint32_t, t);
+      ts = __builtin_amdgcn_fdot2_f32_bf16(t, one, ts, false);
+    }
+    pk[cs] = __builtin_bit_cast(bf16x8, w);
+  }
+  return ts;
+}
 
 __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
   // Distinct LDS objects per buffer (rather than one array indexed by a
   // buffer number) keep every access at a constant base.
   __shared__ __attribute__((aligned(1024))) uint8_t kb0[kTileBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t kb1[kTileBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t kb2[kTileBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t vb0[kTileBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t vb1[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t vb2[kTileBytes];
 
   const int item = p.order ? p.order[blockIdx.x] : (int)blockIdx.x;
   const int bh = item / p.ntiles;
@@ -157,28 +185,28 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
   const auto vr = make_rsrc(p.v + b * p.vs.b + h * p.vs.h, (uint32_t)(p.N - 1) * vst + 256u);
   const DmaOffsets dofs = dma_offsets(kst, vst);
 
-  // Tile cursor: n / s0 = tile being computed, n1..n3 / s1..s3 = the next
-  // three valid tiles (total / N when there are none).  The list entry after n3 is read one step ahead.
-  int s0 = p.N, s1 = p.N, s2 = p.N, s3 = p.N;
+  // Tile cursor: n / s0 = tile being computed, n1, n2 / s1, s2 = the next
+  // two valid tiles (total / N when there are none).  The list entry after
+  // n2 is read one step ahead.
+  int s0 = p.N, s1 = p.N, s2 = p.N;
   int n = next_tile(list, 0, total, spb, p.block, p.nb, p.N, &s0);
   int n1 = next_tile(list, n + 1, total, spb, p.block, p.nb, p.N, &s1);
   int n2 = next_tile(list, n1 + 1, total, spb, p.block, p.nb, p.N, &s2);
-  int n3 = next_tile(list, n2 + 1, total, spb, p.block, p.nb, p.N, &s3);
 
-  // Prologue.  The Q tile is staged through kb2 (same swizzle as K), then
-  // K(0), V(0), K(1), V(1) are issued; once every wave holds its Q fragment,
-  // kb2 receives K(2).  Past the end of the list the starts equal N and the
-  // copies read zeros without touching memory, so every step issues the same
-  // number of copies and the vmcnt arithmetic below is uniform.
+  // Prologue.  The Q tile is staged through vb2 (same swizzle as K) while
+  // K(0), V(0), V(1), K(1) are issued; step 0 refills vb2 with V(2) once every
+  // wave holds its Q fragment.  Past the end of the list the starts equal N
+  // and the copies read zeros without touching memory, so every step issues
+  // the same number of copies and the vmcnt arithmetic below is uniform.
   {
     const auto qr = make_rsrc(p.q + b * p.qs.b + h * p.qs.h, (uint32_t)(p.N - 1) * qst + 256u);
     const DmaOffsets qofs = dma_offsets(qst, qst);
-    dma_tile(kb2, qr, qofs.k, (uint32_t)q0 * qst);
+    dma_tile(vb2, qr, qofs.k, (uint32_t)q0 * qst);
   }
   dma_tile(kb0, kr, dofs.k, (uint32_t)s0 * kst);
   dma_tile(vb0, vr, dofs.v, (uint32_t)s0 * vst);
-  dma_tile(kb1, kr, dofs.k, (uint32_t)s1 * kst);
   dma_tile(vb1, vr, dofs.v, (uint32_t)s1 * vst);
+  dma_tile(kb1, kr, dofs.k, (uint32_t)s1 * kst);
   wait_vm16();  // this wave's rows of Q have landed
   barrier_keep_loads();
 
@@ -190,6 +218,10 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
   //  32*dt + 16*(G&1) + 4*q .. +3; lane l then receives channel 32*dt + (l&31)
   //  of keys kh*32 + 16*cs + 8*hf + 4*g + {0..3}.
   const int krow = kh * 32 + l32;
+  // K read of k-step ks at (kx ^ 32*ks): the chunk swizzle (2*ks + g) ^ (krow & 15)
+  // splits into ks ^ (krow >> 1 & 7) (bits 5..7 of the offset) and g ^ (krow & 1)
+  const uint32_t kx = (uint32_t)krow * kRowBytes + (uint32_t)(((krow >> 1) & 7) << 5) +
+                      (uint32_t)((g ^ (krow & 1)) << 4);
   const int G = lane >> 4, e4 = (lane >> 2) & 3, q4 = lane & 3;
   const int vrow0 = kh * 32 + 4 * (G >> 1) + e4;  // + 16*cs + 8*hf (keeps row & 3)
 
@@ -200,12 +232,11 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
     const int qrow = rh * 32 + l32;
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks)
-      qf[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(kb2 + qrow * kRowBytes +
+      qf[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(vb2 + qrow * kRowBytes +
                                                          swz_k(qrow, 2 * ks + g) * 16));
   }
   wait_lgkm0();
-  barrier_keep_loads();
-  dma_tile(kb2, kr, dofs.k, (uint32_t)s2 * kst);
+  barrier_keep_loads();  // vb2 (Q) is free for V(2)
 
   f32x16 acc[4];
 #pragma unroll
@@ -213,23 +244,35 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[dt][r] = 0.f;
   // Reference max (log2 domain, tau*log2(e)*logit) of this lane's query: the
-  // accumulator holds sum 2^(x - m2) v.  It is raised only when a tile's max
-  // exceeds it by more than kLazy, so most tiles skip the rescale; the
-  // probabilities stay <= 2^kLazy.  Lanes l and l^32 share one query and one m2.
+  // accumulator holds sum 2^(x - m2) v.  It starts at -inf, so the first tile
+  // always sets it, and is raised only when a tile's probabilities would
+  // exceed kSumCap.  Lanes l and l^32 share one query and one m2.
   float m2 = -INFINITY;
-  float lsum = 0.f;  // partial sum of 2^(x - m2) over this lane's keys
+  float lsum = 0.f;  // partial sum of the bf16 probabilities over this lane's keys
 
-  wait_vm12();  // K(0), V(0) landed (K(1), V(1), K(2) may still fly)
+  wait_vm8();  // K(0), V(0) landed (V(1), K(1) may still fly)
   barrier_keep_loads();
 
-  // One 64-key tile, computed from K buffer `kc` and V buffer `vc`, which
-  // then receive K(n+3) and V(n+2).
-  auto step = [&](uint8_t* kc, uint8_t* vc) {
+  // One 64-key tile, computed from K buffer `kc` and V buffer `vc`.  Step n
+  // first refills `vn` (the buffer step n-1 read) with V(n+2); after its K
+  // fragments are in registers and one barrier, `kc` receives K(n+2).  The
+  // V^T fragments are read after that barrier and land during the S MFMAs.
+  auto step = [&](uint8_t* kc, const uint8_t* vc, uint8_t* vn) {
+    dma_tile(vn, vr, dofs.v, (uint32_t)s2 * vst);
+    // derive the 8 K read offsets here each step (one XOR each) rather than
+    // keeping 8 loop-invariant registers live across the loop
+    uint32_t kxs = kx;
+    asm volatile("" : "+v"(kxs));
     bf16x8 kf[8];
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks)
-      kf[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(kc + krow * kRowBytes +
-                                                         swz_k(krow, 2 * ks + g) * 16));
+      kf[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(kc + (kxs ^ (uint32_t)(ks << 5))));
+    // list entry of the tile after n2 (a scalar load, waited below)
+    const int ahead = n2 + 1;
+    const int pre = list[min(ahead / spb, p.kmax - 1)];
+    wait_lgkm0();
+    barrier_keep_loads();  // every wave holds its K fragments: kc is free
+    dma_tile(kc, kr, dofs.k, (uint32_t)s2 * kst);
     u32x4 vf[8];  // V^T fragments, [2*dt + cs]
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) {
@@ -248,13 +291,6 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
           vf[2 * dt + cs][2 * hf + 1] = tw[1];
         }
     }
-    // list entry of the tile after n3 (a scalar load, waited below)
-    const int ahead = n3 + 1;
-    const int pre = list[min(ahead / spb, p.kmax - 1)];
-    wait_lgkm0();
-    barrier_keep_loads();  // every wave holds its fragments: kc and vc are free
-    dma_tile(vc, vr, dofs.v, (uint32_t)s2 * vst);
-    dma_tile(kc, kr, dofs.k, (uint32_t)s3 * kst);
 
     // ---- S^T = K_half . Q^T ------------------------------------------------
     f32x16 s;
@@ -273,35 +309,31 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
     }
 
     // ---- online softmax --------------------------------------------------
-    float mx = s[0];
+    // P^T as B operand: k-step cs uses registers 8cs .. 8cs+7 (keys
+    // 16cs + 4g + {0..3} and 16cs + 8 + 4g + {0..3} of the half).  The tile
+    // sum is taken over the bf16 values the PV product uses (v_dot2 against
+    // (1, 1)), so numerator and normaliser see the same probabilities.
+    bf16x8 pk[2];
+    // with m2 = -inf every probability is +inf or NaN, so the first tile
+    // always takes the branch
+    float ts = tile_probs(s, p.scale_log2, m2, pk);
+    if (__any(!(ts <= kSumCap))) {  // wave-uniform: raise the reference max
+      float mx = s[0];
 #pragma unroll
-    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[r]);
-    mx *= p.scale_log2;
-    if (__any(mx > m2 + kLazy)) {  // wave-uniform: raise the reference max
+      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[r]);
+      mx *= p.scale_log2;
       const float mnew = fmaxf(m2, pair_max32(mx));
-      const float alpha = __builtin_amdgcn_exp2f(m2 - (mnew == -INFINITY ? 0.f : mnew));
+      const float msafe = mnew == -INFINITY ? 0.f : mnew;
+      const float alpha = __builtin_amdgcn_exp2f(m2 - msafe);
       lsum *= alpha;
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[dt][r] *= alpha;
       m2 = mnew;
+      ts = tile_probs(s, p.scale_log2, msafe, pk);
     }
-    const float msafe = m2 == -INFINITY ? 0.f : m2;
-    float pv[16];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      pv[r] = __builtin_amdgcn_exp2f(fmaf(s[r], p.scale_log2, -msafe));
-      lsum += pv[r];
-    }
-
-    // P^T as B operand: k-step cs uses registers 8cs .. 8cs+7 (keys
-    // 16cs + 4g + {0..3} and 16cs + 8 + 4g + {0..3} of the half).
-    bf16x8 pk[2];
-#pragma unroll
-    for (int cs = 0; cs < 2; ++cs)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) pk[cs][e] = (__bf16)pv[8 * cs + e];
+    lsum += ts;
 
     // ---- O^T += V_half^T . P^T -------------------------------------------
 #pragma unroll
@@ -314,40 +346,38 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
     // advance the cursor
     n = n1;
     n1 = n2;
-    n2 = n3;
     s0 = s1;
     s1 = s2;
-    s2 = s3;
-    s3 = p.N;
-    n3 = total;
+    s2 = p.N;
+    n2 = total;
     if (ahead < total) {
       const int j = __builtin_amdgcn_readfirstlane(pre);
       const int st = j * p.block + (ahead % spb) * kTile;
       if (j >= 0 && j < p.nb && st < p.N) {
-        n3 = ahead;
-        s3 = st;
+        n2 = ahead;
+        s2 = st;
       } else {
-        n3 = next_tile(list, ahead + 1, total, spb, p.block, p.nb, p.N, &s3);
+        n2 = next_tile(list, ahead + 1, total, spb, p.block, p.nb, p.N, &s2);
       }
     }
     // keep the whole tile's work ahead of the wait
     __builtin_amdgcn_sched_barrier(0);
-    wait_vm12();  // K(n+1), V(n+1) landed; K(n+2), V(n+2), K(n+3) may fly
-    barrier_keep_loads();
+    wait_vm8();  // K(n+1), V(n+1) landed; V(n+2), K(n+2) may fly
+    barrier_keep_loads();  // also: every wave is done reading vc
   };
-  // step n reads and refills K[n%3], V[n%2]
+  // step n reads K[n%2] and V[n%3] and refills V[(n+2)%3] and K[n%2]
   while (n < total) {
-    step(kb0, vb0);
+    step(kb0, vb0, vb2);
     if (n >= total) break;
-    step(kb1, vb1);
+    step(kb1, vb1, vb0);
     if (n >= total) break;
-    step(kb2, vb0);
+    step(kb0, vb2, vb1);
     if (n >= total) break;
-    step(kb0, vb1);
+    step(kb1, vb0, vb2);
     if (n >= total) break;
-    step(kb1, vb0);
+    step(kb0, vb1, vb0);
     if (n >= total) break;
-    step(kb2, vb1);
+    step(kb1, vb2, vb1);
   }
   wait_vm0();
   __syncthreads();
