@@ -7,16 +7,23 @@
 // as E8M0 block scales of v_mfma_scale_f32_32x32x64_f8f6f4, so the scores come
 // out dequantised with no extra VALU work.
 //
-// One workgroup = 4 wavefronts = one 64-row query tile.  A 32x32x64 fp8 MFMA
-// contracts 64 keys, so each wave takes a whole 64-key tile: waves 0/1 own
-// query rows 0-31 / 32-63 of the even tiles of the list, waves 2/3 of the
-// odd tiles; every step moves two tiles (K and V, 32 KB) global -> LDS with
-// buffer_load ... lds, double-buffered.  Per wave and tile:
+// One workgroup = 4 wavefronts = one 64-row query tile; two workgroups share
+// a CU.  A 32x32x64 fp8 MFMA contracts 64 keys, so each wave takes a whole
+// 64-key tile: waves 0/1 own query rows 0-31 / 32-63 of the first tile of
+// each pair of tiles in the list, waves 2/3 of the second.  Per wave and tile:
 //   S^T (64 keys x 32 queries) = K . Q^T       4 x v_mfma_scale_..._32x32x64 (scales sk, sq)
 //   P = 2^(x - m) * 2^(8 - kLazy) rounded to e4m3 with v_cvt_pk_fp8_f32
 //   O^T (128 x 32)        += V^T . P^T        4 x v_mfma_scale_..._32x32x64 (scales sv, 2^(kLazy-8))
-// The V^T operand is read from the row-major V tile with ds_read_b64_tr_b8.
-// The two tile-parity waves of a row-half merge their softmax states at the end.
+//   row sums of P          += 1^T . P^T        1 more MFMA against an all-ones channel
+// so the normaliser is the sum of exactly the rounded probabilities the PV
+// product uses, accumulated (and rescaled) by the matrix cores.
+// Copies: pairs of K and V tiles go global -> LDS with buffer_load ... lds
+// issued from inline asm.  K pairs are double- and V pairs triple-buffered
+// (80 KB of LDS): each step reads its K fragments, releases the K buffer at
+// one barrier and refills it with the pair two steps ahead; the V buffer the
+// previous step read is refilled at the start of the step.  The V^T operand
+// is read from the row-major V tile with ds_read_b64_tr_b8.  The two
+// tile-parity waves of a row-half merge their softmax states at the end.
 #include "common.h"
 #include "launch.h"
 
@@ -26,10 +33,12 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kRowBytes = kHeadDim;             // 128 B per e4m3 row
 constexpr int kTileBytes = kTile * kRowBytes;   // 8 KB per K or V tile
-constexpr int kBufBytes = 4 * kTileBytes;       // two tiles x (K, V) = 32 KB
+constexpr int kPairBytes = 2 * kTileBytes;      // one pair of tiles
 constexpr float kLazy = 2.f;  // log2 headroom before the accumulator is rescaled
 constexpr float kPScale = 64.f;                  // 2^(8 - kLazy): P in (0, 256] before e4m3
 constexpr int kPScaleInvE8m0 = 127 - 6;          // E8M0 code of 2^-(8 - kLazy)
+constexpr int kOneE8m0 = 127;                    // E8M0 code of 1
+constexpr int kFp8One = 0x38383838;              // four e4m3 ones
 
 // 16-byte-chunk swizzles of 128-byte rows (row = row within the tile):
 // conflict-free for the K A-operand reads (16 rows, one chunk per pass) and
@@ -39,8 +48,9 @@ __device__ __forceinline__ int swz_v(int row, int chunk) {
   return chunk ^ ((((row >> 1) & 1) << 1) | (((row >> 3) & 1) << 2));
 }
 
-typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((__vector_size__(2 * sizeof(int)))) int i32x2;
+typedef const __attribute__((address_space(4))) int32_t* list_ptr;
+typedef const __attribute__((address_space(4))) float* scale_ptr;
 
 struct Params {
   const uint8_t* q;
@@ -59,8 +69,8 @@ struct Params {
   float scale_log2;
 };
 
-__device__ __forceinline__ int tile_start(const int32_t* list, int n, int spb, int block,
-                                          int nb, int N) {
+__device__ __forceinline__ int tile_start(list_ptr list, int n, int spb, int block, int nb,
+                                          int N) {
   const int e = n / spb;
   const int j = list[e];
   if (j < 0 || j >= nb) return -1;
@@ -68,8 +78,8 @@ __device__ __forceinline__ int tile_start(const int32_t* list, int n, int spb, i
   return st < N ? st : -1;
 }
 
-__device__ __forceinline__ int next_tile(const int32_t* list, int n, int total, int spb,
-                                         int block, int nb, int N, int* start) {
+__device__ __forceinline__ int next_tile(list_ptr list, int n, int total, int spb, int block,
+                                         int nb, int N, int* start) {
   for (; n < total; ++n) {
     const int st = tile_start(list, n, spb, block, nb, N);
     if (st >= 0) {
@@ -90,11 +100,19 @@ __device__ __forceinline__ uint32_t dma_offset(int row, int slot, bool is_v) {
   return (uint32_t)row * kRowBytes + (uint32_t)chunk * 16u;
 }
 
-__device__ __forceinline__ void wait_dma() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+// s_waitcnt with the other counters at their maxima (no wait on them).
+__device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+__device__ __forceinline__ void wait_vm8() { __builtin_amdgcn_s_waitcnt(0x0F78); }
+__device__ __forceinline__ void wait_vm16() { __builtin_amdgcn_s_waitcnt(0x4F70); }
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 
 __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
-  __shared__ __attribute__((aligned(1024))) uint8_t lds0[kBufBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t lds1[kBufBytes];
+  // Distinct LDS objects per buffer keep every access at a constant base.
+  __shared__ __attribute__((aligned(1024))) uint8_t kp0[kPairBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t kp1[kPairBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t vp0[kPairBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t vp1[kPairBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t vp2[kPairBytes];
 
   const int item = p.order ? p.order[blockIdx.x] : (int)blockIdx.x;
   const int bh = item / p.ntiles;
@@ -103,7 +121,10 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
   const int q0 = qt * kTile;
   const int iblk = q0 / p.block;
   const int spb = p.block / kTile;
-  const int32_t* list = p.idx + ((int64_t)bh * p.nb + iblk) * p.kmax;
+  // List and scales are read-only here: reading them through the constant
+  // address space makes the uniform reads scalar loads, which vmcnt does not
+  // count.
+  const list_ptr list = (list_ptr)(p.idx + ((int64_t)bh * p.nb + iblk) * p.kmax);
   const int c = min(max(p.cnt[(int64_t)bh * p.nb + iblk], 0), p.kmax);
   const int total = c * spb;
 
@@ -115,79 +136,99 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
   const uint32_t bytes = (uint32_t)p.N * kRowBytes;
   const auto kr = make_rsrc(p.k + head, bytes);
   const auto vr = make_rsrc(p.v + head, bytes);
-  const float* skh = p.sk + (int64_t)bh * p.nb;
-  const float* svh = p.sv + (int64_t)bh * p.nb;
-  const int sq_code = e8m0(p.sq[(int64_t)bh * p.nb + iblk]);
+  const scale_ptr skh = (scale_ptr)(p.sk + (int64_t)bh * p.nb);
+  const scale_ptr svh = (scale_ptr)(p.sv + (int64_t)bh * p.nb);
+  const int sq_code = e8m0(((scale_ptr)p.sq)[(int64_t)bh * p.nb + iblk]);
 
-  // Copies: a step moves two tiles A and B into [K_A | K_B | V_A | V_B]; each
-  // wave copies rows 16w .. 16w+15 of each (two 1 KB instructions of 8 rows),
-  // lane l writing LDS slot l%8 of row l/8 of those 8 rows.
+  // Copies of a pair into [tile A | tile B]: each wave moves rows 16w .. 16w+15
+  // of each tile (two 1 KB copies of 8 rows), lane l writing LDS slot l%8 of
+  // row l/8 of those 8 rows.
   uint32_t koff[2], voff[2];
-  {
-    const int w = threadIdx.x >> 6;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int row = 16 * w + 8 * i + (lane >> 3);
-      koff[i] = dma_offset(row, lane & 7, false);
-      voff[i] = dma_offset(row, lane & 7, true);
-    }
+  for (int i = 0; i < 2; ++i) {
+    const int row = 16 * wave + 8 * i + (lane >> 3);
+    koff[i] = dma_offset(row, lane & 7, false);
+    voff[i] = dma_offset(row, lane & 7, true);
   }
-  auto dma = [&](uint8_t* dst, int a0, int b0) {
-    const int w = threadIdx.x >> 6;
+  const int wv = __builtin_amdgcn_readfirstlane(wave);
+  auto dma_pair = [&](uint8_t* dst, __amdgpu_buffer_rsrc_t r, const uint32_t (&off)[2], int a0,
+                      int b0) {
+    const uint32_t base = lds_addr(dst) + (uint32_t)(16 * wv) * kRowBytes;
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const uint32_t soff = (uint32_t)(t ? b0 : a0) * kRowBytes;
+    for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int r0 = 16 * w + 8 * i;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            kr, (lds_void*)(dst + t * kTileBytes + r0 * kRowBytes), 16, koff[i], soff, 0, 0);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            vr, (lds_void*)(dst + (2 + t) * kTileBytes + r0 * kRowBytes), 16, voff[i], soff, 0,
-            0);
-      }
-    }
+      for (int i = 0; i < 2; ++i)
+        dma16(base + t * kTileBytes + 8 * i * kRowBytes, r, off[i],
+              (uint32_t)(t ? b0 : a0) * kRowBytes);
   };
 
-  // Tile cursor: the current pair (na0, ta) / (nb0, tb) with key blocks
-  // ja / jb, and the next pair (na1, ua) / (nb1, ub).  Missing tiles start at
-  // N: they read zeros and all their keys are masked.  The list entries of
-  // the pair after next and the scales of the next pair are read one step
-  // ahead, alongside that step's copies, so no step waits on them.
+  // Pair cursor: pairs P0 (being computed), P1 and P2 as tile indices
+  // (na*, nb*), start rows (ta*, tb*; N when missing: such tiles read zeros
+  // and all their keys are masked) and key blocks (ja*, jb*).  The list
+  // entries after P2 and the scales of P1 are read one step ahead.
   auto block_of = [&](int n) { return n < total ? list[n / spb] : 0; };
-  int ta = p.N, tb = p.N, ua = p.N, ub = p.N;
-  int na0 = next_tile(list, 0, total, spb, p.block, p.nb, p.N, &ta);
-  int nb0 = next_tile(list, na0 + 1, total, spb, p.block, p.nb, p.N, &tb);
-  int na1 = next_tile(list, nb0 + 1, total, spb, p.block, p.nb, p.N, &ua);
-  int nb1 = next_tile(list, na1 + 1, total, spb, p.block, p.nb, p.N, &ub);
-  int ja = block_of(na0), jb = block_of(nb0), ka = block_of(na1), kb = block_of(nb1);
-  if (na0 < total) dma(lds0, ta, tb);
+  int ta0 = p.N, tb0 = p.N, ta1 = p.N, tb1 = p.N, ta2 = p.N, tb2 = p.N;
+  int na0 = next_tile(list, 0, total, spb, p.block, p.nb, p.N, &ta0);
+  int nb0 = next_tile(list, na0 + 1, total, spb, p.block, p.nb, p.N, &tb0);
+  int na1 = next_tile(list, nb0 + 1, total, spb, p.block, p.nb, p.N, &ta1);
+  int nb1 = next_tile(list, na1 + 1, total, spb, p.block, p.nb, p.N, &tb1);
+  int na2 = next_tile(list, nb1 + 1, total, spb, p.block, p.nb, p.N, &ta2);
+  int nb2 = next_tile(list, na2 + 1, total, spb, p.block, p.nb, p.N, &tb2);
+  int ja1 = block_of(na1), jb1 = block_of(nb1);
+  int ja2 = block_of(na2), jb2 = block_of(nb2);
   // scale codes of the current pair: (K, V) for tiles A and B
-  int sk_a = e8m0(skh[ja]), sv_a = e8m0(svh[ja]), sk_b = e8m0(skh[jb]), sv_b = e8m0(svh[jb]);
+  const int ja0 = block_of(na0), jb0 = block_of(nb0);
+  int sk_a = e8m0(skh[ja0]), sv_a = e8m0(svh[ja0]), sk_b = e8m0(skh[jb0]), sv_b = e8m0(svh[jb0]);
 
-  // Q fragment (B operand of K.Q^T): query row l32 of this row-half, bytes
+  // Prologue: the Q tile is staged through vp2 (K swizzle) while the K and V
+  // pairs P0 and P1 are issued; step 0 refills vp2 with V(P2) once every wave
+  // holds its Q fragment.  Every step issues the same number of copies, so
+  // the vmcnt arithmetic below is uniform.
+  {
+    const auto qr = make_rsrc(p.q + head, bytes);
+    const uint32_t base = lds_addr(vp2) + (uint32_t)(16 * wv) * kRowBytes;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) dma16(base + 8 * i * kRowBytes, qr, koff[i], (uint32_t)q0 * kRowBytes);
+  }
+  dma_pair(kp0, kr, koff, ta0, tb0);
+  dma_pair(vp0, vr, voff, ta0, tb0);
+  dma_pair(vp1, vr, voff, ta1, tb1);
+  dma_pair(kp1, kr, koff, ta1, tb1);
+  wait_vm16();  // this wave's rows of Q have landed
+  barrier_keep_loads();
+
+  // Q fragment (B operand of K.Q^T): query row 32*rh + l32, bytes
   // 64*ks + 32*g .. +31 of the row.
   i32x8 qf[2];
   {
-    const auto qr = make_rsrc(p.q + head, bytes);
-    const uint32_t off = (uint32_t)(q0 + rh * 32 + l32) * kRowBytes + g * 32;
+    const int row = rh * 32 + l32;
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
-      const u32x4 lo = buf_ld16(qr, off + ks * 64), hi = buf_ld16(qr, off + ks * 64 + 16);
+      const int c0 = 4 * ks + 2 * g;
+      const u32x4 lo = *reinterpret_cast<const u32x4*>(vp2 + row * kRowBytes + swz_k(row, c0) * 16);
+      const u32x4 hi = *reinterpret_cast<const u32x4*>(vp2 + row * kRowBytes + swz_k(row, c0 + 1) * 16);
+#pragma unroll
       for (int x = 0; x < 4; ++x) {
         qf[ks][x] = (int)lo[x];
         qf[ks][4 + x] = (int)hi[x];
       }
     }
   }
+  wait_lgkm0();
+  barrier_keep_loads();  // vp2 (Q) is free for V(P2)
 
-  f32x16 acc[4];
+  f32x16 acc[4], accl;  // O^T, and the row sums in register 0 of lanes 0..31
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[dt][r] = 0.f;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) accl[r] = 0.f;
+  // all-ones channel 0 of the row-sum A operand: lanes holding channel 0
+  i32x8 ones;
+#pragma unroll
+  for (int x = 0; x < 8; ++x) ones[x] = l32 == 0 ? kFp8One : 0;
   float m2 = -INFINITY;
-  float lsum = 0.f;
 
   // V^T transpose read: lane 16G + 2e + h supplies the 8 bytes of key
   // 16a + 8(e>>2) + 4(G>>1) + (e&3) at channels 32*dt + 16(G&1) + 8h .. +7;
@@ -195,8 +236,8 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
   const int G = lane >> 4, e8 = (lane >> 1) & 7, h8 = lane & 1;
   const int vrow0 = 8 * (e8 >> 2) + 4 * (G >> 1) + (e8 & 3);  // + 16a
 
-  wait_dma();
-  __syncthreads();
+  wait_vm8();  // K(P0), V(P0) landed (V(P1), K(P1) may still fly)
+  barrier_keep_loads();
 
   // Next valid tile at or after index `ahead` whose raw list entry `pre`
   // was prefetched: the common case decodes it directly, an invalid entry
@@ -217,16 +258,54 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
     return m;
   };
 
-  auto step = [&](const uint8_t* cur, uint8_t* nxt) {
-    dma(nxt, ua, ub);
-    // one step ahead: scales of the next pair, list entries after it
-    const float fka = skh[ka], fva = svh[ka], fkb = skh[kb], fvb = svh[kb];
-    const int pre1 = list[min((nb1 + 1) / spb, p.kmax - 1)];
-    const int pre2 = list[min((nb1 + 2) / spb, p.kmax - 1)];
+  // One pair: compute from K pair buffer `kc` and V pair buffer `vc`; `vn`
+  // (read by the previous step) receives V(P2) at once and `kc` receives
+  // K(P2) after the barrier that follows the K fragment reads.
+  auto step = [&](uint8_t* kc, const uint8_t* vc, uint8_t* vn) {
+    dma_pair(vn, vr, voff, ta2, tb2);
+    const uint8_t* kt = kc + par * kTileBytes;
+    i32x8 kf[2][2];  // [row tile][k-step]
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+      const int row = rt * 32 + l32;
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const int c0 = 4 * ks + 2 * g;
+        const u32x4 lo = *reinterpret_cast<const u32x4*>(kt + row * kRowBytes + swz_k(row, c0) * 16);
+        const u32x4 hi =
+            *reinterpret_cast<const u32x4*>(kt + row * kRowBytes + swz_k(row, c0 + 1) * 16);
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          kf[rt][ks][x] = (int)lo[x];
+          kf[rt][ks][4 + x] = (int)hi[x];
+        }
+      }
+    }
+    // one step ahead: scales of P1, list entries after P2
+    const float fka = skh[ja1], fva = svh[ja1], fkb = skh[jb1], fvb = svh[jb1];
+    const int pre1 = list[min((nb2 + 1) / spb, p.kmax - 1)];
+    const int pre2 = list[min((nb2 + 2) / spb, p.kmax - 1)];
+    wait_lgkm0();
+    barrier_keep_loads();  // every wave holds its K fragments: kc is free
+    dma_pair(kc, kr, koff, ta2, tb2);
 
-    const int start = par ? tb : ta;
-    const uint8_t* kt = cur + par * kTileBytes;
-    const uint8_t* vt = cur + (2 + par) * kTileBytes;
+    const uint8_t* vt = vc + par * kTileBytes;
+    i32x8 vf[4];
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+      const int lc = 2 * dt + (G & 1);  // logical 16-B chunk of channels 32dt + 16(G&1)
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        const int row = vrow0 + 16 * a;
+        const i32x2 t = __builtin_amdgcn_ds_read_tr8_b64_v2i32(
+            (__attribute__((address_space(3))) i32x2*)(vt + row * kRowBytes +
+                                                       swz_v(row, lc) * 16 + h8 * 8));
+        vf[dt][2 * a] = t[0];
+        vf[dt][2 * a + 1] = t[1];
+      }
+    }
+
+    const int start = par ? tb0 : ta0;
     const int sk_code = par ? sk_b : sk_a;
     const int sv_code = par ? sv_b : sv_a;
 
@@ -236,21 +315,10 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
     for (int rt = 0; rt < 2; ++rt) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[rt][r] = 0.f;
-      const int row = rt * 32 + l32;
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        const int c0 = 4 * ks + 2 * g;
-        const u32x4 lo = *reinterpret_cast<const u32x4*>(kt + row * kRowBytes + swz_k(row, c0) * 16);
-        const u32x4 hi =
-            *reinterpret_cast<const u32x4*>(kt + row * kRowBytes + swz_k(row, c0 + 1) * 16);
-        i32x8 kf;
-        for (int x = 0; x < 4; ++x) {
-          kf[x] = (int)lo[x];
-          kf[4 + x] = (int)hi[x];
-        }
-        s[rt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(kf, qf[ks], s[rt], 0, 0, 0,
-                                                                 sk_code, 0, sq_code);
-      }
+      for (int ks = 0; ks < 2; ++ks)
+        s[rt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(kf[rt][ks], qf[ks], s[rt], 0, 0,
+                                                                 0, sk_code, 0, sq_code);
     }
     // lane holds keys 32*rt + 8*(r>>2) + 4*g + (r&3) of query l32
     if (start + kTile > p.N) {
@@ -270,10 +338,10 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[rt][r]);
     mx *= p.scale_log2;
-    if (__any(mx > m2 + kLazy)) {
+    if (__any(mx > m2 + kLazy)) {  // wave-uniform: raise the reference max
       const float mnew = fmaxf(m2, pair_max32(mx));
       const float alpha = __builtin_amdgcn_exp2f(m2 - (mnew == -INFINITY ? 0.f : mnew));
-      lsum *= alpha;
+      accl[0] *= alpha;
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -282,7 +350,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
     }
     const float msafe = m2 == -INFINITY ? 0.f : m2;
     // P^T as B operand: slot 16*rt + r <- s[rt][r]; values 2^(x - m) * 2^(8 - kLazy)
-    // rounded to e4m3, the exact pre-rounding values summed into lsum.
+    // rounded to e4m3
     i32x8 pk;
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
@@ -290,62 +358,71 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
       for (int r = 0; r < 16; r += 4) {
         float x[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          x[u] = __builtin_amdgcn_exp2f(fmaf(s[rt][r + u], p.scale_log2, -msafe));
-          lsum += x[u];
-        }
-        int w = __builtin_amdgcn_cvt_pk_fp8_f32(x[0] * kPScale, x[1] * kPScale, 0, false);
-        w = __builtin_amdgcn_cvt_pk_fp8_f32(x[2] * kPScale, x[3] * kPScale, w, true);
+        for (int u = 0; u < 4; ++u)
+          x[u] = __builtin_amdgcn_exp2f(fmaf(s[rt][r + u], p.scale_log2, -msafe)) * kPScale;
+        int w = __builtin_amdgcn_cvt_pk_fp8_f32(x[0], x[1], 0, false);
+        w = __builtin_amdgcn_cvt_pk_fp8_f32(x[2], x[3], w, true);
         pk[4 * rt + r / 4] = w;
       }
     }
 
-    // ---- O^T += V^T . P^T ------------------------------------------------
+    // ---- O^T += V^T . P^T, row sums += 1^T . P^T ----------------------------
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt) {
-      const int lc = 2 * dt + (G & 1);  // logical 16-B chunk of channels 32dt + 16(G&1)
-      i32x8 vf;
-#pragma unroll
-      for (int a = 0; a < 4; ++a) {
-        const int row = vrow0 + 16 * a;
-        const i32x2 t = __builtin_amdgcn_ds_read_tr8_b64_v2i32(
-            (__attribute__((address_space(3))) i32x2*)(vt + row * kRowBytes +
-                                                       swz_v(row, lc) * 16 + h8 * 8));
-        vf[2 * a] = t[0];
-        vf[2 * a + 1] = t[1];
-      }
-      acc[dt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vf, pk, acc[dt], 0, 0, 0, sv_code,
-                                                                0, kPScaleInvE8m0);
-    }
+    for (int dt = 0; dt < 4; ++dt)
+      acc[dt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vf[dt], pk, acc[dt], 0, 0, 0,
+                                                                sv_code, 0, kPScaleInvE8m0);
+    accl = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(ones, pk, accl, 0, 0, 0, kOneE8m0, 0,
+                                                           kPScaleInvE8m0);
 
-    wait_dma();
-    __syncthreads();
+    // advance the cursor
     na0 = na1;
     nb0 = nb1;
-    ta = ua;
-    tb = ub;
+    ta0 = ta1;
+    tb0 = tb1;
+    na1 = na2;
+    nb1 = nb2;
+    ta1 = ta2;
+    tb1 = tb2;
+    ja1 = ja2;
+    jb1 = jb2;
     sk_a = e8m0(fka);
     sv_a = e8m0(fva);
     sk_b = e8m0(fkb);
     sv_b = e8m0(fvb);
-    const int prev = nb1;
-    na1 = advance(prev + 1, pre1, &ua, &ka);
-    if (na1 == prev + 1) {
-      nb1 = advance(na1 + 1, pre2, &ub, &kb);
+    const int prev = nb2;
+    na2 = advance(prev + 1, pre1, &ta2, &ja2);
+    if (na2 == prev + 1) {
+      nb2 = advance(na2 + 1, pre2, &tb2, &jb2);
     } else {
-      nb1 = next_tile(list, na1 + 1, total, spb, p.block, p.nb, p.N, &ub);
-      kb = block_of(nb1);
+      nb2 = next_tile(list, na2 + 1, total, spb, p.block, p.nb, p.N, &tb2);
+      jb2 = block_of(nb2);
     }
+    // keep the whole pair's work ahead of the wait
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vm8();  // K(P1), V(P1) landed; V(P2), K(P2) may fly
+    barrier_keep_loads();  // also: every wave is done reading vc
   };
+  // step n reads K pair buffer n%2 and V pair buffer n%3, refills V (n+2)%3
   while (na0 < total) {
-    step(lds0, lds1);
+    step(kp0, vp0, vp2);
     if (na0 >= total) break;
-    step(lds1, lds0);
+    step(kp1, vp1, vp0);
+    if (na0 >= total) break;
+    step(kp0, vp2, vp1);
+    if (na0 >= total) break;
+    step(kp1, vp0, vp2);
+    if (na0 >= total) break;
+    step(kp0, vp1, vp0);
+    if (na0 >= total) break;
+    step(kp1, vp2, vp1);
   }
+  wait_vm0();
+  __syncthreads();
 
   // ---- merge the two tile-parity waves, normalise, store -----------------
-  lsum += __shfl_xor(lsum, 32, kWave);
-  float* mrg = reinterpret_cast<float*>(rh ? lds1 : lds0);  // 66 x 64 floats per row-half
+  // the row sum of query l32 sits in register 0 of lane l32
+  float lsum = __shfl(accl[0], l32, kWave);
+  float* mrg = reinterpret_cast<float*>(rh ? vp0 : kp0);  // 66 x 64 floats per row-half
   if (par == 1) {
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
