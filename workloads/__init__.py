@@ -41,7 +41,7 @@ import numpy as np
 import torch
 
 __all__ = ["Workload", "WORKLOADS", "make_head", "make_inputs", "random_block_lists",
-           "softmax_scale"]
+           "softmax_scale", "rope_pairs_wan", "rope_table", "comp_params"]
 
 
 def softmax_scale(d: int) -> float:
@@ -207,3 +207,46 @@ def random_block_lists(nqb: int, nkb: int, kmax: int, seed: int, p_empty: float 
     for i in range(nqb):
         idx[i, :cnt[i]] = np.sort(rng.choice(nkb, size=cnt[i], replace=False))
     return idx, cnt
+
+
+# --------------------------------------------------------------------------
+# Inputs of the compensation branch: the rotary schedule and synthetic
+# low-rank weights (the trained ones are not available).
+# --------------------------------------------------------------------------
+def rope_pairs_wan(head_dim: int = 128, theta: float = 10000.0):
+    """(axis, freq) of every coordinate pair of the 3D RoPE schedule of a
+    Wan-style video DiT over head_dim coordinates: a time band of
+    head_dim - 4*(head_dim//6) coordinates, then height and width bands of
+    2*(head_dim//6) each; in a band of width w the k-th pair turns by
+    theta^(-2k/w) radians per grid step along the band's axis."""
+    third = head_dim // 6
+    axis, freq = [], []
+    for ax, w in ((0, head_dim - 4 * third), (1, 2 * third), (2, 2 * third)):
+        for k in range(w // 2):
+            axis.append(ax)
+            freq.append(theta ** (-2.0 * k / w))
+    return np.array(axis), np.array(freq)
+
+
+def rope_table(grid, rank: int, head_dim: int = 128) -> np.ndarray:
+    """float32 (cos, sin) [N, rank/2, 2] of the first `rank` coordinates of
+    that schedule at every token of the t-major latent grid (T, Hg, Wg)."""
+    axis, freq = rope_pairs_wan(head_dim)
+    axis, freq = axis[:rank // 2], freq[:rank // 2]
+    pos = _coords(grid).numpy()
+    ang = pos[:, axis] * freq[None, :]
+    return np.stack([np.cos(ang), np.sin(ang)], axis=-1).astype(np.float32)
+
+
+def comp_params(wl: Workload, rank: int = 64, gate_scale: float = 0.5, seed_extra: int = 0):
+    """Synthetic compensation-branch inputs of a workload: low-rank
+    projections P_q, P_k bf16 [H, rank, d] ~ N(0, 1/d), RMSNorm weights
+    gamma fp32 [H, d] ~ 1 + 0.1 N(0, 1), token-wise gates fp32 [B, H, N]
+    ~ gate_scale * N(0, 1)."""
+    g = _gen(wl.seed, 991, seed_extra)
+    d = wl.head_dim
+    pq = (torch.randn(wl.heads, rank, d, generator=g) / math.sqrt(d)).to(torch.bfloat16)
+    pk = (torch.randn(wl.heads, rank, d, generator=g) / math.sqrt(d)).to(torch.bfloat16)
+    gamma = 1.0 + 0.1 * torch.randn(wl.heads, d, generator=g)
+    gate = gate_scale * torch.randn(wl.batch, wl.heads, wl.seqlen, generator=g)
+    return pq, pk, gamma, gate
