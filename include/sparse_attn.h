@@ -54,7 +54,7 @@ enum {
 };
 
 /* Workspace consumers (second argument of sparse_attn_workspace_size). */
-enum { SA_OP_SELECT = 0, SA_OP_SCHEDULE = 1 };
+enum { SA_OP_SELECT = 0, SA_OP_SCHEDULE = 1, SA_OP_COMP_STATE = 2 };
 
 /*
  * Problem descriptor (host struct).
@@ -184,6 +184,43 @@ int sparse_attn_fwd_fp8(const sparse_attn_desc* desc, const uint8_t* q8, const f
                         const uint8_t* k8, const float* sk, const uint8_t* v8, const float* sv,
                         const int32_t* idx, const int32_t* cnt, int32_t kmax,
                         const int32_t* order, void* o, float* lse, void* stream);
+
+/*
+ * Compensation branch of compensated sparse attention (paper §2 Eq.
+ * comp-sparse; §4.1 gives the low-rank branch with a token-wise gate):
+ *   q~_i = R_r(p_i) silu(P_q q_i^norm),  k~_j = R_r(p_j) silu(P_k k_j^norm),
+ *   C = sum_j k~_j v_j^T,  O_i = O_s,i + g_i * rms(O_s,i) * RMSNorm(q~_i^T C).
+ * rank r must be 64 (the paper's compensation rank), else SA_ERR_UNSUPPORTED.
+ * R_r rotates coordinate pairs (2m, 2m+1), m < r/2, as (a, b) -> (a c - b s,
+ * a s + b c) with (c, s) = rope[token][m]; rope is fp32 [L][r/2][2], shared by
+ * all heads (the caller's rotary schedule, e.g. the first r coordinates of the
+ * backbone's 3D RoPE).  P_q, P_k are bf16 [H][r][d] row-major.  silu(x) =
+ * x sigmoid(x); RMSNorm(y) = y / sqrt(mean_d y^2 + eps) * gamma; rms(x) =
+ * sqrt(mean_d x^2).  Products run on bf16 operands with fp32 accumulation.
+ */
+
+/* Low-rank state C for every (b, h).
+ *  k_norm  bf16 [B][H][L][d] via kn_stride (the backbone's normalised keys)
+ *  v       bf16 via desc->v_stride
+ *  state   fp32 out, contiguous [B][H][r][d]
+ *  ws      ws_bytes >= sparse_attn_workspace_size(SA_OP_COMP_STATE)
+ * Deterministic: partial sums over fixed token chunks added in a fixed order. */
+int sparse_attn_comp_state(const sparse_attn_desc* desc, int32_t rank, const void* k_norm,
+                           const int64_t kn_stride[3], const void* v, const void* pk,
+                           const float* rope, float* state, void* ws, size_t ws_bytes,
+                           void* stream);
+
+/* Gated output O = O_s + g * rms(O_s) * RMSNorm(q~^T C).
+ *  q_norm  bf16 [B][H][L][d] via qn_stride
+ *  state   fp32 [B][H][r][d] from sparse_attn_comp_state
+ *  gamma   fp32 [H][d] RMSNorm weight, or NULL for ones; eps >= 0
+ *  gate    fp32 [B][H][L] via gate_stride (elements; 0 broadcasts)
+ *  o_s     bf16 sparse-branch output via desc->o_stride
+ *  o       bf16 out via desc->o_stride; may be o_s itself (in place) */
+int sparse_attn_comp_out(const sparse_attn_desc* desc, int32_t rank, const void* q_norm,
+                         const int64_t qn_stride[3], const void* pq, const float* rope,
+                         const float* state, const float* gamma, float eps, const float* gate,
+                         const int64_t gate_stride[3], const void* o_s, void* o, void* stream);
 
 #ifdef __cplusplus
 }

@@ -18,19 +18,22 @@ __all__ = [
     "SA_OP_SELECT", "SA_OP_SCHEDULE", "library", "sparse_attn_version",
     "sparse_attn_status_str", "sparse_attn_keep_count", "sparse_attn_workspace_size",
     "sparse_attn_num_tiles", "sparse_attn_select", "sparse_attn_schedule", "sparse_attn_fwd",
-    "sparse_attn_quant_fp8", "sparse_attn_fwd_fp8", "make_desc", "EXPORTED_SYMBOLS",
+    "sparse_attn_quant_fp8", "sparse_attn_fwd_fp8", "sparse_attn_comp_state",
+    "sparse_attn_comp_out", "SA_OP_COMP_STATE", "COMP_RANK", "make_desc", "EXPORTED_SYMBOLS",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsparseattn.so")
 
 SA_SELECT_ROW_TOPK = 0
 SA_SELECT_HEAD_TOPK = 1
-SA_OP_SELECT, SA_OP_SCHEDULE = 0, 1
+SA_OP_SELECT, SA_OP_SCHEDULE, SA_OP_COMP_STATE = 0, 1, 2
+COMP_RANK = 64
 
 EXPORTED_SYMBOLS = (
     "sparse_attn_version", "sparse_attn_status_str", "sparse_attn_keep_count",
     "sparse_attn_workspace_size", "sparse_attn_num_tiles", "sparse_attn_select",
     "sparse_attn_schedule", "sparse_attn_fwd", "sparse_attn_quant_fp8", "sparse_attn_fwd_fp8",
+    "sparse_attn_comp_state", "sparse_attn_comp_out",
 )
 
 
@@ -53,6 +56,7 @@ class SparseAttnDesc(ctypes.Structure):
 _LIB = None
 _P = ctypes.c_void_p
 _I32P = ctypes.POINTER(ctypes.c_int32)
+_I64P = ctypes.POINTER(ctypes.c_int64)
 
 
 def library() -> ctypes.CDLL:
@@ -80,6 +84,10 @@ def library() -> ctypes.CDLL:
                                                      _P, _P, _P]),
             "sparse_attn_fwd_fp8": (ctypes.c_int, [D, _P, _P, _P, _P, _P, _P, _P, _P,
                                                    ctypes.c_int32, _P, _P, _P, _P]),
+            "sparse_attn_comp_state": (ctypes.c_int, [D, ctypes.c_int32, _P, _I64P, _P, _P, _P,
+                                                      _P, _P, ctypes.c_size_t, _P]),
+            "sparse_attn_comp_out": (ctypes.c_int, [D, ctypes.c_int32, _P, _I64P, _P, _P, _P,
+                                                    _P, ctypes.c_float, _P, _I64P, _P, _P, _P]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(lib, name)
@@ -269,3 +277,50 @@ def sparse_attn_fwd_fp8(q8, sq, k8, sk, v8, sv, idx, cnt, block: int = 64,
 def default_softmax_scale(d: int) -> float:
     """fp32(1/sqrt(d)), the scale the library uses when 0 is passed."""
     return float(torch.tensor(1.0 / math.sqrt(d), dtype=torch.float32))
+
+
+def _st3(strides):
+    return (ctypes.c_int64 * 3)(*strides)
+
+
+def sparse_attn_comp_state(k_norm, v, pk, rope, state=None, ws=None):
+    """Low-rank state C = sum_j k~_j v_j^T of the compensation branch.
+    k_norm, v bf16 [B, H, N, 128]; pk bf16 [H, 64, 128]; rope fp32 [N, 32, 2].
+    Returns state fp32 [B, H, 64, 128]."""
+    B, H, N, d = k_norm.shape
+    desc = make_desc(k_norm, k_norm, v)
+    if state is None:
+        state = torch.empty(B, H, COMP_RANK, d, dtype=torch.float32, device=k_norm.device)
+    for t, name, dt in ((pk, "pk", torch.bfloat16), (rope, "rope", torch.float32),
+                        (state, "state", torch.float32)):
+        _dense(t, name, dt)
+    if ws is None:
+        ws = _workspace(desc, SA_OP_COMP_STATE, 1, k_norm.device)
+    st = library().sparse_attn_comp_state(ctypes.byref(desc), COMP_RANK, _ptr(k_norm),
+                                          _st3(_strides(k_norm)), _ptr(v), _ptr(pk), _ptr(rope),
+                                          _ptr(state), _ptr(ws), ws.numel(), _stream(k_norm))
+    _check(st, "sparse_attn_comp_state")
+    return state
+
+
+def sparse_attn_comp_out(q_norm, pq, rope, state, gate, o_s, gamma=None, eps: float = 1e-6,
+                         o=None):
+    """Gated output O = O_s + g * rms(O_s) * RMSNorm(q~^T C) (o may be o_s).
+    gate fp32 [B, H, N] (any strides, including 0); gamma fp32 [H, 128] or None."""
+    B, H, N, d = q_norm.shape
+    if o is None:
+        o = torch.empty_like(o_s)
+    if _strides(o) != _strides(o_s):
+        raise ValueError("o and o_s must share their strides")
+    desc = make_desc(q_norm, o=o_s)
+    for t, name, dt in ((pq, "pq", torch.bfloat16), (rope, "rope", torch.float32),
+                        (state, "state", torch.float32), (gamma, "gamma", torch.float32)):
+        _dense(t, name, dt)
+    if gate.dtype != torch.float32 or gate.dim() != 3:
+        raise ValueError("gate must be a float32 [B, H, N] tensor")
+    st = library().sparse_attn_comp_out(ctypes.byref(desc), COMP_RANK, _ptr(q_norm),
+                                        _st3(_strides(q_norm)), _ptr(pq), _ptr(rope),
+                                        _ptr(state), _ptr(gamma), eps, _ptr(gate),
+                                        _st3(gate.stride()), _ptr(o_s), _ptr(o), _stream(q_norm))
+    _check(st, "sparse_attn_comp_out")
+    return o

@@ -91,6 +91,7 @@ size_t sparse_attn_workspace_size(const sparse_attn_desc* desc, int32_t op, int3
   switch (op) {
     case SA_OP_SELECT: return sa::select_workspace_bytes(s);
     case SA_OP_SCHEDULE: return kmax >= 1 ? sa::schedule_workspace_bytes(s) : 0;
+    case SA_OP_COMP_STATE: return sa::comp_state_workspace_bytes(s);
     default: return 0;
   }
 }
@@ -219,3 +220,71 @@ int sparse_attn_fwd_fp8(const sparse_attn_desc* desc, const uint8_t* q8, const f
 }
 
 }  // extern "C"
+
+// ---- compensation branch (paper §2 Eq. comp-sparse, §4.1) -----------------
+namespace {
+// Strides of a [B][H][N] fp32 gate: non-negative (0 broadcasts).
+bool gate_strides_ok(const int64_t st[3]) {
+  return st && st[0] >= 0 && st[1] >= 0 && st[2] >= 0;
+}
+}  // namespace
+
+int sparse_attn_comp_state(const sparse_attn_desc* desc, int32_t rank, const void* k_norm,
+                           const int64_t kn_stride[3], const void* v, const void* pk,
+                           const float* rope, float* state, void* ws, size_t ws_bytes,
+                           void* stream) {
+  Shape s;
+  int st = check_desc(desc, &s);
+  if (st != SA_OK) return st;
+  if (rank != 64) return SA_ERR_UNSUPPORTED;
+  if (!k_norm || !kn_stride || !v || !pk || !rope || !state || !ws) return SA_ERR_INVALID_ARG;
+  if (!aligned16(k_norm) || !aligned16(v) || !aligned16(pk) || !aligned16(rope) ||
+      !aligned16(state))
+    return SA_ERR_INVALID_ARG;
+  if (!strides_ok(kn_stride) || !strides_ok(desc->v_stride)) return SA_ERR_INVALID_ARG;
+  if (!offsets_fit(s, kn_stride, 2) || !offsets_fit(s, desc->v_stride, 2)) return SA_ERR_UNSUPPORTED;
+  if ((int64_t)s.N * 256 >= ((int64_t)1 << 32)) return SA_ERR_UNSUPPORTED;  // rope offsets
+  if (ws_bytes < sa::comp_state_workspace_bytes(s)) return SA_ERR_WORKSPACE;
+  sa::CompStateIn in{};
+  in.k_norm = k_norm;
+  in.v = v;
+  in.pk = pk;
+  in.rope = rope;
+  in.kns = to_strides(kn_stride);
+  in.vs = to_strides(desc->v_stride);
+  return launch_status(
+      sa::launch_comp_state(s, in, state, ws, static_cast<hipStream_t>(stream)));
+}
+
+int sparse_attn_comp_out(const sparse_attn_desc* desc, int32_t rank, const void* q_norm,
+                         const int64_t qn_stride[3], const void* pq, const float* rope,
+                         const float* state, const float* gamma, float eps, const float* gate,
+                         const int64_t gate_stride[3], const void* o_s, void* o,
+                         void* stream) {
+  Shape s;
+  int st = check_desc(desc, &s);
+  if (st != SA_OK) return st;
+  if (rank != 64) return SA_ERR_UNSUPPORTED;
+  if (!q_norm || !qn_stride || !pq || !rope || !state || !gate || !o_s || !o)
+    return SA_ERR_INVALID_ARG;
+  if (!aligned16(q_norm) || !aligned16(pq) || !aligned16(rope) || !aligned16(state) ||
+      !aligned16(o_s) || !aligned16(o) || (gamma && !aligned16(gamma)))
+    return SA_ERR_INVALID_ARG;
+  if (!strides_ok(qn_stride) || !strides_ok(desc->o_stride) || !gate_strides_ok(gate_stride))
+    return SA_ERR_INVALID_ARG;
+  if (!(eps >= 0.f) || isinf(eps)) return SA_ERR_INVALID_ARG;
+  sa::CompOutIn in{};
+  in.q_norm = q_norm;
+  in.pq = pq;
+  in.rope = rope;
+  in.state = state;
+  in.gamma = gamma;
+  in.gate = gate;
+  in.o_s = o_s;
+  in.o = o;
+  in.qns = to_strides(qn_stride);
+  in.gs = to_strides(gate_stride);
+  in.oss = to_strides(desc->o_stride);
+  in.eps = eps;
+  return launch_status(sa::launch_comp_out(s, in, static_cast<hipStream_t>(stream)));
+}

@@ -1,0 +1,445 @@
+// Compensation branch and gate epilogue of compensated sparse attention on
+// gfx950 (paper §2 Eq. comp-sparse; §4.1 defines the branch):
+//
+//   q~_i = R_r(p_i) silu(P_q q_i^norm),   k~_j = R_r(p_j) silu(P_k k_j^norm)
+//   C = sum_j k~_j v_j^T                       (rank r = 64, per (batch, head))
+//   O_i = O_s,i + g_i * rms(O_s,i) * RMSNorm(q~_i^T C)
+//
+// R_r rotates consecutive coordinate pairs (2m, 2m+1) by angles given as a
+// (cos, sin) table per token and pair.  Three launches:
+//   comp_state  : per (head, chunk of 2048 tokens) the projection k_norm P_k^T
+//                 on the matrix cores in the layout that keeps tokens inside a
+//                 lane (so k~ is directly the B operand of the next product),
+//                 silu and the rotation (the partner coordinate of a pair sits
+//                 in the neighbouring lane: one DPP swap), then
+//                 C^T += V^T K~ with V^T read transposed from LDS; the four
+//                 waves' partials are summed through LDS in a fixed order.
+//   comp_reduce : the chunk partials of a head summed in chunk order -> C.
+//   comp_out    : per (head, 128 tokens) the projection P_q q_norm^T in the
+//                 layout that keeps one token per lane, silu and rotation,
+//                 O_lr^T = C^T q~^T against a bf16 hi + lo copy of C^T in LDS, then
+//                 RMSNorm, the gate and the sum with O_s, all per lane.
+// The projections multiply the bf16 inputs exactly (fp32 accumulation).  In
+// the two low-rank products the fp32 operands k~, q~ and C are each split as
+// hi + lo with hi = bf16(x) and lo = bf16(x - hi) (about 16 significant
+// bits), and the products taken as hi.hi + hi.lo + lo.hi on the bf16 matrix
+// cores, so the state and O_lr carry close to fp32 accuracy; silu, rotation
+// and the normalisations are fp32.
+#include "common.h"
+#include "launch.h"
+
+namespace sa {
+namespace {
+
+constexpr int kRank = 64;
+constexpr int kSub = 128;               // tokens per sub-tile (4 waves x 32)
+constexpr int kChunk = 2048;            // tokens per state workgroup
+constexpr int kStateElems = kRank * kHeadDim;
+constexpr int kRopeBytes = kRank / 2 * 2 * 4;  // (cos, sin) fp32 per pair, per token
+constexpr int kVRow = kHeadDim * 2;     // bf16 V row in LDS
+constexpr int kCtStride = 72;           // bf16 per C^T row in LDS (64 + 8 padding)
+
+typedef __attribute__((__vector_size__(4 * sizeof(short)))) short i16x4;
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+__device__ __forceinline__ float silu(float x) { return x / (1.f + __expf(-x)); }
+
+// 16-byte-chunk swizzle of the V rows in LDS (as in the forward): conflict-free
+// for the transpose reads of 4 rows x 4 chunks per half-wave.
+__device__ __forceinline__ int swz_v(int row, int chunk) { return chunk ^ ((row & 3) << 2); }
+
+struct StateArgs {
+  const uint16_t* kn;
+  const uint16_t* v;
+  const uint16_t* pk;
+  const float* rope;
+  float* partial;  // [BH][chunks][kStateElems], lane-register order
+  Strides kns, vs;
+  int H, N, chunks;
+};
+
+// partial element e = ((dt*2 + nb)*16 + reg)*64 + lane holds C^T[d][r] with
+// r = 32 nb + (lane & 31), d = 32 dt + 8 (reg >> 2) + 4 (lane >> 5) + (reg & 3).
+__global__ __launch_bounds__(256) void comp_state_kernel(StateArgs a) {
+  __shared__ __attribute__((aligned(16))) uint8_t vt[kSub * kVRow];
+  const int bh = blockIdx.x, chunk = blockIdx.y;  // heads vary fastest: rope rows shared in L2
+  const int b = bh / a.H, h = bh - b * a.H;
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  const int g = lane >> 5, l32 = lane & 31;
+  const int t_begin = chunk * kChunk, t_end = min(t_begin + kChunk, a.N);
+
+  const uint32_t kst = (uint32_t)a.kns.n * 2, vst = (uint32_t)a.vs.n * 2;
+  const auto kr = make_rsrc(a.kn + b * a.kns.b + h * a.kns.h, (uint32_t)(a.N - 1) * kst + 256u);
+  const auto vr = make_rsrc(a.v + b * a.vs.b + h * a.vs.h, (uint32_t)(a.N - 1) * vst + 256u);
+  const auto rr = make_rsrc(a.rope, (uint32_t)a.N * kRopeBytes);
+
+  // P_k as B operand of k_norm P_k^T: column r = l32 + 32 nb, k = d 16 ks + 8 g .. +7
+  bf16x8 pkf[2][8];
+  const uint16_t* pkh = a.pk + (int64_t)h * kStateElems;
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks)
+      pkf[nb][ks] = as_bf16x8(ld16(pkh + (l32 + 32 * nb) * kHeadDim + 16 * ks + 8 * g));
+
+  f32x16 acc[4][2];  // C^T: [dt][nb]
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[dt][nb][r] = 0.f;
+
+  // transpose-read addresses of V^T (rows = this wave's tokens, as the
+  // forward's keys): lane 16G + 4e + q reads the 8-byte chunk of token
+  // 32 wave + 16 s + 8 hf + 4 (G>>1) + e at channels 32 dt + 16 (G&1) + 4 q
+  const int G = lane >> 4, e4 = (lane >> 2) & 3, q4 = lane & 3;
+  const int vrow0 = 32 * wave + 4 * (G >> 1) + e4;
+
+  for (int t0 = t_begin; t0 < t_end; t0 += kSub) {
+    const int tw = t0 + 32 * wave;
+    // k_norm as A operand: token tw + l32, channels 16 ks + 8 g .. +7
+    bf16x8 kf[8];
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks)
+      kf[ks] = as_bf16x8(buf_ld16(kr, (uint32_t)(tw + l32) * kst + (16 * ks + 8 * g) * 2));
+    // V rows of the sub-tile: thread t moves chunks e = t + 256 m -> row e/16, chunk e%16
+    u32x4 vrow[8];
+#pragma unroll
+    for (int m = 0; m < 8; ++m) {
+      const int e = t + 256 * m, row = e >> 4, ch = e & 15;
+      vrow[m] = buf_ld16(vr, (uint32_t)(t0 + row) * vst + ch * 16);
+    }
+    // (cos, sin) of this lane's pair m = (32 nb + l32) / 2 at its 16 tokens
+    // tw + 8 j + 4 g + rr
+    float2 cs[2][16];
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int tok = tw + 8 * (i >> 2) + 4 * g + (i & 3);
+        const uint32_t off = (uint32_t)tok * kRopeBytes + (uint32_t)((32 * nb + l32) >> 1) * 8u;
+        const u32x2 w = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rr, off, 0, 0));
+        cs[nb][i] = make_float2(__uint_as_float(w[0]), __uint_as_float(w[1]));
+      }
+    __syncthreads();  // every wave is done reading the previous sub-tile's V
+#pragma unroll
+    for (int m = 0; m < 8; ++m) {
+      const int e = t + 256 * m, row = e >> 4, ch = e & 15;
+      *reinterpret_cast<u32x4*>(vt + row * kVRow + swz_v(row, ch) * 16) = vrow[m];
+    }
+
+    // projection k_norm P_k^T: lane holds column r = 32 nb + l32 of tokens
+    // 8 j + 4 g + rr (register 4 j + rr)
+    f32x16 pr[2];
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) pr[nb][r] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks)
+        pr[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], pkf[nb][ks], pr[nb], 0, 0, 0);
+    }
+    // silu, then the rotation of pair (r & ~1, r | 1): the partner column is
+    // the neighbouring lane (DPP quad_perm 1,0,3,2)
+    const bool odd = (l32 & 1) != 0;
+    // K~ as B operand, split hi + lo: [nb][k-step s], tokens 16 s + 4 g + rr, 16 s + 8 + 4 g + rr
+    bf16x8 kt[2][2], kl[2][2];
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      float y[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float x = silu(pr[nb][i]);
+        const float o = __int_as_float(
+            __builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xF, 0xF, false));
+        const float c = cs[nb][i].x, s = cs[nb][i].y;
+        // even r: (x, o) = (a, b) -> a c - b s;  odd r: (o, x) = (a, b) -> a s + b c
+        y[i] = odd ? fmaf(o, s, x * c) : fmaf(x, c, -o * s);
+      }
+#pragma unroll
+      for (int sk = 0; sk < 2; ++sk)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const __bf16 hi = (__bf16)y[8 * sk + e];
+          kt[nb][sk][e] = hi;
+          kl[nb][sk][e] = (__bf16)(y[8 * sk + e] - (float)hi);
+        }
+    }
+    __syncthreads();  // the sub-tile's V rows are in LDS
+
+    // C^T += V^T K~ over this wave's 32 tokens
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+      const int lc = 4 * dt + 2 * (G & 1) + (q4 >> 1);
+      const int half = (q4 & 1) * 8;
+#pragma unroll
+      for (int sk = 0; sk < 2; ++sk) {
+        u32x4 vv;
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          const int row = vrow0 + 16 * sk + 8 * hf;
+          const i16x4 tr = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) i16x4*)(vt + row * kVRow + swz_v(row, lc) * 16 +
+                                                         half));
+          const u32x2 tw2 = __builtin_bit_cast(u32x2, tr);
+          vv[2 * hf] = tw2[0];
+          vv[2 * hf + 1] = tw2[1];
+        }
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) {
+          acc[dt][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv), kt[nb][sk],
+                                                                acc[dt][nb], 0, 0, 0);
+          acc[dt][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv), kl[nb][sk],
+                                                                acc[dt][nb], 0, 0, 0);
+        }
+      }
+    }
+  }
+
+  // sum the four waves' partials in wave order through LDS, then store
+  float* red = reinterpret_cast<float*>(vt);  // 32 KB = kStateElems floats
+  for (int w = 0; w < 4; ++w) {
+    __syncthreads();
+    if (wave == w) {
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int e = ((dt * 2 + nb) * 16 + r) * 64 + lane;
+            red[e] = w == 0 ? acc[dt][nb][r] : red[e] + acc[dt][nb][r];
+          }
+    }
+  }
+  __syncthreads();
+  float* out = a.partial + ((int64_t)bh * a.chunks + chunk) * kStateElems;
+  for (int e = t; e < kStateElems; e += 256) out[e] = red[e];
+}
+
+// C[bh][r][d] = sum over chunks (in chunk order) of the partials.
+__global__ __launch_bounds__(256) void comp_reduce_kernel(const float* __restrict__ partial,
+                                                          int chunks, float* __restrict__ state) {
+  const int bh = blockIdx.x;
+  const float* src = partial + (int64_t)bh * chunks * kStateElems;
+  float* dst = state + (int64_t)bh * kStateElems;
+  for (int e = threadIdx.x; e < kStateElems; e += 256) {
+    float s = 0.f;
+    for (int c = 0; c < chunks; ++c) s += src[(int64_t)c * kStateElems + e];
+    const int lane = e & 63, reg = (e >> 6) & 15, blk = e >> 10;  // blk = dt * 2 + nb
+    const int dt = blk >> 1, nb = blk & 1;
+    const int r = 32 * nb + (lane & 31);
+    const int d = 32 * dt + 8 * (reg >> 2) + 4 * (lane >> 5) + (reg & 3);
+    dst[r * kHeadDim + d] = s;
+  }
+}
+
+struct OutArgs {
+  const uint16_t* qn;
+  const uint16_t* pq;
+  const float* rope;
+  const float* state;
+  const float* gamma;  // [H][d] or null
+  const float* gate;
+  const uint16_t* os;
+  uint16_t* o;
+  Strides qns, gs, oss;
+  int H, N;
+  float eps;
+};
+
+// LDS position of rank index r in a C^T row: within each group of 16 the
+// middle quads swap, so that lane group g reads the 8 indices
+// {16s + 4g + 0..3, 16s + 8 + 4g + 0..3} of k-step s as one 16-byte chunk.
+__device__ __forceinline__ int ct_pos(int r) {
+  const int q = r & 15, quad = q >> 2;
+  const int nq = quad == 1 ? 2 : (quad == 2 ? 1 : quad);
+  return (r & ~15) + 4 * nq + (q & 3);
+}
+
+__global__ __launch_bounds__(256) void comp_out_kernel(OutArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t ct[kHeadDim * kCtStride];   // C^T hi
+  __shared__ __attribute__((aligned(16))) uint16_t ctl[kHeadDim * kCtStride];  // C^T lo
+  const int bh = blockIdx.x, tile = blockIdx.y;
+  const int b = bh / a.H, h = bh - b * a.H;
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  const int g = lane >> 5, l32 = lane & 31;
+
+  // C^T of this head as bf16 hi + lo into LDS
+  const float* st = a.state + (int64_t)bh * kStateElems;
+  for (int e = t; e < kStateElems; e += 256) {
+    const int r = e / kHeadDim, d = e - r * kHeadDim;
+    const float x = st[e];
+    const __bf16 hi = (__bf16)x;
+    ct[d * kCtStride + ct_pos(r)] = __builtin_bit_cast(uint16_t, hi);
+    ctl[d * kCtStride + ct_pos(r)] = __builtin_bit_cast(uint16_t, (__bf16)(x - (float)hi));
+  }
+
+  // P_q as A operand of P_q q_norm^T: row r = l32 + 32 rb, k = d 16 ks + 8 g .. +7
+  bf16x8 pqf[2][8];
+  const uint16_t* pqh = a.pq + (int64_t)h * kStateElems;
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks)
+      pqf[rb][ks] = as_bf16x8(ld16(pqh + (l32 + 32 * rb) * kHeadDim + 16 * ks + 8 * g));
+
+  const int tok = tile * kSub + 32 * wave + l32;  // this lane's token
+  const bool live = tok < a.N;
+  const int tokc = live ? tok : a.N - 1;  // clamped for the loads
+  // q_norm as B operand: column token, k = channels 16 ks + 8 g .. +7
+  const uint16_t* qrow = a.qn + b * a.qns.b + h * a.qns.h + (int64_t)tokc * a.qns.n;
+  bf16x8 qf[8];
+#pragma unroll
+  for (int ks = 0; ks < 8; ++ks) qf[ks] = as_bf16x8(ld16(qrow + 16 * ks + 8 * g));
+
+  // projection: lane holds token `tok`, rank indices 32 rb + 8 j + 4 g + rr
+  f32x16 pr[2];
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) pr[rb][r] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks)
+      pr[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pqf[rb][ks], qf[ks], pr[rb], 0, 0, 0);
+  }
+  // silu and rotation: pairs (rr = 0, 1) and (2, 3) of each (rb, j) are pairs
+  // m = 16 rb + 4 j + 2 g + {0, 1}, whose (cos, sin) are 16 contiguous bytes
+  const float* rope_t = a.rope + (int64_t)tokc * (kRank / 2) * 2;
+  // q~^T as B operand split hi + lo, k-step s: indices 16 s + 4 g + rr, 16 s + 8 + 4 g + rr
+  bf16x8 qt[4], ql[4];
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const f32x4 csn = *reinterpret_cast<const f32x4*>(rope_t + 2 * (16 * rb + 4 * j + 2 * g));
+      float y[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) y[u] = silu(pr[rb][4 * j + u]);
+      const float r0 = fmaf(y[0], csn[0], -y[1] * csn[1]);
+      const float r1 = fmaf(y[0], csn[1], y[1] * csn[0]);
+      const float r2 = fmaf(y[2], csn[2], -y[3] * csn[3]);
+      const float r3 = fmaf(y[2], csn[3], y[3] * csn[2]);
+      const int s = 2 * rb + (j >> 1), half = 4 * (j & 1);
+      const float rv[4] = {r0, r1, r2, r3};
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const __bf16 hi = (__bf16)rv[u];
+        qt[s][half + u] = hi;
+        ql[s][half + u] = (__bf16)(rv[u] - (float)hi);
+      }
+    }
+  __syncthreads();  // C^T is in LDS
+
+  // O_lr^T = C^T q~^T: lane holds token `tok`, channels 32 dt + 8 j + 4 g + rr
+  f32x16 y[4];
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) y[dt][r] = 0.f;
+    const uint16_t* crow = ct + (32 * dt + l32) * kCtStride;
+    const uint16_t* clrow = ctl + (32 * dt + l32) * kCtStride;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const bf16x8 cf = as_bf16x8(*reinterpret_cast<const u32x4*>(crow + 16 * s + 8 * g));
+      const bf16x8 cl = as_bf16x8(*reinterpret_cast<const u32x4*>(clrow + 16 * s + 8 * g));
+      y[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cl, qt[s], y[dt], 0, 0, 0);
+      y[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cf, ql[s], y[dt], 0, 0, 0);
+      y[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cf, qt[s], y[dt], 0, 0, 0);
+    }
+  }
+
+  // RMSNorm of O_lr and rms of O_s over the 128 channels (64 here, 64 in lane l ^ 32)
+  const uint16_t* osrow = a.os + b * a.oss.b + h * a.oss.h + (int64_t)tokc * a.oss.n;
+  float osv[4][16];
+  float ss_y = 0.f, ss_o = 0.f;
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const u32x2 w = *reinterpret_cast<const u32x2*>(osrow + 32 * dt + 8 * j + 4 * g);
+      osv[dt][4 * j + 0] = bf16_lo(w[0]);
+      osv[dt][4 * j + 1] = bf16_hi(w[0]);
+      osv[dt][4 * j + 2] = bf16_lo(w[1]);
+      osv[dt][4 * j + 3] = bf16_hi(w[1]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        ss_y = fmaf(y[dt][4 * j + u], y[dt][4 * j + u], ss_y);
+        ss_o = fmaf(osv[dt][4 * j + u], osv[dt][4 * j + u], ss_o);
+      }
+    }
+  ss_y += __shfl_xor(ss_y, 32, kWave);
+  ss_o += __shfl_xor(ss_o, 32, kWave);
+  const float rstd = 1.f / sqrtf(ss_y * (1.f / kHeadDim) + a.eps);
+  const float rms_o = sqrtf(ss_o * (1.f / kHeadDim));
+  const float gv = a.gate[b * a.gs.b + h * a.gs.h + (int64_t)tokc * a.gs.n];
+  const float coef = gv * rms_o * rstd;
+  if (!live) return;
+  uint16_t* orow = a.o + b * a.oss.b + h * a.oss.h + (int64_t)tok * a.oss.n;
+  const float* gam = a.gamma ? a.gamma + (int64_t)h * kHeadDim : nullptr;
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int d0 = 32 * dt + 8 * j + 4 * g;
+      f32x4 gm = {1.f, 1.f, 1.f, 1.f};
+      if (gam) gm = *reinterpret_cast<const f32x4*>(gam + d0);
+      float x[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) x[u] = fmaf(coef * y[dt][4 * j + u], gm[u], osv[dt][4 * j + u]);
+      u32x2 w;
+      w[0] = pack_bf16x2(x[0], x[1]);
+      w[1] = pack_bf16x2(x[2], x[3]);
+      *reinterpret_cast<u32x2*>(orow + d0) = w;
+    }
+}
+
+}  // namespace
+
+size_t comp_state_workspace_bytes(const Shape& s) {
+  const int64_t chunks = (s.N + kChunk - 1) / kChunk;
+  return (size_t)s.B * s.H * chunks * kStateElems * sizeof(float);
+}
+
+hipError_t launch_comp_state(const Shape& s, const CompStateIn& in, float* state, void* ws,
+                             hipStream_t stream) {
+  StateArgs a;
+  a.kn = static_cast<const uint16_t*>(in.k_norm);
+  a.v = static_cast<const uint16_t*>(in.v);
+  a.pk = static_cast<const uint16_t*>(in.pk);
+  a.rope = in.rope;
+  a.partial = static_cast<float*>(ws);
+  a.kns = in.kns;
+  a.vs = in.vs;
+  a.H = s.H;
+  a.N = s.N;
+  a.chunks = (s.N + kChunk - 1) / kChunk;
+  comp_state_kernel<<<dim3(s.B * s.H, a.chunks), 256, 0, stream>>>(a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  comp_reduce_kernel<<<s.B * s.H, 256, 0, stream>>>(a.partial, a.chunks, state);
+  return hipGetLastError();
+}
+
+hipError_t launch_comp_out(const Shape& s, const CompOutIn& in, hipStream_t stream) {
+  OutArgs a;
+  a.qn = static_cast<const uint16_t*>(in.q_norm);
+  a.pq = static_cast<const uint16_t*>(in.pq);
+  a.rope = in.rope;
+  a.state = in.state;
+  a.gamma = in.gamma;
+  a.gate = in.gate;
+  a.os = static_cast<const uint16_t*>(in.o_s);
+  a.o = static_cast<uint16_t*>(in.o);
+  a.qns = in.qns;
+  a.gs = in.gs;
+  a.oss = in.oss;
+  a.H = s.H;
+  a.N = s.N;
+  a.eps = in.eps;
+  comp_out_kernel<<<dim3(s.B * s.H, (s.N + kSub - 1) / kSub), 256, 0, stream>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace sa

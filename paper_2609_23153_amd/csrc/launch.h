@@ -54,6 +54,31 @@ struct FwdArgs {
 hipError_t launch_fwd_bf16(const Shape& s, const FwdArgs& a, hipStream_t stream);
 hipError_t launch_fwd_fp8(const Shape& s, const FwdArgs& a, hipStream_t stream);
 
+// ---- compensation branch -------------------------------------------------
+struct CompStateIn {
+  const void* k_norm;  // bf16 [B][H][N][128] via kns
+  const void* v;       // bf16 via vs
+  const void* pk;      // bf16 [H][64][128]
+  const float* rope;   // fp32 [N][32][2] (cos, sin)
+  Strides kns, vs;
+};
+struct CompOutIn {
+  const void* q_norm;  // bf16 via qns
+  const void* pq;      // bf16 [H][64][128]
+  const float* rope;
+  const float* state;  // fp32 [B][H][64][128]
+  const float* gamma;  // fp32 [H][128] or null
+  const float* gate;   // fp32 via gs
+  const void* o_s;     // bf16 via oss
+  void* o;             // bf16 via oss (may equal o_s)
+  Strides qns, gs, oss;
+  float eps;
+};
+size_t comp_state_workspace_bytes(const Shape& s);
+hipError_t launch_comp_state(const Shape& s, const CompStateIn& in, float* state, void* ws,
+                             hipStream_t stream);
+hipError_t launch_comp_out(const Shape& s, const CompOutIn& in, hipStream_t stream);
+
 // ---- fp8 quantisation ----------------------------------------------------
 hipError_t launch_quant_fp8(const Shape& s, const void* x, Strides xs, uint8_t* x8,
                             float* scale, hipStream_t stream);

@@ -161,3 +161,25 @@ def test_quant_and_fwd_fp8_reject_bad_arguments():
     assert f(P, P, P, P, P, P, P, P, 0, None, P, None, None) == -1       # kmax 0
     assert f(P, P, P, P, P, P, None, P, 7, None, P, None, None) == -1    # null idx
     assert f(P, P, MIS, P, P, P, P, P, 7, None, P, None, None) == -1     # misaligned k8
+
+
+def test_comp_entry_points_reject_bad_arguments():
+    lib = sa.library()
+    ds = desc(B=1, H=2, N=4096)
+    st3 = (ctypes.c_int64 * 3)(2 * 4096 * 128, 4096 * 128, 128)
+    need = lib.sparse_attn_workspace_size(ctypes.byref(ds), sa.SA_OP_COMP_STATE, 1)
+    assert need == 1 * 2 * 2 * 64 * 128 * 4          # 2 chunks of 2048 tokens per head
+    cs = lambda *a: lib.sparse_attn_comp_state(ctypes.byref(ds), *a)
+    assert cs(32, P, st3, P, P, P, P, P, need, None) == -2          # rank must be 64
+    assert cs(64, None, st3, P, P, P, P, P, need, None) == -1       # null k_norm
+    assert cs(64, MIS, st3, P, P, P, P, P, need, None) == -1        # misaligned
+    assert cs(64, P, None, P, P, P, P, P, need, None) == -1         # null strides
+    assert cs(64, P, st3, P, P, P, P, P, need - 1, None) == -3      # workspace
+    co = lambda *a: lib.sparse_attn_comp_out(ctypes.byref(ds), *a)
+    g3 = (ctypes.c_int64 * 3)(2 * 4096, 4096, 1)
+    bad_g3 = (ctypes.c_int64 * 3)(2 * 4096, -4096, 1)
+    assert co(16, P, st3, P, P, P, None, 1e-6, P, g3, P, P, None) == -2      # rank
+    assert co(64, P, st3, P, P, P, None, 1e-6, None, g3, P, P, None) == -1   # null gate
+    assert co(64, P, st3, P, P, P, None, -1.0, P, g3, P, P, None) == -1      # eps < 0
+    assert co(64, P, st3, P, P, P, None, 1e-6, P, bad_g3, P, P, None) == -1  # gate stride
+    assert co(64, P, st3, P, P, P, MIS, 1e-6, P, g3, P, P, None) == -1       # gamma misaligned

@@ -235,7 +235,7 @@ def rope_table(grid, rank: int, head_dim: int = 128) -> np.ndarray:
     axis, freq = axis[:rank // 2], freq[:rank // 2]
     pos = _coords(grid).numpy()
     ang = pos[:, axis] * freq[None, :]
-    return np.stack([np.cos(ang), np.sin(ang)], axis=-1).astype(np.float32)
+    return np.ascontiguousarray(np.stack([np.cos(ang), np.sin(ang)], axis=-1), dtype=np.float32)
 
 
 def comp_params(wl: Workload, rank: int = 64, gate_scale: float = 0.5, seed_extra: int = 0):
