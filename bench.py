@@ -72,6 +72,9 @@ def parse_args():
                     help="heads of the workload the oracle runs for the CPU baseline")
     ap.add_argument("--fp8", choices=["on", "off"], default="on",
                     help="also time the fp8 path on the outlier workload of the same shape")
+    ap.add_argument("--comp", choices=["on", "off"], default="on",
+                    help="also time the compensation branch and gate epilogue on the bf16 "
+                         "layer's inputs and sparse output")
     ap.add_argument("--copy-calib", action="store_true",
                     help="also time a plain 1 GiB device copy (HBM counter calibration)")
     return ap.parse_args()
@@ -99,6 +102,61 @@ def blas_threads():
     except Exception:
         pass
     return len(os.sched_getaffinity(0))
+
+
+def bench_comp(args, sa, W, dev, wl, q, k, v, o_s, sparse_ms):
+    """Compensation branch and gate epilogue at the same shape: the low-rank
+    state from K and V, then the gated output from Q and the sparse branch's
+    output (the layer's Q and K stand in for the normalised queries and keys;
+    rank-64 projections, RMSNorm weights and gates are synthetic)."""
+    B, H, N, d = q.shape
+    r = sa.COMP_RANK
+    pq, pk, gamma, gate = (t.to(dev) for t in W.comp_params(wl, r))
+    rope = torch.from_numpy(W.rope_table(wl.grid, r)).to(dev)
+    state = torch.empty(B, H, d, r, dtype=torch.float32, device=dev)
+    desc = sa.make_desc(k, k, v)
+    ws = torch.empty(sa.sparse_attn_workspace_size(desc, sa.SA_OP_COMP_STATE, 1),
+                     dtype=torch.uint8, device=dev)
+    o = torch.empty_like(o_s)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+
+    def step(e=None):
+        if e:
+            e[0].record()
+        sa.sparse_attn_comp_state(k, v, pk, rope, state=state, ws=ws)
+        if e:
+            e[1].record()
+        sa.sparse_attn_comp_out(q, pq, rope, state, gate, o_s, gamma=gamma, o=o)
+        if e:
+            e[2].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    for s_ in range(args.steps):
+        step(ev[s_])
+    torch.cuda.synchronize()
+    st_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    out_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    tok = B * H * N
+    rope_b = N * (r // 2) * 2 * 4
+    st_bytes = 2 * tok * d * 2 + rope_b + H * r * d * 2 + B * H * r * d * 4
+    out_bytes = 3 * tok * d * 2 + rope_b + H * r * d * 2 + B * H * r * d * 4 + tok * 4 + H * d * 4
+    gbs = lambda b_, ms: b_ / (ms * 1e-3) / 1e9
+    return {
+        "ms_per_call": {"comp_state": round(st_ms, 4), "comp_out": round(out_ms, 4)},
+        "compensated_step_ms": round(sparse_ms + st_ms + out_ms, 4),
+        "rank": r,
+        "roofline": {
+            "kernels": ["comp_state_kernel", "comp_out_kernel"], "bound": "hbm",
+            "achieved": round(gbs(st_bytes + out_bytes, st_ms + out_ms), 1),
+            "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(gbs(st_bytes + out_bytes, st_ms + out_ms) / PEAK_HBM_GBS, 4),
+            "traffic": None, "algorithmic_bytes": {"comp_state": st_bytes, "comp_out": out_bytes},
+        },
+        "gbs": {"comp_state": round(gbs(st_bytes, st_ms), 1),
+                "comp_out": round(gbs(out_bytes, out_ms), 1)},
+    }
 
 
 def bench_fp8(args, sa, W, dev):
@@ -264,6 +322,8 @@ def main():
         },
     }
 
+    if args.comp == "on":
+        out["compensation"] = bench_comp(args, sa, W, dev, wl, q, kk, v, o, ms_step)
     if args.fp8 == "on":
         out["fp8"] = bench_fp8(args, sa, W, dev)
 

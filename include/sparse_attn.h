@@ -199,10 +199,10 @@ int sparse_attn_fwd_fp8(const sparse_attn_desc* desc, const uint8_t* q8, const f
  * sqrt(mean_d x^2).  Products run on bf16 operands with fp32 accumulation.
  */
 
-/* Low-rank state C for every (b, h).
+/* Low-rank state C for every (b, h), stored transposed.
  *  k_norm  bf16 [B][H][L][d] via kn_stride (the backbone's normalised keys)
  *  v       bf16 via desc->v_stride
- *  state   fp32 out, contiguous [B][H][r][d]
+ *  state   fp32 out, contiguous [B][H][d][r]: state[b][h][c][m] = C[m][c]
  *  ws      ws_bytes >= sparse_attn_workspace_size(SA_OP_COMP_STATE)
  * Deterministic: partial sums over fixed token chunks added in a fixed order. */
 int sparse_attn_comp_state(const sparse_attn_desc* desc, int32_t rank, const void* k_norm,
@@ -212,7 +212,7 @@ int sparse_attn_comp_state(const sparse_attn_desc* desc, int32_t rank, const voi
 
 /* Gated output O = O_s + g * rms(O_s) * RMSNorm(q~^T C).
  *  q_norm  bf16 [B][H][L][d] via qn_stride
- *  state   fp32 [B][H][r][d] from sparse_attn_comp_state
+ *  state   fp32 [B][H][d][r] from sparse_attn_comp_state
  *  gamma   fp32 [H][d] RMSNorm weight, or NULL for ones; eps >= 0
  *  gate    fp32 [B][H][L] via gate_stride (elements; 0 broadcasts)
  *  o_s     bf16 sparse-branch output via desc->o_stride

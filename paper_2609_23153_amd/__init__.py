@@ -286,11 +286,11 @@ def _st3(strides):
 def sparse_attn_comp_state(k_norm, v, pk, rope, state=None, ws=None):
     """Low-rank state C = sum_j k~_j v_j^T of the compensation branch.
     k_norm, v bf16 [B, H, N, 128]; pk bf16 [H, 64, 128]; rope fp32 [N, 32, 2].
-    Returns state fp32 [B, H, 64, 128]."""
+    Returns the state transposed, fp32 [B, H, 128, 64] (state[..., c, m] = C[m, c])."""
     B, H, N, d = k_norm.shape
     desc = make_desc(k_norm, k_norm, v)
     if state is None:
-        state = torch.empty(B, H, COMP_RANK, d, dtype=torch.float32, device=k_norm.device)
+        state = torch.empty(B, H, d, COMP_RANK, dtype=torch.float32, device=k_norm.device)
     for t, name, dt in ((pk, "pk", torch.bfloat16), (rope, "rope", torch.float32),
                         (state, "state", torch.float32)):
         _dense(t, name, dt)

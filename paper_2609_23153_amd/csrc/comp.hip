@@ -14,7 +14,8 @@
 //                 in the neighbouring lane: one DPP swap), then
 //                 C^T += V^T K~ with V^T read transposed from LDS; the four
 //                 waves' partials are summed through LDS in a fixed order.
-//   comp_reduce : the chunk partials of a head summed in chunk order -> C.
+//   comp_reduce : the chunk partials of a head summed in chunk order -> C^T
+//                 (fp32, d-major: row d holds the r values of C[.][d]).
 //   comp_out    : per (head, 128 tokens) the projection P_q q_norm^T in the
 //                 layout that keeps one token per lane, silu and rotation,
 //                 O_lr^T = C^T q~^T against a bf16 hi + lo copy of C^T in LDS, then
@@ -33,7 +34,9 @@ namespace {
 
 constexpr int kRank = 64;
 constexpr int kSub = 128;               // tokens per sub-tile (4 waves x 32)
-constexpr int kChunk = 2048;            // tokens per state workgroup
+constexpr int kChunk = 1024;            // tokens per state workgroup
+constexpr int kReduceSplit = 32;        // workgroups per head in the chunk reduction
+static_assert(kReduceSplit * 256 == 64 * 128, "one reduction thread per state element");
 constexpr int kStateElems = kRank * kHeadDim;
 constexpr int kRopeBytes = kRank / 2 * 2 * 4;  // (cos, sin) fp32 per pair, per token
 constexpr int kVRow = kHeadDim * 2;     // bf16 V row in LDS
@@ -96,20 +99,26 @@ __global__ __launch_bounds__(256) void comp_state_kernel(StateArgs a) {
   const int G = lane >> 4, e4 = (lane >> 2) & 3, q4 = lane & 3;
   const int vrow0 = 32 * wave + 4 * (G >> 1) + e4;
 
-  for (int t0 = t_begin; t0 < t_end; t0 += kSub) {
+  // k_norm as A operand (token tw + l32, channels 16 ks + 8 g .. +7) and the
+  // sub-tile's V rows (thread t moves chunks e = t + 256 m -> row e/16, chunk
+  // e%16); the next sub-tile's are fetched while the current one is computed
+  bf16x8 kf[8];
+  u32x4 vrow[8];
+  auto load_kv = [&](int t0) {
     const int tw = t0 + 32 * wave;
-    // k_norm as A operand: token tw + l32, channels 16 ks + 8 g .. +7
-    bf16x8 kf[8];
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks)
       kf[ks] = as_bf16x8(buf_ld16(kr, (uint32_t)(tw + l32) * kst + (16 * ks + 8 * g) * 2));
-    // V rows of the sub-tile: thread t moves chunks e = t + 256 m -> row e/16, chunk e%16
-    u32x4 vrow[8];
 #pragma unroll
     for (int m = 0; m < 8; ++m) {
       const int e = t + 256 * m, row = e >> 4, ch = e & 15;
       vrow[m] = buf_ld16(vr, (uint32_t)(t0 + row) * vst + ch * 16);
     }
+  };
+  if (t_begin < t_end) load_kv(t_begin);
+
+  for (int t0 = t_begin; t0 < t_end; t0 += kSub) {
+    const int tw = t0 + 32 * wave;
     // (cos, sin) of this lane's pair m = (32 nb + l32) / 2 at its 16 tokens
     // tw + 8 j + 4 g + rr
     float2 cs[2][16];
@@ -140,6 +149,7 @@ __global__ __launch_bounds__(256) void comp_state_kernel(StateArgs a) {
       for (int ks = 0; ks < 8; ++ks)
         pr[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], pkf[nb][ks], pr[nb], 0, 0, 0);
     }
+    if (t0 + kSub < t_end) load_kv(t0 + kSub);  // prefetch the next sub-tile
     // silu, then the rotation of pair (r & ~1, r | 1): the partner column is
     // the neighbouring lane (DPP quad_perm 1,0,3,2)
     const bool odd = (l32 & 1) != 0;
@@ -218,21 +228,20 @@ __global__ __launch_bounds__(256) void comp_state_kernel(StateArgs a) {
   for (int e = t; e < kStateElems; e += 256) out[e] = red[e];
 }
 
-// C[bh][r][d] = sum over chunks (in chunk order) of the partials.
+// C^T[bh][d][r] = sum over chunks (in chunk order) of the partials; each
+// workgroup sums 256 of a head's elements.
 __global__ __launch_bounds__(256) void comp_reduce_kernel(const float* __restrict__ partial,
                                                           int chunks, float* __restrict__ state) {
   const int bh = blockIdx.x;
-  const float* src = partial + (int64_t)bh * chunks * kStateElems;
-  float* dst = state + (int64_t)bh * kStateElems;
-  for (int e = threadIdx.x; e < kStateElems; e += 256) {
-    float s = 0.f;
-    for (int c = 0; c < chunks; ++c) s += src[(int64_t)c * kStateElems + e];
-    const int lane = e & 63, reg = (e >> 6) & 15, blk = e >> 10;  // blk = dt * 2 + nb
-    const int dt = blk >> 1, nb = blk & 1;
-    const int r = 32 * nb + (lane & 31);
-    const int d = 32 * dt + 8 * (reg >> 2) + 4 * (lane >> 5) + (reg & 3);
-    dst[r * kHeadDim + d] = s;
-  }
+  const int e = blockIdx.y * 256 + threadIdx.x;
+  const float* src = partial + (int64_t)bh * chunks * kStateElems + e;
+  float s = 0.f;
+  for (int c = 0; c < chunks; ++c) s += src[(int64_t)c * kStateElems];
+  const int lane = e & 63, reg = (e >> 6) & 15, blk = e >> 10;  // blk = dt * 2 + nb
+  const int dt = blk >> 1, nb = blk & 1;
+  const int r = 32 * nb + (lane & 31);
+  const int d = 32 * dt + 8 * (reg >> 2) + 4 * (lane >> 5) + (reg & 3);
+  state[(int64_t)bh * kStateElems + d * kRank + r] = s;
 }
 
 struct OutArgs {
@@ -266,15 +275,49 @@ __global__ __launch_bounds__(256) void comp_out_kernel(OutArgs a) {
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
   const int g = lane >> 5, l32 = lane & 31;
 
-  // C^T of this head as bf16 hi + lo into LDS
+  // every per-token load is issued first, so its latency overlaps the staging of C^T
+  const int tok = tile * kSub + 32 * wave + l32;  // this lane's token
+  const bool live = tok < a.N;
+  const int tokc = live ? tok : a.N - 1;  // clamped for the loads
+  // q_norm as B operand: column token, k = channels 16 ks + 8 g .. +7
+  const uint16_t* qrow = a.qn + b * a.qns.b + h * a.qns.h + (int64_t)tokc * a.qns.n;
+  bf16x8 qf[8];
+#pragma unroll
+  for (int ks = 0; ks < 8; ++ks) qf[ks] = as_bf16x8(ld16(qrow + 16 * ks + 8 * g));
+
+  // O_s of this lane's token: channels 32 dt + 8 j + 4 g + {0..3}
+  const uint16_t* osrow = a.os + b * a.oss.b + h * a.oss.h + (int64_t)tokc * a.oss.n;
+  u32x2 osw[4][4];
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      osw[dt][j] = *reinterpret_cast<const u32x2*>(osrow + 32 * dt + 8 * j + 4 * g);
+  const float gv = a.gate[b * a.gs.b + h * a.gs.h + (int64_t)tokc * a.gs.n];
+
+  // C^T of this head as bf16 hi + lo into LDS: thread t converts quads of
+  // 4 consecutive r (16-byte loads) and stores each as 8 bytes at its
+  // permuted position
   const float* st = a.state + (int64_t)bh * kStateElems;
-  for (int e = t; e < kStateElems; e += 256) {
-    const int r = e / kHeadDim, d = e - r * kHeadDim;
-    const float x = st[e];
-    const __bf16 hi = (__bf16)x;
-    ct[d * kCtStride + ct_pos(r)] = __builtin_bit_cast(uint16_t, hi);
-    ctl[d * kCtStride + ct_pos(r)] = __builtin_bit_cast(uint16_t, (__bf16)(x - (float)hi));
+#pragma unroll
+  for (int m = 0; m < kStateElems / 4 / 256; ++m) {
+    const int qd = t + 256 * m;              // quad index: d = qd / 16, r = 4 (qd % 16)
+    const int d = qd >> 4, r = (qd & 15) * 4;
+    const f32x4 x = *reinterpret_cast<const f32x4*>(st + 4 * qd);
+    u32x2 hw, lw;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const __bf16 h0 = (__bf16)x[2 * u], h1 = (__bf16)x[2 * u + 1];
+      const __bf16 l0 = (__bf16)(x[2 * u] - (float)h0), l1 = (__bf16)(x[2 * u + 1] - (float)h1);
+      hw[u] = (uint32_t)__builtin_bit_cast(uint16_t, h0) |
+              ((uint32_t)__builtin_bit_cast(uint16_t, h1) << 16);
+      lw[u] = (uint32_t)__builtin_bit_cast(uint16_t, l0) |
+              ((uint32_t)__builtin_bit_cast(uint16_t, l1) << 16);
+    }
+    *reinterpret_cast<u32x2*>(ct + d * kCtStride + ct_pos(r)) = hw;
+    *reinterpret_cast<u32x2*>(ctl + d * kCtStride + ct_pos(r)) = lw;
   }
+
 
   // P_q as A operand of P_q q_norm^T: row r = l32 + 32 rb, k = d 16 ks + 8 g .. +7
   bf16x8 pqf[2][8];
@@ -284,15 +327,6 @@ __global__ __launch_bounds__(256) void comp_out_kernel(OutArgs a) {
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks)
       pqf[rb][ks] = as_bf16x8(ld16(pqh + (l32 + 32 * rb) * kHeadDim + 16 * ks + 8 * g));
-
-  const int tok = tile * kSub + 32 * wave + l32;  // this lane's token
-  const bool live = tok < a.N;
-  const int tokc = live ? tok : a.N - 1;  // clamped for the loads
-  // q_norm as B operand: column token, k = channels 16 ks + 8 g .. +7
-  const uint16_t* qrow = a.qn + b * a.qns.b + h * a.qns.h + (int64_t)tokc * a.qns.n;
-  bf16x8 qf[8];
-#pragma unroll
-  for (int ks = 0; ks < 8; ++ks) qf[ks] = as_bf16x8(ld16(qrow + 16 * ks + 8 * g));
 
   // projection: lane holds token `tok`, rank indices 32 rb + 8 j + 4 g + rr
   f32x16 pr[2];
@@ -351,14 +385,13 @@ __global__ __launch_bounds__(256) void comp_out_kernel(OutArgs a) {
   }
 
   // RMSNorm of O_lr and rms of O_s over the 128 channels (64 here, 64 in lane l ^ 32)
-  const uint16_t* osrow = a.os + b * a.oss.b + h * a.oss.h + (int64_t)tokc * a.oss.n;
   float osv[4][16];
   float ss_y = 0.f, ss_o = 0.f;
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const u32x2 w = *reinterpret_cast<const u32x2*>(osrow + 32 * dt + 8 * j + 4 * g);
+      const u32x2 w = osw[dt][j];
       osv[dt][4 * j + 0] = bf16_lo(w[0]);
       osv[dt][4 * j + 1] = bf16_hi(w[0]);
       osv[dt][4 * j + 2] = bf16_lo(w[1]);
@@ -373,7 +406,6 @@ __global__ __launch_bounds__(256) void comp_out_kernel(OutArgs a) {
   ss_o += __shfl_xor(ss_o, 32, kWave);
   const float rstd = 1.f / sqrtf(ss_y * (1.f / kHeadDim) + a.eps);
   const float rms_o = sqrtf(ss_o * (1.f / kHeadDim));
-  const float gv = a.gate[b * a.gs.b + h * a.gs.h + (int64_t)tokc * a.gs.n];
   const float coef = gv * rms_o * rstd;
   if (!live) return;
   uint16_t* orow = a.o + b * a.oss.b + h * a.oss.h + (int64_t)tok * a.oss.n;
@@ -418,7 +450,8 @@ hipError_t launch_comp_state(const Shape& s, const CompStateIn& in, float* state
   comp_state_kernel<<<dim3(s.B * s.H, a.chunks), 256, 0, stream>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  comp_reduce_kernel<<<s.B * s.H, 256, 0, stream>>>(a.partial, a.chunks, state);
+  comp_reduce_kernel<<<dim3(s.B * s.H, kReduceSplit), 256, 0, stream>>>(a.partial, a.chunks,
+                                                                         state);
   return hipGetLastError();
 }
 

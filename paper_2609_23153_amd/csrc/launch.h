@@ -66,7 +66,7 @@ struct CompOutIn {
   const void* q_norm;  // bf16 via qns
   const void* pq;      // bf16 [H][64][128]
   const float* rope;
-  const float* state;  // fp32 [B][H][64][128]
+  const float* state;  // fp32 [B][H][128][64] (C^T, d-major)
   const float* gamma;  // fp32 [H][128] or null
   const float* gate;   // fp32 via gs
   const void* o_s;     // bf16 via oss

@@ -168,7 +168,7 @@ def test_comp_entry_points_reject_bad_arguments():
     ds = desc(B=1, H=2, N=4096)
     st3 = (ctypes.c_int64 * 3)(2 * 4096 * 128, 4096 * 128, 128)
     need = lib.sparse_attn_workspace_size(ctypes.byref(ds), sa.SA_OP_COMP_STATE, 1)
-    assert need == 1 * 2 * 2 * 64 * 128 * 4          # 2 chunks of 2048 tokens per head
+    assert need == 1 * 2 * 4 * 64 * 128 * 4          # 4 chunks of 1024 tokens per head
     cs = lambda *a: lib.sparse_attn_comp_state(ctypes.byref(ds), *a)
     assert cs(32, P, st3, P, P, P, P, P, need, None) == -2          # rank must be 64
     assert cs(64, None, st3, P, P, P, P, P, need, None) == -1       # null k_norm

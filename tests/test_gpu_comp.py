@@ -56,7 +56,7 @@ def check_head(b, h, qn, kn, v, o_s, pq, pk, gamma, gate, rope, state, o, what, 
                rows=None):
     rp = rope.numpy()
     ref_state = O.comp_state(widen(kn[b, h]), widen(v[b, h]), widen(pk[h]), rp)
-    es = rel_l2(state[b, h], ref_state)
+    es = rel_l2(state[b, h].T, ref_state)          # the state is stored as C^T
     g = None if gamma is None else gamma[h].double().numpy()
     olr = O.comp_lowrank(widen(qn[b, h]), widen(pq[h]), rp, ref_state, g, eps)
     ref = O.comp_combine(widen(o_s[b, h]), olr, gate[b, h].double().numpy())
