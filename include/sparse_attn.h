@@ -7,8 +7,8 @@
  * M_phi keeps a few key blocks per query block, and exact softmax attention is
  * evaluated only over the kept blocks (§3 states that the sparse branch of
  * RoLA, VSA and SLA is exact softmax on a retained block subset).  The paper
- * leaves the selector open ("top-k selection, blockwise scores, ..."); this
- * library implements top-k over mean-pooled block scores.
+ * leaves the selector open (a top-k rule or block-level scores among other
+ * choices); this library implements top-k over mean-pooled block scores.
  *
  * Conventions shared by every call
  *  - All tensor pointers are DEVICE pointers; descriptors, strides and sizes
