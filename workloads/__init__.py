@@ -41,7 +41,8 @@ import numpy as np
 import torch
 
 __all__ = ["Workload", "WORKLOADS", "make_head", "make_inputs", "random_block_lists",
-           "softmax_scale", "rope_pairs_wan", "rope_table", "comp_params"]
+           "softmax_scale", "rope_pairs_wan", "rope_table", "comp_params",
+           "LINEAR_SHAPES", "linear_inputs"]
 
 
 def softmax_scale(d: int) -> float:
@@ -250,3 +251,55 @@ def comp_params(wl: Workload, rank: int = 64, gate_scale: float = 0.5, seed_extr
     gamma = 1.0 + 0.1 * torch.randn(wl.heads, d, generator=g)
     gate = gate_scale * torch.randn(wl.batch, wl.heads, wl.seqlen, generator=g)
     return pq, pk, gamma, gate
+
+
+# --------------------------------------------------------------------------
+# Inputs of the W8A8 linear layers: activations with channel outliers and
+# synthetic weights (the trained ones are not available).
+# --------------------------------------------------------------------------
+# (tokens M, in features K, out features N) of the 14B-720P block's linears:
+# the q/k/v/o projections and the two feed-forward layers (hidden 5120,
+# FFN 13824), at 75,600 tokens.
+LINEAR_SHAPES = {
+    "wan14b_720p_qkvo": (75600, 5120, 5120),
+    "wan14b_720p_ffn_up": (75600, 5120, 13824),
+    "wan14b_720p_ffn_down": (75600, 13824, 5120),
+}
+
+
+def linear_inputs(m: int, k: int, n: int, seed: int = 0, outlier_frac: float = 0.001,
+                  outlier_gain: float = 20.0, rows=None):
+    """bf16 activations X [M', K] and weights W [N, K], fp32 bias [N].
+
+    X ~ N(0, 1) with a fraction ``outlier_frac`` of the input channels (at
+    least one) multiplied by ``outlier_gain`` on every token, as the channel
+    outliers of transformer activations; each token also gets a gain
+    exp(0.5 N(0, 1)) so per-token scales differ.  W ~ N(0, 1/K) with a
+    per-output-channel gain exp(0.5 N(0, 1)); bias ~ 0.1 N(0, 1).  Every
+    token row is drawn from its own seed, so ``rows`` (a list of token
+    indices) regenerates just those rows."""
+    gw = _gen(seed, 4242)
+    w = torch.randn(n, k, generator=gw) / math.sqrt(k)
+    w = (w * torch.exp(0.5 * torch.randn(n, 1, generator=gw))).to(torch.bfloat16)
+    bias = 0.1 * torch.randn(n, generator=gw)
+    n_out = max(1, int(round(outlier_frac * k)))
+    ch = torch.randperm(k, generator=gw)[:n_out]
+    chan_gain = torch.ones(k)
+    chan_gain[ch] = outlier_gain
+    step = 256                                   # token rows drawn per generator
+    rows = list(range(m)) if rows is None else list(rows)
+    x = torch.empty(len(rows), k, dtype=torch.bfloat16)
+    by_chunk = {}
+    for i, r in enumerate(rows):
+        if not 0 <= r < m:
+            raise IndexError(r)
+        by_chunk.setdefault(r // step, []).append((i, r))
+    for c, members in by_chunk.items():
+        g = _gen(seed, 4243, c)
+        lo, hi = c * step, min(m, (c + 1) * step)
+        xc = torch.randn(hi - lo, k, generator=g)
+        xc = (xc * torch.exp(0.5 * torch.randn(hi - lo, 1, generator=g)) * chan_gain).to(torch.bfloat16)
+        dst = torch.tensor([i for i, _ in members])
+        src = torch.tensor([r - lo for _, r in members])
+        x[dst] = xc[src]
+    return x, w, bias
