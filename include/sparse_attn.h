@@ -222,6 +222,46 @@ int sparse_attn_comp_out(const sparse_attn_desc* desc, int32_t rank, const void*
                          const float* state, const float* gamma, float eps, const float* gate,
                          const int64_t gate_stride[3], const void* o_s, void* o, void* stream);
 
+/*
+ * W8A8 FP8 linear layers (paper §4.3: the attention and feed-forward
+ * projections run on OCP e4m3 weights and activations; each weight output
+ * channel has a static scale fixed offline, each activation token a scale
+ * taken at run time, and the per-token quantisation is one fused pass).
+ *
+ * sparse_attn_quant_rows_fp8: per-row quantisation of bf16 x [rows][cols]
+ * (row stride ldx elements) in one pass: a = max(max_k |x[r][k]|, 2^-100),
+ * scale[r] = fp32(a / 448), q[r][k] = e4m3(fp32(x[r][k] * fp32(448 / a))),
+ * rounded to nearest with ties to even (every fp32 step correctly rounded).
+ * Used per token on activations and, once offline, per output channel on
+ * weights [N][K].
+ *  x      bf16 device pointer, 16-byte aligned; ldx >= cols, ldx % 8 == 0
+ *  rows   >= 0 (0 launches nothing); cols >= 8, cols % 8 == 0
+ *  q      uint8 [rows][cols] contiguous, 16-byte aligned (written)
+ *  scale  fp32 [rows] (written)
+ * Errors: SA_ERR_INVALID_ARG for null pointers, misalignment or bad sizes. */
+int sparse_attn_quant_rows_fp8(const void* x, int64_t rows, int64_t cols, int64_t ldx, uint8_t* q,
+                               float* scale, void* stream);
+
+/*
+ * sparse_attn_linear_w8a8: y[m][n] = bf16((sum_k dec(xq[m][k]) dec(wq[n][k]))
+ * * sx[m] * sw[n] + bias[n]) with fp32 accumulation on the fp8 matrix cores
+ * (the fp32 epilogue is fmaf(acc * sx[m], sw[n], bias[n]), rounded to nearest
+ * even bf16).
+ *  xq, sx   activation codes [M][K] (row stride ldx bytes) and scales [M], as
+ *           written by sparse_attn_quant_rows_fp8
+ *  wq, sw   weight codes [N][K] (row stride ldw bytes) and scales [N]
+ *  bias     fp32 [N] or NULL
+ *  y        bf16 [M][N], row stride ldy elements (written)
+ * Layout rules: K % 64 == 0 and K >= 64; N % 8 == 0; M, N >= 0 (either 0
+ * launches nothing); ldx, ldw >= K and multiples of 16; ldy >= N and a multiple
+ * of 8; xq, wq, sw, bias and y 16-byte aligned; M, N < 2^31 and 256 * ldx,
+ * 256 * ldw < 2^32.
+ * Errors: SA_ERR_INVALID_ARG for null pointers, misalignment or bad sizes;
+ * SA_ERR_UNSUPPORTED for sizes beyond the limits above. */
+int sparse_attn_linear_w8a8(const uint8_t* xq, const float* sx, int64_t ldx, const uint8_t* wq,
+                            const float* sw, int64_t ldw, const float* bias, void* y, int64_t ldy,
+                            int64_t M, int64_t N, int64_t K, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

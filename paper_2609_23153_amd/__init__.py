@@ -20,6 +20,7 @@ __all__ = [
     "sparse_attn_num_tiles", "sparse_attn_select", "sparse_attn_schedule", "sparse_attn_fwd",
     "sparse_attn_quant_fp8", "sparse_attn_fwd_fp8", "sparse_attn_comp_state",
     "sparse_attn_comp_out", "SA_OP_COMP_STATE", "COMP_RANK", "make_desc", "EXPORTED_SYMBOLS",
+    "sparse_attn_quant_rows_fp8", "sparse_attn_linear_w8a8",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsparseattn.so")
@@ -33,7 +34,8 @@ EXPORTED_SYMBOLS = (
     "sparse_attn_version", "sparse_attn_status_str", "sparse_attn_keep_count",
     "sparse_attn_workspace_size", "sparse_attn_num_tiles", "sparse_attn_select",
     "sparse_attn_schedule", "sparse_attn_fwd", "sparse_attn_quant_fp8", "sparse_attn_fwd_fp8",
-    "sparse_attn_comp_state", "sparse_attn_comp_out",
+    "sparse_attn_comp_state", "sparse_attn_comp_out", "sparse_attn_quant_rows_fp8",
+    "sparse_attn_linear_w8a8",
 )
 
 
@@ -88,6 +90,12 @@ def library() -> ctypes.CDLL:
                                                       _P, _P, ctypes.c_size_t, _P]),
             "sparse_attn_comp_out": (ctypes.c_int, [D, ctypes.c_int32, _P, _I64P, _P, _P, _P,
                                                     _P, ctypes.c_float, _P, _I64P, _P, _P, _P]),
+            "sparse_attn_quant_rows_fp8": (ctypes.c_int, [_P, ctypes.c_int64, ctypes.c_int64,
+                                                          ctypes.c_int64, _P, _P, _P]),
+            "sparse_attn_linear_w8a8": (ctypes.c_int, [_P, _P, ctypes.c_int64, _P, _P,
+                                                       ctypes.c_int64, _P, _P, ctypes.c_int64,
+                                                       ctypes.c_int64, ctypes.c_int64,
+                                                       ctypes.c_int64, _P]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(lib, name)
@@ -324,3 +332,51 @@ def sparse_attn_comp_out(q_norm, pq, rope, state, gate, o_s, gamma=None, eps: fl
                                         _st3(gate.stride()), _ptr(o_s), _ptr(o), _stream(q_norm))
     _check(st, "sparse_attn_comp_out")
     return o
+
+
+# ------------------------------------------------------- W8A8 fp8 linear layers
+def _rows_2d(t, name, dtype):
+    if t.dim() != 2 or t.dtype != dtype or t.stride(1) != 1:
+        raise ValueError(f"{name} must be a 2-D {dtype} tensor with unit column stride")
+
+
+def sparse_attn_quant_rows_fp8(x, q=None, scale=None):
+    """Per-row e4m3 quantisation of bf16 x [rows, cols] (any row stride).
+    Returns (q uint8 [rows, cols] contiguous, scale fp32 [rows])."""
+    _rows_2d(x, "x", torch.bfloat16)
+    rows, cols = x.shape
+    if q is None:
+        q = torch.empty(rows, cols, dtype=torch.uint8, device=x.device)
+    if scale is None:
+        scale = torch.empty(rows, dtype=torch.float32, device=x.device)
+    if not q.is_contiguous() or tuple(q.shape) != (rows, cols) or q.dtype != torch.uint8:
+        raise ValueError("q must be a contiguous uint8 [rows, cols] tensor")
+    _dense(scale, "scale", torch.float32)
+    st = library().sparse_attn_quant_rows_fp8(_ptr(x), rows, cols, x.stride(0), _ptr(q),
+                                              _ptr(scale), _stream(x))
+    _check(st, "sparse_attn_quant_rows_fp8")
+    return q, scale
+
+
+def sparse_attn_linear_w8a8(xq, sx, wq, sw, bias=None, y=None):
+    """y [M, N] bf16 = (xq wq^T) * sx sw^T + bias over e4m3 codes xq [M, K],
+    wq [N, K] (unit column stride, any row stride) and fp32 scales sx [M],
+    sw [N]; bias fp32 [N] or None."""
+    _rows_2d(xq, "xq", torch.uint8)
+    _rows_2d(wq, "wq", torch.uint8)
+    M, K = xq.shape
+    N = wq.shape[0]
+    if wq.shape[1] != K:
+        raise ValueError("xq and wq must have the same K")
+    _dense(sx, "sx", torch.float32)
+    _dense(sw, "sw", torch.float32)
+    if bias is not None:
+        _dense(bias, "bias", torch.float32)
+    if y is None:
+        y = torch.empty(M, N, dtype=torch.bfloat16, device=xq.device)
+    _rows_2d(y, "y", torch.bfloat16)
+    st = library().sparse_attn_linear_w8a8(
+        _ptr(xq), _ptr(sx), xq.stride(0), _ptr(wq), _ptr(sw), wq.stride(0),
+        None if bias is None else _ptr(bias), _ptr(y), y.stride(0), M, N, K, _stream(xq))
+    _check(st, "sparse_attn_linear_w8a8")
+    return y

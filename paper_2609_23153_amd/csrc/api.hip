@@ -219,6 +219,49 @@ int sparse_attn_fwd_fp8(const sparse_attn_desc* desc, const uint8_t* q8, const f
   return launch_status(sa::launch_fwd_fp8(s, a, static_cast<hipStream_t>(stream)));
 }
 
+int sparse_attn_quant_rows_fp8(const void* x, int64_t rows, int64_t cols, int64_t ldx, uint8_t* q,
+                               float* scale, void* stream) {
+  if (!x || !q || !scale) return SA_ERR_INVALID_ARG;
+  if (rows < 0 || cols < 8 || (cols & 7) != 0 || ldx < cols || (ldx & 7) != 0)
+    return SA_ERR_INVALID_ARG;
+  if (!aligned16(x) || !aligned16(q)) return SA_ERR_INVALID_ARG;
+  if (cols > ((int64_t)1 << 30) || rows > ((int64_t)1 << 40)) return SA_ERR_UNSUPPORTED;
+  return launch_status(sa::launch_quant_rows_fp8(x, ldx, rows, (int)cols, q, scale,
+                                                 static_cast<hipStream_t>(stream)));
+}
+
+int sparse_attn_linear_w8a8(const uint8_t* xq, const float* sx, int64_t ldx, const uint8_t* wq,
+                            const float* sw, int64_t ldw, const float* bias, void* y, int64_t ldy,
+                            int64_t M, int64_t N, int64_t K, void* stream) {
+  if (!xq || !sx || !wq || !sw || !y) return SA_ERR_INVALID_ARG;
+  if (M < 0 || N < 0 || K < 64 || (K & 63) != 0 || (N & 7) != 0) return SA_ERR_INVALID_ARG;
+  if (ldx < K || (ldx & 15) != 0 || ldw < K || (ldw & 15) != 0 || ldy < N || (ldy & 7) != 0)
+    return SA_ERR_INVALID_ARG;
+  if (!aligned16(xq) || !aligned16(wq) || !aligned16(sw) || (bias && !aligned16(bias)) ||
+      !aligned16(y))
+    return SA_ERR_INVALID_ARG;
+  // 32-bit tile counts and per-tile byte offsets of the kernel
+  if (M >= ((int64_t)1 << 31) || N >= ((int64_t)1 << 31) || K >= ((int64_t)1 << 31))
+    return SA_ERR_UNSUPPORTED;
+  if (256 * ldx >= ((int64_t)1 << 32) || 256 * ldw >= ((int64_t)1 << 32)) return SA_ERR_UNSUPPORTED;
+  if (((M + 255) / 256) * ((N + 255) / 256) >= ((int64_t)1 << 31)) return SA_ERR_UNSUPPORTED;
+  sa::LinearIn in{};
+  in.xq = xq;
+  in.sx = sx;
+  in.wq = wq;
+  in.sw = sw;
+  in.bias = bias;
+  in.y = y;
+  in.ldx = ldx;
+  in.ldw = ldw;
+  in.ldy = ldy;
+  in.M = M;
+  in.N = N;
+  in.K = K;
+  in.group_m = 0;
+  return launch_status(sa::launch_linear_w8a8(in, static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"
 
 // ---- compensation branch (paper §2 Eq. comp-sparse, §4.1) -----------------

@@ -79,6 +79,26 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return f32_to_bf16_rne(lo) | (f32_to_bf16_rne(hi) << 16);
 }
 
+// OCP e4m3fn code of y for |y| < 464 (callers scale so that |y| <= 448, up
+// to one fp32 rounding): nearest value, ties to even, sign bit kept (so -0
+// and tiny negatives give 0x80).  Integer arithmetic on the fp32 fields.
+__device__ __forceinline__ uint32_t e4m3_rne(float y) {
+  const uint32_t u = __float_as_uint(y);
+  const uint32_t sign = (u >> 24) & 0x80u;
+  const uint32_t a = u & 0x7fffffffu;
+  uint32_t code;
+  if (a < 0x3c800000u) {  // |y| < 2^-6: e4m3 subnormal grid of step 2^-9
+    code = (uint32_t)__builtin_rintf(__uint_as_float(a) * 512.f);  // 0 .. 8
+  } else {
+    const uint32_t e = a >> 23;          // fp32 biased exponent (>= 121)
+    const uint32_t m3 = (a >> 20) & 7u;  // top 3 mantissa bits
+    const uint32_t rem = a & 0xfffffu;
+    const uint32_t up = (rem > 0x80000u) || (rem == 0x80000u && (m3 & 1u));
+    code = (((e - 120u) << 3) | m3) + up;  // e4m3 exponent bias 7 = fp32 bias 127 - 120
+  }
+  return sign | code;
+}
+
 // Whole-wave reductions through DPP-free cross-lane shuffles.
 __device__ __forceinline__ float wave_max(float x) {
 #pragma unroll

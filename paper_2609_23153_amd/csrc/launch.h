@@ -83,4 +83,22 @@ hipError_t launch_comp_out(const Shape& s, const CompOutIn& in, hipStream_t stre
 hipError_t launch_quant_fp8(const Shape& s, const void* x, Strides xs, uint8_t* x8,
                             float* scale, hipStream_t stream);
 
+// ---- W8A8 fp8 linear layers -----------------------------------------------
+// Per-row e4m3 quantisation of bf16 x [rows][cols] (row stride ldx elements)
+// into q [rows][cols] (contiguous) and fp32 scale [rows].
+hipError_t launch_quant_rows_fp8(const void* x, int64_t ldx, int64_t rows, int cols, uint8_t* q,
+                                 float* scale, hipStream_t stream);
+struct LinearIn {
+  const uint8_t* xq;  // [M][K] activation codes, row stride ldx bytes
+  const float* sx;    // [M]
+  const uint8_t* wq;  // [N][K] weight codes, row stride ldw bytes
+  const float* sw;    // [N]
+  const float* bias;  // [N] or null
+  void* y;            // bf16 [M][N], row stride ldy elements
+  int64_t ldx, ldw, ldy;
+  int64_t M, N, K;
+  int group_m;        // tile rows per launch-order group (0: default)
+};
+hipError_t launch_linear_w8a8(const LinearIn& in, hipStream_t stream);
+
 }  // namespace sa

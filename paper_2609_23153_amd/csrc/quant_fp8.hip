@@ -16,25 +16,6 @@ namespace {
 
 constexpr int kQThreads = 256;
 
-// |y| <= 448 (guaranteed by the scale choice): nearest e4m3fn code, ties to
-// even, sign bit kept (so -0 and tiny negatives give 0x80).
-__device__ __forceinline__ uint32_t e4m3_rne(float y) {
-  const uint32_t u = __float_as_uint(y);
-  const uint32_t sign = (u >> 24) & 0x80u;
-  const uint32_t a = u & 0x7fffffffu;
-  uint32_t code;
-  if (a < 0x3c800000u) {  // |y| < 2^-6: e4m3 subnormal grid of step 2^-9
-    code = (uint32_t)__builtin_rintf(__uint_as_float(a) * 512.f);  // 0 .. 8
-  } else {
-    const uint32_t e = a >> 23;          // fp32 biased exponent (>= 121)
-    const uint32_t m3 = (a >> 20) & 7u;  // top 3 mantissa bits
-    const uint32_t rem = a & 0xfffffu;
-    const uint32_t up = (rem > 0x80000u) || (rem == 0x80000u && (m3 & 1u));
-    code = (((e - 120u) << 3) | m3) + up;  // e4m3 exponent bias 7 = fp32 bias 127 - 120
-  }
-  return sign | code;
-}
-
 // Smallest e with amax <= 448 * 2^e, clamped to >= -126 so that 2^e is a
 // normal fp32 (and a valid E8M0 scale code); 0 for an all-zero block.
 __device__ __forceinline__ int scale_exponent(float amax) {

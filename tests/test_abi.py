@@ -183,3 +183,40 @@ def test_comp_entry_points_reject_bad_arguments():
     assert co(64, P, st3, P, P, P, None, -1.0, P, g3, P, P, None) == -1      # eps < 0
     assert co(64, P, st3, P, P, P, None, 1e-6, P, bad_g3, P, P, None) == -1  # gate stride
     assert co(64, P, st3, P, P, P, MIS, 1e-6, P, g3, P, P, None) == -1       # gamma misaligned
+
+
+def test_w8a8_linear_entry_points_reject_bad_arguments():
+    lib = sa.library()
+    q = lib.sparse_attn_quant_rows_fp8
+    assert q(None, 4, 64, 64, P, P, None) == -1          # null x
+    assert q(P, 4, 60, 64, P, P, None) == -1             # cols % 8
+    assert q(P, 4, 64, 32, P, P, None) == -1             # ldx < cols
+    assert q(P, 4, 64, 68, P, P, None) == -1             # ldx % 8
+    assert q(MIS, 4, 64, 64, P, P, None) == -1           # misaligned x
+    assert q(P, -1, 64, 64, P, P, None) == -1            # rows < 0
+    assert q(P, 0, 64, 64, P, P, None) == 0              # empty: nothing launched
+    lin = lib.sparse_attn_linear_w8a8
+    ok = (P, P, 128, P, P, 128, None, P, 256, 300, 256, 128, None)
+
+    def call(**kw):
+        names = ("xq", "sx", "ldx", "wq", "sw", "ldw", "bias", "y", "ldy", "M", "N", "K", "s")
+        args = dict(zip(names, ok))
+        args.update(kw)
+        return lin(*[args[n] for n in names])
+
+    assert call(M=0) == 0                                # empty: nothing launched
+    assert call(N=0, ldy=0) == 0
+    assert call(xq=None) == -1
+    assert call(sw=None) == -1
+    assert call(K=96, ldx=128, ldw=128) == -1            # K % 64
+    assert call(K=0) == -1
+    assert call(N=260, ldy=264) == -1                    # N % 8
+    assert call(ldx=120) == -1                           # ldx < K
+    assert call(ldw=136) == -1                           # ldw % 16
+    assert call(ldy=255) == -1                           # ldy < N
+    assert call(ldy=260) == -1                           # ldy % 8
+    assert call(y=ctypes.c_void_p((1 << 20) + 8)) == -1  # y not 16-byte aligned
+    assert call(wq=MIS) == -1                            # misaligned codes
+    assert call(bias=MIS) == -1                          # misaligned bias
+    assert call(M=-5) == -1
+    assert call(ldx=1 << 24, K=64) == -2                 # 256 * ldx does not fit 32 bits

@@ -1,0 +1,188 @@
+"""GPU parity of the W8A8 FP8 linear layer (paper §4.3) through the C ABI
+against the fp64 oracle on identical seeded inputs.
+
+Codes and scales of the per-row quantisation are compared bit for bit (both
+sides take the fp32 roundings that decide them).  The product is compared
+with the oracle's fp64 product of the same codes.  The GPU's error has three
+parts, with y' the fp32 value before the bf16 rounding and y the exact one:
+  * the bf16 rounding, |bf16(y') - y'| <= 2^-8 |y'|;
+  * the matrix cores' sums: one fp8 MFMA adds its 64 exact products and the
+    accumulator with a fixed-point alignment of about 17 bits below the
+    largest term rather than fp32 rounding (a measured case: 2^16 plus 63
+    products of 2^-6 returns 2^16 + 0.375 where fp32 gives 2^16 + 0.984), so
+    each of the K/64 steps may err by up to 2^-16 of the sum of the
+    magnitudes it adds, bounded by absref = sum_k |x_k w_k| s_x s_w;
+  * four fp32 roundings in the scale-and-bias epilogue, 2^-22 |y|.
+Hence |got - y| <= 2^-8 |y| + (1 + 2^-8)((K/64) 2^-16 absref + 2^-22 |y|).
+The rel-L2 bar 5e-3 is twice the largest RMS relative bf16 rounding error
+(2^-8 / sqrt(3)), so a wrong tile or K slice cannot hide in it."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2609_23153_amd as sa
+import workloads as W
+from gpu_helpers import rel_l2, say
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    sa.library()
+    yield
+    torch.cuda.synchronize()
+
+
+def check_quant(x_cpu, q, s, what, rows=None):
+    """Bit-exact codes and scales of the given rows (all by default)."""
+    rows = np.arange(x_cpu.shape[0]) if rows is None else np.asarray(rows)
+    ref_q, ref_s = O.quant_rows_fp8(x_cpu[rows].float().numpy())
+    got_q = q[rows].cpu().numpy() if isinstance(q, torch.Tensor) else q[rows]
+    got_s = s[rows].cpu().numpy() if isinstance(s, torch.Tensor) else s[rows]
+    nbad = int((got_q != ref_q).sum())
+    say(f"  {what}: {len(rows)} rows, code mismatches {nbad}, "
+        f"scale mismatches {int((got_s != ref_s).sum())}")
+    assert nbad == 0
+    assert np.array_equal(got_s.view(np.uint32), ref_s.view(np.uint32))
+    return ref_q, ref_s
+
+
+def check_linear(y, a8, sa_, w8, sw, bias, what, rows=None):
+    rows = np.arange(a8.shape[0]) if rows is None else np.asarray(rows)
+    b = None if bias is None else bias.numpy()
+    ref = O.linear_w8a8(a8[rows], sa_[rows], w8, sw, b)
+    table = O.e4m3_table()
+    absref = (np.abs(table[a8[rows].astype(np.int64)]) @ np.abs(table[w8.astype(np.int64)]).T
+              * sa_[rows].astype(np.float64)[:, None] * sw.astype(np.float64)[None, :])
+    got = y.cpu()[rows].double().numpy() if isinstance(y, torch.Tensor) else y[rows]
+    K = a8.shape[1]
+    bound = (2.0 ** -8 * np.abs(ref)
+             + (1 + 2.0 ** -8) * ((K / 64) * 2.0 ** -16 * absref + 2.0 ** -22 * np.abs(ref))
+             + 1e-30)
+    err = np.abs(got - ref)
+    e = rel_l2(got, ref)
+    say(f"  {what}: rel_l2={e:.3e}  max err/bound={float((err / bound).max()):.3f}")
+    assert e <= 5e-3
+    assert np.all(err <= bound), float((err / bound).max())
+
+
+def quant_gpu(x_cpu, pad_cols=0):
+    """Quantise on the GPU; pad_cols > 0 passes a row-strided view."""
+    if pad_cols:
+        wide = torch.zeros(x_cpu.shape[0], x_cpu.shape[1] + pad_cols, dtype=torch.bfloat16)
+        wide[:, :x_cpu.shape[1]] = x_cpu
+        xd = wide.to(DEV)[:, :x_cpu.shape[1]]
+        assert xd.stride(0) == x_cpu.shape[1] + pad_cols
+    else:
+        xd = x_cpu.to(DEV)
+    q, s = sa.sparse_attn_quant_rows_fp8(xd)
+    torch.cuda.synchronize()
+    return q, s
+
+
+@pytest.mark.parametrize("rows,cols,pad", [
+    (300, 5120, 0),      # a 5120-channel activation row (ten 16-byte chunks per lane)
+    (77, 64, 8),         # short rows, row-strided input
+    (9, 13824, 0),       # the FFN hidden width (register-resident, 28 chunks)
+    (5, 20480, 16),      # beyond the register-resident widths: two-pass kernel
+    (3, 1032, 0),        # ragged last chunk
+])
+def test_quant_rows_bit_exact(rows, cols, pad):
+    x, _, _ = W.linear_inputs(rows, cols, 4, seed=rows + cols)
+    q, s = quant_gpu(x, pad)
+    check_quant(x, q, s, f"quant {rows}x{cols} pad {pad}")
+
+
+def test_quant_rows_edge_values():
+    """A zero row, a row of bf16 subnormals (amax below the 2^-100 floor),
+    a row with one huge value, exact ties of the e4m3 grid and -0."""
+    cols = 256
+    x = torch.zeros(6, cols)
+    x[1, :] = torch.linspace(-1e-38, 1e-38, cols)
+    x[2, :] = torch.randn(cols, generator=torch.Generator().manual_seed(3))
+    x[2, 17] = 3.0e38
+    x[3, :] = 448.0
+    x[3, 1::2] = torch.tensor([1.0 + k / 16.0 for k in range(cols // 2)]) * 2.0 ** -3  # ties
+    x[4, :] = -0.0
+    x[5, :] = torch.randn(cols, generator=torch.Generator().manual_seed(4)) * 2.0 ** -60
+    x = x.to(torch.bfloat16)
+    q, s = quant_gpu(x)
+    check_quant(x, q, s, "edge rows")
+
+
+def linear_case(M, N, K, seed, bias=True, pad_y=0):
+    x, w, b = W.linear_inputs(M, K, N, seed=seed)
+    bias_t = b if bias else None
+    xq, sx = quant_gpu(x)
+    wq, sw = quant_gpu(w)
+    a8, sa_ = check_quant(x, xq, sx, f"x {M}x{K}")
+    w8, sw_ = check_quant(w, wq, sw, f"w {N}x{K}")
+    if pad_y:
+        ybuf = torch.full((M, N + pad_y), float("nan"), dtype=torch.bfloat16, device=DEV)
+        y = ybuf[:, :N]
+    else:
+        ybuf = y = None
+    y = sa.sparse_attn_linear_w8a8(xq, sx, wq, sw, None if bias_t is None else bias_t.to(DEV), y=y)
+    torch.cuda.synchronize()
+    if pad_y:   # the padding columns are untouched
+        assert torch.isnan(ybuf[:, N:].float()).all()
+    return y, a8, sa_, w8, sw_, bias_t
+
+
+@pytest.mark.parametrize("M,N,K,bias,pad_y", [
+    (512, 512, 512, True, 0),     # 2 x 2 tiles, 8 stages
+    (300, 200, 192, True, 0),     # ragged tiles in both M and N, 3 stages (< pipeline depth)
+    (1, 8, 64, False, 0),         # one row, one stage
+    (777, 1032, 256, True, 16),   # row-strided output, ragged everywhere
+    (64, 256, 1088, False, 0),    # 17 stages (odd), single tile
+])
+def test_linear_small(M, N, K, bias, pad_y):
+    y, a8, sa_, w8, sw, b = linear_case(M, N, K, seed=M + N + K, bias=bias, pad_y=pad_y)
+    check_linear(y, a8, sa_, w8, sw, b, f"linear M{M} N{N} K{K}")
+
+
+def test_linear_deterministic_and_zero_rows():
+    M, N, K = 260, 264, 320
+    x, w, b = W.linear_inputs(M, K, N, seed=11)
+    x[5] = 0
+    xd, wd = x.to(DEV), w.to(DEV)
+    xq, sx = sa.sparse_attn_quant_rows_fp8(xd)
+    wq, sw = sa.sparse_attn_quant_rows_fp8(wd)
+    y1 = sa.sparse_attn_linear_w8a8(xq, sx, wq, sw, b.to(DEV))
+    y2 = sa.sparse_attn_linear_w8a8(xq, sx, wq, sw, b.to(DEV))
+    torch.cuda.synchronize()
+    assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
+    # a zero token row yields exactly the bias (rounded to bf16)
+    assert torch.equal(y1[5].cpu(), b.to(torch.bfloat16))
+
+
+@pytest.mark.parametrize("name,m_sub", [("wan14b_720p_qkvo", None), ("wan14b_720p_ffn_down", 2048)])
+def test_linear_full_size(name, m_sub):
+    """The 14B-720P projection at 75,600 tokens (the benchmark's launch), and
+    the FFN down projection (K = 13824) on 2048 tokens: quantisation and
+    product checked on sampled tokens, every output checked finite."""
+    M, K, N = W.LINEAR_SHAPES[name]
+    if m_sub:
+        M = m_sub
+    x, w, b = W.linear_inputs(M, K, N, seed=7)
+    say(f"  {name}: M={M} K={K} N={N} generated")
+    xd, wd = x.to(DEV), w.to(DEV)
+    xq, sx = sa.sparse_attn_quant_rows_fp8(xd)
+    wq, sw = sa.sparse_attn_quant_rows_fp8(wd)
+    y = sa.sparse_attn_linear_w8a8(xq, sx, wq, sw, b.to(DEV))
+    torch.cuda.synchronize()
+    assert torch.isfinite(y.float()).all()
+    rng = np.random.default_rng(1)
+    rows = np.unique(np.concatenate([[0, 255, 256, M - 1], rng.integers(0, M, 60)]))
+    a8, sa_ = check_quant(x, xq, sx, f"{name} x", rows)
+    w8, sw_ = check_quant(w, wq, sw, f"{name} w")
+    a8_full = np.zeros((M, K), np.uint8)
+    sa_full = np.zeros(M, np.float32)
+    a8_full[rows], sa_full[rows] = a8, sa_
+    check_linear(y, a8_full, sa_full, w8, sw_, b, f"{name} linear", rows)
