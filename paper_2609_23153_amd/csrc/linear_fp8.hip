@@ -170,184 +170,291 @@ struct LinArgs {
   int tiles_m, tiles_n, group_m;
 };
 
-__global__ __launch_bounds__(256) void linear_w8a8_kernel(LinArgs a) {
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[kStages * kStageBytes];
+constexpr int kOutLds = 4 * 4096;    // per wave: 32 rows x 64 output channels of bf16
+constexpr int kScaleLds = 4 * 1024;  // sx | sw | bias of the current tile (+ one spare)
+constexpr int kLdsBytes = kStages * kStageBytes + kOutLds + kScaleLds;
 
-  // tile of this workgroup: contiguous runs per XCD (dispatch deals
-  // workgroup ids round-robin over the 8 XCDs), grouped order inside
-  const int T = a.tiles_m * a.tiles_n;
-  const int id = blockIdx.x, xcd = id & 7, local = id >> 3;
-  const int per = T >> 3, rem = T & 7;
-  const int t = xcd * per + min(xcd, rem) + local;
+// Lane index within the wavefront, recomputed at every use (volatile asm of
+// the two mbcnt instructions), so that no register holds it across a loop.
+__device__ __forceinline__ int fresh_lane_id() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+
+// Tile t (in the grouped order) -> its first token and output channel.
+__device__ __forceinline__ void tile_origin(const LinArgs& a, int t, int& m0, int& n0) {
   const int gsz = a.group_m * a.tiles_n;
   const int grp = t / gsz;
   const int first_m = grp * a.group_m;
   const int gm = min(a.group_m, a.tiles_m - first_m);
   const int within = t - grp * gsz;
-  const int m0 = (first_m + within % gm) * kBM;
-  const int n0 = (within / gm) * kBN;
+  m0 = (first_m + within % gm) * kBM;
+  n0 = (within / gm) * kBN;
+}
+
+// Global -> LDS copy of one stage (K slice `k0` of the tile's 256 weight rows
+// and 256 activation rows) into the stage buffer at LDS byte address `base`.
+__device__ __forceinline__ void copy_stage(uint32_t base, __amdgpu_buffer_rsrc_t wr,
+                                           __amdgpu_buffer_rsrc_t xr, const uint32_t (&woff)[4],
+                                           const uint32_t (&xoff)[4], uint32_t k0) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) dma16(base + 16 * i * kBK, wr, woff[i], k0);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) dma16(base + kHalfBytes + 16 * i * kBK, xr, xoff[i], k0);
+}
+
+// A (weights) and B (activations) fragments of one stage buffer `sb`.
+__device__ __forceinline__ void read_frags(const uint8_t* sb, uint32_t fa0, uint32_t fa1,
+                                           uint32_t fb0, uint32_t fb1, i32x8 (&fa)[4],
+                                           i32x8 (&fb)[4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const u32x4 lo = *reinterpret_cast<const u32x4*>(sb + fa0 + 32 * i * kBK);
+    const u32x4 hi = *reinterpret_cast<const u32x4*>(sb + fa1 + 32 * i * kBK);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      fa[i][e] = (int)lo[e];
+      fa[i][4 + e] = (int)hi[e];
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const u32x4 lo = *reinterpret_cast<const u32x4*>(sb + fb0 + 32 * j * kBK);
+    const u32x4 hi = *reinterpret_cast<const u32x4*>(sb + fb1 + 32 * j * kBK);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      fb[j][e] = (int)lo[e];
+      fb[j][4 + e] = (int)hi[e];
+    }
+  }
+}
+
+// Half the MFMAs of a stage: accumulator columns 2 half, 2 half + 1.  FIRST
+// starts the accumulators from zero (the first stage of a tile).
+template <bool FIRST>
+__device__ __forceinline__ void mfma_half(f32x16 (&acc)[4][4], const i32x8 (&fa)[4],
+                                          const i32x8 (&fb)[4], int half) {
+  const f32x16 zero = {};
+#pragma unroll
+  for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int j = 2 * half + jj;
+      acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+          fa[i], fb[j], FIRST ? zero : acc[i][j], 0, 0, 0, kOneE8m0, 0, kOneE8m0);
+    }
+}
+
+// Persistent: one workgroup per CU walks its share of the output tiles, and
+// the copy pipeline runs on across tile boundaries (the first stages of the
+// next tile are in flight while the current one finishes and is stored).
+__global__ __launch_bounds__(256) void linear_w8a8_kernel(LinArgs a) {
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[kLdsBytes];
+  constexpr int kOutOff = kStages * kStageBytes;  // byte offsets in lds
+  constexpr int kScaleOff = kOutOff + kOutLds;
+
+  // Tiles of this workgroup.  Dispatch deals workgroup ids round-robin over
+  // the 8 XCDs; XCD x owns a contiguous run of the grouped tile order, and its
+  // workgroups take that run's tiles in turn, so the ones running together on
+  // an XCD share activation and weight rows in its L2.
+  const int T = a.tiles_m * a.tiles_n;
+  const int G = gridDim.x;
+  const int id = blockIdx.x, xcd = id & 7, lw = id >> 3;
+  const int wgs_x = (G >> 3) + (xcd < (G & 7) ? 1 : 0);
+  const int tiles_x = (T >> 3) + (xcd < (T & 7) ? 1 : 0);
+  const int t_first = xcd * (T >> 3) + min(xcd, T & 7) + lw;
+  const int ntiles = lw < tiles_x ? (tiles_x - lw + wgs_x - 1) / wgs_x : 0;
+  if (ntiles == 0) return;
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int wv = __builtin_amdgcn_readfirstlane(wave);
-  const int wn = wave >> 1, wm = wave & 1;  // this wave's 128 x 128 quarter
+  const int wn = wv >> 1, wm = wv & 1;  // this wave's 128 x 128 quarter (uniform)
   const int g = lane >> 5, l32 = lane & 31;
-
-  // copies: wave w moves rows 64w .. 64w+63 of both halves, 16 rows per
-  // instruction; lane l lands in slot l%4 of row l/4
-  const auto wr = make_rsrc(a.w + (int64_t)n0 * a.ldw, (uint32_t)(min(kBN, a.N - n0) * a.ldw));
-  const auto xr = make_rsrc(a.x + (int64_t)m0 * a.ldx, (uint32_t)(min(kBM, a.M - m0) * a.ldx));
-  uint32_t woff[4], xoff[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = 64 * wave + 16 * i + (lane >> 2);
-    const int c = swz64(row, lane & 3);  // logical chunk stored in this slot (the map is an involution)
-    woff[i] = (uint32_t)(row * a.ldw + 16 * c);
-    xoff[i] = (uint32_t)(row * a.ldx + 16 * c);
-  }
+  const int S = a.K / kBK;
   const uint32_t lds0 = lds_addr(lds);
-  auto copy_stage = [&](int st, int buf) {
-    const uint32_t base = lds0 + (uint32_t)(buf * kStageBytes + 64 * wv * kBK);
-    const uint32_t k0 = (uint32_t)(st * kBK);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) dma16(base + 16 * i * kBK, wr, woff[i], k0);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) dma16(base + kHalfBytes + 16 * i * kBK, xr, xoff[i], k0);
-  };
 
-  // fragment addresses: A (weights) row 128 wn + 32 i + l32, B (activations)
-  // row 128 wm + 32 j + l32; bytes 32 g .. 32 g + 31 of the row = logical
-  // chunks 2g, 2g + 1.  The swizzle term (row >> 2) & 3 depends on l32 only.
-  const int s1 = (l32 >> 2) & 3;
-  const uint32_t fa0 = (uint32_t)((128 * wn + l32) * kBK + 16 * ((2 * g) ^ s1));
-  const uint32_t fa1 = (uint32_t)((128 * wn + l32) * kBK + 16 * ((2 * g + 1) ^ s1));
-  const uint32_t fb0 = (uint32_t)(kHalfBytes + (128 * wm + l32) * kBK + 16 * ((2 * g) ^ s1));
-  const uint32_t fb1 = (uint32_t)(kHalfBytes + (128 * wm + l32) * kBK + 16 * ((2 * g + 1) ^ s1));
-  auto read_frags = [&](int buf, i32x8 (&fa)[4], i32x8 (&fb)[4]) {
-    const uint8_t* sb = lds + buf * kStageBytes;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const u32x4 lo = *reinterpret_cast<const u32x4*>(sb + fa0 + 32 * i * kBK);
-      const u32x4 hi = *reinterpret_cast<const u32x4*>(sb + fa1 + 32 * i * kBK);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        fa[i][e] = (int)lo[e];
-        fa[i][4 + e] = (int)hi[e];
-      }
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const u32x4 lo = *reinterpret_cast<const u32x4*>(sb + fb0 + 32 * j * kBK);
-      const u32x4 hi = *reinterpret_cast<const u32x4*>(sb + fb1 + 32 * j * kBK);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        fb[j][e] = (int)lo[e];
-        fb[j][4 + e] = (int)hi[e];
-      }
-    }
-  };
+  const uint32_t cbase = lds0 + (uint32_t)(64 * wv * kBK);  // this wave's rows in stage 0
+  // Per-lane copy offsets and fragment addresses.  They are derived again at
+  // every tile from a freshly computed lane index, so that they are not live
+  // (and spilled) across the epilogue, where the accumulators need the
+  // registers.
+  uint32_t woff[4], xoff[4], fa0, fa1, fb0, fb1;
+#define LIN_LANE_SETUP()                                                                      \
+  do {                                                                                        \
+    const int ln_ = fresh_lane_id();                                                          \
+    /* copies: wave w moves rows 64w .. 64w+63 of both halves, 16 rows per instruction;       \
+       lane l lands in slot l%4 of row l/4 (the swizzle is an involution) */                  \
+    _Pragma("unroll") for (int i_ = 0; i_ < 4; ++i_) {                                        \
+      const int row_ = 64 * wv + 16 * i_ + (ln_ >> 2);                                        \
+      const int c_ = swz64(row_, ln_ & 3);                                                    \
+      woff[i_] = (uint32_t)(row_ * a.ldw + 16 * c_);                                          \
+      xoff[i_] = (uint32_t)(row_ * a.ldx + 16 * c_);                                          \
+    }                                                                                         \
+    /* fragments: A (weights) row 128 wn + 32 i + l32, B (activations) row 128 wm + 32 j +    \
+       l32; bytes 32 g .. 32 g + 31 = logical chunks 2g, 2g + 1; the swizzle term             \
+       (row >> 2) & 3 depends on l32 only */                                                  \
+    const int g_ = ln_ >> 5, l_ = ln_ & 31, s1_ = (l_ >> 2) & 3;                              \
+    fa0 = (uint32_t)((128 * wn + l_) * kBK + 16 * ((2 * g_) ^ s1_));                          \
+    fa1 = (uint32_t)((128 * wn + l_) * kBK + 16 * ((2 * g_ + 1) ^ s1_));                      \
+    fb0 = (uint32_t)(kHalfBytes + (128 * wm + l_) * kBK + 16 * ((2 * g_) ^ s1_));             \
+    fb1 = (uint32_t)(kHalfBytes + (128 * wm + l_) * kBK + 16 * ((2 * g_ + 1) ^ s1_));         \
+  } while (0)
+  LIN_LANE_SETUP();
+
+
+  // current and next tile: origins and the byte ranges of their rows
+  int tile = t_first, m0, n0, nm0, nn0;
+  tile_origin(a, tile, m0, n0);
+  bool has_next = ntiles > 1;
+  nm0 = m0;
+  nn0 = n0;
+  if (has_next) tile_origin(a, tile + wgs_x, nm0, nn0);
+  auto wbytes = [&](int n) { return (uint32_t)(min(kBN, a.N - n) * a.ldw); };
+  auto xbytes = [&](int m) { return (uint32_t)(min(kBM, a.M - m) * a.ldx); };
+
+  // Copy number q of the current tile (q >= S: stage q - S of the next one,
+  // which needs S >= 4; past the end a repeat of the last stage, into a
+  // buffer that is never read again): every stage issues the same 8 copies
+  // per wave, so every wait is one constant.
+#define LIN_COPY(q, buf)                                                                      \
+  do {                                                                                        \
+    const bool cur_ = (q) < S;                                                                \
+    const bool use_c_ = cur_ || !has_next;                                                    \
+    const int st_ = cur_ ? (q) : (has_next ? (q) - S : S - 1);                               \
+    const int mo_ = use_c_ ? m0 : nm0, no_ = use_c_ ? n0 : nn0;                               \
+    copy_stage(cbase + (uint32_t)((buf) * kStageBytes),                                       \
+               make_rsrc(a.w + (int64_t)no_ * a.ldw, wbytes(no_)),                            \
+               make_rsrc(a.x + (int64_t)mo_ * a.ldx, xbytes(mo_)), woff, xoff,                \
+               (uint32_t)(st_ * kBK));                                                        \
+  } while (0)
+
+  // scale vectors of the current tile into LDS: wave 0 sx, wave 1 sw, wave 2
+  // bias (zeros without bias: an empty range reads zero), wave 3 a spare copy
+  // of sx; 1 KB each
+#define LIN_COPY_SCALES()                                                                     \
+  do {                                                                                        \
+    const int which_ = wv == 3 ? 0 : wv;                                                      \
+    const float* src_ = which_ == 0 ? a.sx + m0 : (which_ == 1 ? a.sw + n0 : a.bias + n0);   \
+    const int valid_ = which_ == 0 ? min(kBM, a.M - m0)                                       \
+                                   : (which_ == 2 && !a.bias ? 0 : min(kBN, a.N - n0));       \
+    dma16(lds0 + (uint32_t)kScaleOff + 1024u * wv,                                            \
+          make_rsrc(which_ == 2 && !a.bias ? a.sw : src_, (uint32_t)valid_ * 4u),             \
+          16u * (uint32_t)fresh_lane_id(),                                                    \
+          0u);                                                                                \
+  } while (0)
 
   f32x16 acc[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-  auto mfma_half = [&](const i32x8 (&fa)[4], const i32x8 (&fb)[4], int half) {
-#pragma unroll
-    for (int jj = 0; jj < 2; ++jj)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int j = 2 * half + jj;
-        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa[i], fb[j], acc[i][j], 0, 0,
-                                                                    0, kOneE8m0, 0, kOneE8m0);
-      }
-  };
-
-  // Every stage issues the same 8 copies per wave, so each wait is one
-  // constant vmcnt and the loop body is a single basic block: the copies
-  // of stages past the end (index clamped to the last stage) land in
-  // buffers that are never read again.
-  const int S = a.K / kBK;
-#pragma unroll
-  for (int st = 0; st < kStages; ++st) copy_stage(min(st, S - 1), st);
-  wait_vm24();  // stage 0 landed (this wave's part); stages 1..3 in flight
-  barrier_keep_loads();
-
   i32x8 fa_c[4], fb_c[4], fa_n[4], fb_n[4];
-  read_frags(0, fa_c, fb_c);
 
-  // stage s (with a successor): first half of the MFMAs; the wait for stage
-  // s+1 and the barrier that releases stage s's buffer; its refill with
-  // stage s+4; the fragments of stage s+1; second half
-  for (int s = 0; s + 1 < S; ++s) {
-    mfma_half(fa_c, fb_c, 0);
-    wait_vm16();  // stage s+1 landed; s+2 and s+3 may still be in flight
-    wait_lgkm0();
-    barrier_keep_loads();  // every wave has stage s+1 and is done reading stage s
-    copy_stage(min(s + kStages, S - 1), s & (kStages - 1));
-    read_frags((s + 1) & (kStages - 1), fa_n, fb_n);
-    mfma_half(fa_c, fb_c, 1);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      fa_c[i] = fa_n[i];
-      fb_c[i] = fb_n[i];
-    }
-  }
-  mfma_half(fa_c, fb_c, 0);
-  mfma_half(fa_c, fb_c, 1);
-  wait_vm0();  // the clamped copies of the last stages
-
-  // Epilogue through LDS, so that the stores are whole 256-byte row segments.
-  // acc[i][j][4q + u] is output channel 128 wn + 32 i + 8 q + 4 g + u of
-  // token 128 wm + 32 j + l32 (tile-local).  Each wave stages its 128 x 128
-  // bf16 block in its own 32 KB of LDS (rows of 256 bytes, 16-byte chunk c of
-  // row r at slot c ^ (r & 15)), then stores 4 rows x 256 bytes per
-  // instruction.  The stage buffers are reused: every wave must be done with
-  // its last fragment reads and every copy must have landed first.
-  wait_lgkm0();
+  // prologue: stages 0..3 of the sequence
+  LIN_COPY(0, 0);
+  LIN_COPY(1, 1);
+  LIN_COPY(2, 2);
+  LIN_COPY(3, 3);
+  LIN_COPY_SCALES();
+  wait_vm24();  // stage 0 landed (this wave's part); the rest may be in flight
   barrier_keep_loads();
-  uint8_t* stg = lds + wave * (kBM / 2) * 256;
-  float sxv[4];
+  read_frags(lds, fa0, fa1, fb0, fb1, fa_c, fb_c);
+  int j = 0;  // global stage number: stage s of the k-th tile is k S + s, in buffer j % 4
+
+  // one stage: first half of the MFMAs; the wait for the next stage and the
+  // barrier that releases this one's buffer; its refill with the stage 4
+  // ahead; the next fragments; second half
+#define LIN_STAGE(s, FIRST)                                                                   \
+  do {                                                                                        \
+    mfma_half<FIRST>(acc, fa_c, fb_c, 0);                                                     \
+    wait_vm16();                                                                              \
+    wait_lgkm0();                                                                             \
+    barrier_keep_loads();                                                                     \
+    LIN_COPY((s) + kStages, j & (kStages - 1));                                               \
+    read_frags(lds + ((j + 1) & (kStages - 1)) * kStageBytes, fa0, fa1, fb0, fb1, fa_n, fb_n); \
+    mfma_half<FIRST>(acc, fa_c, fb_c, 1);                                                     \
+    _Pragma("unroll") for (int i_ = 0; i_ < 4; ++i_) {                                        \
+      fa_c[i_] = fa_n[i_];                                                                    \
+      fb_c[i_] = fb_n[i_];                                                                    \
+    }                                                                                         \
+    ++j;                                                                                      \
+  } while (0)
+
+  for (int k = 0; k < ntiles; ++k) {
+    LIN_LANE_SETUP();
+    LIN_STAGE(0, true);
+    for (int s = 1; s < S; ++s) LIN_STAGE(s, false);
+
+    // (The scale vectors of this tile were copied at its first stage; with
+    // S >= 4 stages the in-loop waits and barriers have covered them.)
+    // Epilogue through LDS in 8 passes of 32 tokens x 64 output channels per
+    // wave, each stored as 128-byte row segments.  acc[i][jj][4q + u] is
+    // output channel 128 wn + 32 i + 8 q + 4 g + u of token 128 wm + 32 jj +
+    // l32 (tile-local).  Staging row r holds 64 channels (8 chunks of 16
+    // bytes, chunk c at slot c ^ (r & 7)).
+    // (a freshly computed lane index, so that the compiler derives the
+    // epilogue addresses here instead of keeping them live across the main
+    // loop)
+    const int le = fresh_lane_id();
+    const int ge = le >> 5, l32e = le & 31;
+    uint8_t* stg = lds + kOutOff + wv * 4096;
+    const float* sxl = reinterpret_cast<const float*>(lds + kScaleOff);
+    const float* swl = sxl + 256;
+    const float* bl = sxl + 512;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int m = m0 + 128 * wm + 32 * j + l32;
-    sxv[j] = m < a.M ? a.sx[m] : 0.f;
-  }
+    for (int jj = 0; jj < 4; ++jj) {
+      const float sxv = sxl[128 * wm + 32 * jj + l32e];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+      for (int ih = 0; ih < 2; ++ih) {
+        __builtin_amdgcn_sched_barrier(0);  // one pass at a time: bounded registers
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int n = n0 + 128 * wn + 32 * i + 8 * q + 4 * g;
-      f32x4 swv = {0.f, 0.f, 0.f, 0.f}, bv = {0.f, 0.f, 0.f, 0.f};
-      if (n < a.N) {
-        swv = *reinterpret_cast<const f32x4*>(a.sw + n);
-        if (a.bias) bv = *reinterpret_cast<const f32x4*>(a.bias + n);
-      }
+        for (int i2 = 0; i2 < 2; ++i2) {
+          const int i = 2 * ih + i2;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r = 32 * j + l32;
-        float v[4];
+          for (int q = 0; q < 4; ++q) {
+            const int nl = 128 * wn + 32 * i + 8 * q + 4 * ge;
+            const f32x4 swv = *reinterpret_cast<const f32x4*>(swl + nl);
+            const f32x4 bv = *reinterpret_cast<const f32x4*>(bl + nl);
+            float v[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) v[u] = fmaf(acc[i][j][4 * q + u] * sxv[j], swv[u], bv[u]);
-        u32x2 o;
-        o[0] = pack_bf16x2(v[0], v[1]);
-        o[1] = pack_bf16x2(v[2], v[3]);
-        *reinterpret_cast<u32x2*>(stg + r * 256 + (((4 * i + q) ^ (r & 15)) << 4) + 8 * g) = o;
+            for (int u = 0; u < 4; ++u) v[u] = fmaf(acc[i][jj][4 * q + u] * sxv, swv[u], bv[u]);
+            u32x2 o;
+            o[0] = pack_bf16x2(v[0], v[1]);
+            o[1] = pack_bf16x2(v[2], v[3]);
+            const int c = 4 * i2 + q;  // chunk of 8 channels within the 64
+            *reinterpret_cast<u32x2*>(stg + l32e * 128 + ((c ^ (l32e & 7)) << 4) + 8 * ge) = o;
+          }
+        }
+        wait_lgkm0();  // the wave reads back only what it wrote itself
+        const int c = le & 7;
+        const int n = n0 + 128 * wn + 64 * ih + 8 * c;
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          const int r = 8 * p + (le >> 3);
+          const u32x4 v = *reinterpret_cast<const u32x4*>(stg + r * 128 + ((c ^ (r & 7)) << 4));
+          const int m = m0 + 128 * wm + 32 * jj + r;
+          if (m < a.M && n < a.N) st16(a.y + (int64_t)m * a.ldy + n, v);
+        }
+        wait_lgkm0();  // reads done before the next pass overwrites the staging rows
       }
     }
+
+    // advance: the next tile becomes current; the copies of its first stages
+    // are already in flight
+    tile += wgs_x;
+    m0 = nm0;
+    n0 = nn0;
+    has_next = k + 2 < ntiles;
+    if (has_next) tile_origin(a, tile + wgs_x, nm0, nn0);
+    if (k + 1 < ntiles) {
+      // the scale vectors of the next tile: every wave has read this tile's
+      // (its epilogue waited for its LDS reads); the barrier covers them all
+      barrier_keep_loads();
+      LIN_COPY_SCALES();
+    }
   }
-  wait_lgkm0();  // the wave reads back only what it wrote itself
-  const int c = lane & 15;
-  const int n = n0 + 128 * wn + 8 * c;
-#pragma unroll 4
-  for (int p = 0; p < 32; ++p) {
-    const int r = 4 * p + (lane >> 4);
-    const u32x4 v = *reinterpret_cast<const u32x4*>(stg + r * 256 + ((c ^ (r & 15)) << 4));
-    const int m = m0 + 128 * wm + r;
-    if (m < a.M && n < a.N) st16(a.y + (int64_t)m * a.ldy + n, v);
-  }
+#undef LIN_STAGE
+#undef LIN_LANE_SETUP
+#undef LIN_COPY_SCALES
+#undef LIN_COPY
+  wait_vm0();  // the repeated copies past the end
 }
 
 }  // namespace
@@ -389,8 +496,14 @@ hipError_t launch_linear_w8a8(const LinearIn& in, hipStream_t stream) {
   a.tiles_m = (int)((in.M + kBM - 1) / kBM);
   a.tiles_n = (int)((in.N + kBN - 1) / kBN);
   a.group_m = in.group_m > 0 ? in.group_m : 4;
-  const int T = a.tiles_m * a.tiles_n;
-  linear_w8a8_kernel<<<dim3((unsigned)T), 256, 0, stream>>>(a);
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  const int64_t T = (int64_t)a.tiles_m * a.tiles_n;
+  const int grid = (int)(T < cus ? T : cus);  // one persistent workgroup per CU
+  linear_w8a8_kernel<<<dim3((unsigned)grid), 256, 0, stream>>>(a);
   return hipGetLastError();
 }
 

@@ -196,7 +196,7 @@ def test_w8a8_linear_entry_points_reject_bad_arguments():
     assert q(P, -1, 64, 64, P, P, None) == -1            # rows < 0
     assert q(P, 0, 64, 64, P, P, None) == 0              # empty: nothing launched
     lin = lib.sparse_attn_linear_w8a8
-    ok = (P, P, 128, P, P, 128, None, P, 256, 300, 256, 128, None)
+    ok = (P, P, 256, P, P, 256, None, P, 256, 300, 256, 256, None)
 
     def call(**kw):
         names = ("xq", "sx", "ldx", "wq", "sw", "ldw", "bias", "y", "ldy", "M", "N", "K", "s")
@@ -208,10 +208,11 @@ def test_w8a8_linear_entry_points_reject_bad_arguments():
     assert call(N=0, ldy=0) == 0
     assert call(xq=None) == -1
     assert call(sw=None) == -1
-    assert call(K=96, ldx=128, ldw=128) == -1            # K % 64
+    assert call(K=288, ldx=384, ldw=384) == -1           # K % 64
+    assert call(K=192, ldx=192, ldw=192) == -1           # K < 256
     assert call(K=0) == -1
     assert call(N=260, ldy=264) == -1                    # N % 8
-    assert call(ldx=120) == -1                           # ldx < K
+    assert call(ldx=240) == -1                           # ldx < K
     assert call(ldw=136) == -1                           # ldw % 16
     assert call(ldy=255) == -1                           # ldy < N
     assert call(ldy=260) == -1                           # ldy % 8
@@ -219,4 +220,4 @@ def test_w8a8_linear_entry_points_reject_bad_arguments():
     assert call(wq=MIS) == -1                            # misaligned codes
     assert call(bias=MIS) == -1                          # misaligned bias
     assert call(M=-5) == -1
-    assert call(ldx=1 << 24, K=64) == -2                 # 256 * ldx does not fit 32 bits
+    assert call(ldx=1 << 24) == -2                       # 256 * ldx does not fit 32 bits
