@@ -252,7 +252,7 @@ int sparse_attn_quant_rows_fp8(const void* x, int64_t rows, int64_t cols, int64_
  *  wq, sw   weight codes [N][K] (row stride ldw bytes) and scales [N]
  *  bias     fp32 [N] or NULL
  *  y        bf16 [M][N], row stride ldy elements (written)
- * Layout rules: K % 64 == 0 and K >= 256; N % 8 == 0; M, N >= 0 (either 0
+ * Layout rules: K % 128 == 0 and K >= 256; N % 8 == 0; M, N >= 0 (either 0
  * launches nothing); ldx, ldw >= K and multiples of 16; ldy >= N and a multiple
  * of 8; xq, wq, sw, bias and y 16-byte aligned; M, N < 2^31 and 256 * ldx,
  * 256 * ldw < 2^32.

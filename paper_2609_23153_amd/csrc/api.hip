@@ -234,7 +234,7 @@ int sparse_attn_linear_w8a8(const uint8_t* xq, const float* sx, int64_t ldx, con
                             const float* sw, int64_t ldw, const float* bias, void* y, int64_t ldy,
                             int64_t M, int64_t N, int64_t K, void* stream) {
   if (!xq || !sx || !wq || !sw || !y) return SA_ERR_INVALID_ARG;
-  if (M < 0 || N < 0 || K < 256 || (K & 63) != 0 || (N & 7) != 0) return SA_ERR_INVALID_ARG;
+  if (M < 0 || N < 0 || K < 256 || (K & 127) != 0 || (N & 7) != 0) return SA_ERR_INVALID_ARG;
   if (ldx < K || (ldx & 15) != 0 || ldw < K || (ldw & 15) != 0 || ldy < N || (ldy & 7) != 0)
     return SA_ERR_INVALID_ARG;
   if (!aligned16(xq) || !aligned16(wq) || !aligned16(sw) || (bias && !aligned16(bias)) ||

@@ -10,19 +10,20 @@
 // codes = e4m3(x * (448 / a)), each quotient and product a correctly rounded
 // fp32 operation, the code rounded to nearest with ties to even.
 //
-// Product: one workgroup (4 waves) per 256 x 256 output tile, computed
-// transposed (D^T = W X^T), so that each lane ends with four consecutive
-// output channels of one token; the tile leaves through LDS as whole
-// 256-byte row segments.  Each wave owns a 128 x 128
-// quarter: 4 x 4 accumulators of v_mfma_scale_f32_32x32x64_f8f6f4 (unit
-// scales).  K advances 64 bytes per stage; a stage is the 256 weight rows and
-// 256 activation rows of that K slice (32 KB), moved global -> LDS with
-// buffer_load ... lds (issued from inline asm, rows past M or N read zero),
-// four stages in flight (128 KB).  Each stage is read once per wave as
-// fragments; the barrier that releases a stage's buffer sits between the two
-// halves of the previous stage's MFMAs, so the next fragments load while the
-// matrix cores still work.  Tiles are ordered in groups of `group_m` tile
-// rows and dealt to the 8 XCDs in contiguous runs, so the workgroups that run
+// Product: persistent workgroups (4 waves, one per CU) walk 256 x 256 output
+// tiles, each computed transposed (D^T = W X^T), so that each lane ends with
+// four consecutive output channels of one token; the tile leaves through LDS
+// as whole row segments.  Each wave owns a 128 x 128 quarter: 4 x 4
+// accumulators of v_mfma_scale_f32_32x32x64_f8f6f4 (unit scales).  K
+// advances 128 bytes per stage, so that every row segment a stage copies is
+// one whole 128-byte line (64-byte segments halve the L2 -> LDS rate); a
+// stage (the tile's 256 weight rows and 256 activation rows, 64 KB) moves
+// global -> LDS with buffer_load ... lds, issued from inline asm, rows past
+// M or N reading zero.  Two stage buffers: the copy of stage s+2 is issued
+// at the barrier that releases stage s, between stage s's two MFMA steps,
+// so it has a whole stage of MFMAs to land; the copy pipeline runs on across
+// tile boundaries.  Tiles are ordered in groups of `group_m` tile rows and
+// dealt to the 8 XCDs in contiguous runs, so the workgroups that run
 // together on one XCD share their activation and weight rows in its L2.
 #include "common.h"
 #include "launch.h"
@@ -125,33 +126,25 @@ __global__ __launch_bounds__(256) void quant_rows_stream_kernel(const uint16_t* 
 
 constexpr int kBM = 256;                       // tokens per tile
 constexpr int kBN = 256;                       // output channels per tile
-constexpr int kBK = 64;                        // bytes of K per stage
-constexpr int kStages = 4;
-constexpr int kHalfBytes = kBN * kBK;          // 16 KB: the weight (or activation) rows of a stage
+constexpr int kBK = 128;                       // bytes of K per stage: whole 128-byte lines
+constexpr int kStages = 2;
+constexpr int kHalfBytes = kBN * kBK;          // 32 KB: the weight (or activation) rows of a stage
 constexpr int kStageBytes = 2 * kHalfBytes;    // [weights | activations]
 constexpr int kOneE8m0 = 127;                  // E8M0 code of 1
 
-// Physical 16-byte slot of logical chunk c (0..3) of a 64-byte row: the
+// Physical 16-byte slot of logical chunk c (0..7) of a 128-byte row: the
 // sixteen lanes that one LDS cycle serves read sixteen consecutive rows at
-// the same logical chunk; row 4a + b then lands in 16-byte bank group
-// 4b + (c ^ a) of the 256-byte bank window, all sixteen distinct.
-__device__ __forceinline__ int swz64(int row, int c) { return c ^ ((row >> 2) & 3); }
+// the same logical chunk; row 2a + b then lands in 16-byte bank group
+// 8b + (c ^ a) of the 256-byte bank window, all sixteen distinct.
+__device__ __forceinline__ int swz128(int row, int c) { return c ^ ((row >> 1) & 7); }
 
 __device__ __forceinline__ void wait_vm0() {
   __builtin_amdgcn_sched_barrier(0);
   __builtin_amdgcn_s_waitcnt(0x0F70);
 }
-__device__ __forceinline__ void wait_vm8() {
-  __builtin_amdgcn_sched_barrier(0);
-  __builtin_amdgcn_s_waitcnt(0x0F78);
-}
 __device__ __forceinline__ void wait_vm16() {
   __builtin_amdgcn_sched_barrier(0);
   __builtin_amdgcn_s_waitcnt(0x4F70);
-}
-__device__ __forceinline__ void wait_vm24() {
-  __builtin_amdgcn_sched_barrier(0);
-  __builtin_amdgcn_s_waitcnt(0x4F78);
 }
 __device__ __forceinline__ void wait_lgkm0() {
   __builtin_amdgcn_sched_barrier(0);
@@ -196,15 +189,17 @@ __device__ __forceinline__ void tile_origin(const LinArgs& a, int t, int& m0, in
 // Global -> LDS copy of one stage (K slice `k0` of the tile's 256 weight rows
 // and 256 activation rows) into the stage buffer at LDS byte address `base`.
 __device__ __forceinline__ void copy_stage(uint32_t base, __amdgpu_buffer_rsrc_t wr,
-                                           __amdgpu_buffer_rsrc_t xr, const uint32_t (&woff)[4],
-                                           const uint32_t (&xoff)[4], uint32_t k0) {
+                                           __amdgpu_buffer_rsrc_t xr, const uint32_t (&woff)[8],
+                                           const uint32_t (&xoff)[8], uint32_t k0) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) dma16(base + 16 * i * kBK, wr, woff[i], k0);
+  for (int i = 0; i < 8; ++i) dma16(base + 8 * i * kBK, wr, woff[i], k0);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) dma16(base + kHalfBytes + 16 * i * kBK, xr, xoff[i], k0);
+  for (int i = 0; i < 8; ++i) dma16(base + kHalfBytes + 8 * i * kBK, xr, xoff[i], k0);
 }
 
-// A (weights) and B (activations) fragments of one stage buffer `sb`.
+// A (weights) and B (activations) fragments of one 64-byte K step of the
+// stage buffer `sb`: fa*/fb* are the byte offsets of the lane's two 16-byte
+// chunks in the first A / B row of the step (swizzle applied).
 __device__ __forceinline__ void read_frags(const uint8_t* sb, uint32_t fa0, uint32_t fa1,
                                            uint32_t fb0, uint32_t fb1, i32x8 (&fa)[4],
                                            i32x8 (&fb)[4]) {
@@ -230,20 +225,65 @@ __device__ __forceinline__ void read_frags(const uint8_t* sb, uint32_t fa0, uint
   }
 }
 
-// Half the MFMAs of a stage: accumulator columns 2 half, 2 half + 1.  FIRST
-// starts the accumulators from zero (the first stage of a tile).
-template <bool FIRST>
-__device__ __forceinline__ void mfma_half(f32x16 (&acc)[4][4], const i32x8 (&fa)[4],
-                                          const i32x8 (&fb)[4], int half) {
+// Part t (0..15) of the fragment reads of one K step: A fragments 0..3 then
+// B fragments 0..3, two 16-byte halves each.
+template <int T>
+__device__ __forceinline__ void read_frag_part(const uint8_t* sb, const uint32_t (&fk)[4],
+                                               i32x8 (&fa)[4], i32x8 (&fb)[4]) {
+  constexpr int f = T >> 1, h = T & 1;
+  if constexpr (f < 4) {
+    const u32x4 v = *reinterpret_cast<const u32x4*>(sb + fk[h] + 32 * f * kBK);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) fa[f][4 * h + e] = (int)v[e];
+  } else {
+    const u32x4 v = *reinterpret_cast<const u32x4*>(sb + fk[2 + h] + 32 * (f - 4) * kBK);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) fb[f - 4][4 * h + e] = (int)v[e];
+  }
+}
+
+// MFMA t (0..15) of one K step: accumulator (i, j) = (t % 4, t / 4).
+template <int T, bool FIRST>
+__device__ __forceinline__ void mfma_one(f32x16 (&acc)[4][4], const i32x8 (&fa)[4],
+                                         const i32x8 (&fb)[4]) {
+  constexpr int i = T & 3, j = T >> 2;
   const f32x16 zero = {};
-#pragma unroll
-  for (int jj = 0; jj < 2; ++jj)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int j = 2 * half + jj;
-      acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-          fa[i], fb[j], FIRST ? zero : acc[i][j], 0, 0, 0, kOneE8m0, 0, kOneE8m0);
-    }
+  acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+      fa[i], fb[j], FIRST ? zero : acc[i][j], 0, 0, 0, kOneE8m0, 0, kOneE8m0);
+}
+
+// The two interleaved phases of a stage, each one MFMA step with the reads
+// and copies it hides: MFMA t, then fragment part t (and copy t).
+template <int T, bool FIRST>
+__device__ __forceinline__ void phase0(f32x16 (&acc)[4][4], const i32x8 (&fa0)[4],
+                                       const i32x8 (&fb0)[4], const uint8_t* sb,
+                                       const uint32_t (&fk1)[4], i32x8 (&fa1)[4],
+                                       i32x8 (&fb1)[4]) {
+  if constexpr (T < 16) {
+    mfma_one<T, FIRST>(acc, fa0, fb0);
+    read_frag_part<T>(sb, fk1, fa1, fb1);
+    __builtin_amdgcn_sched_barrier(0);
+    phase0<T + 1, FIRST>(acc, fa0, fb0, sb, fk1, fa1, fb1);
+  }
+}
+template <int T>
+__device__ __forceinline__ void phase1(f32x16 (&acc)[4][4], const i32x8 (&fa1)[4],
+                                       const i32x8 (&fb1)[4], const uint8_t* nb,
+                                       const uint32_t (&fk0)[4], i32x8 (&fa0)[4],
+                                       i32x8 (&fb0)[4], uint32_t cbuf,
+                                       __amdgpu_buffer_rsrc_t wr, __amdgpu_buffer_rsrc_t xr,
+                                       const uint32_t (&woff)[8], const uint32_t (&xoff)[8],
+                                       uint32_t k0) {
+  if constexpr (T < 16) {
+    if constexpr (T < 8)
+      dma16(cbuf + 8 * T * kBK, wr, woff[T], k0);
+    else
+      dma16(cbuf + kHalfBytes + 8 * (T - 8) * kBK, xr, xoff[T - 8], k0);
+    mfma_one<T, false>(acc, fa1, fb1);
+    read_frag_part<T>(nb, fk0, fa0, fb0);
+    __builtin_amdgcn_sched_barrier(0);
+    phase1<T + 1>(acc, fa1, fb1, nb, fk0, fa0, fb0, cbuf, wr, xr, woff, xoff, k0);
+  }
 }
 
 // Persistent: one workgroup per CU walks its share of the output tiles, and
@@ -279,26 +319,29 @@ __global__ __launch_bounds__(256) void linear_w8a8_kernel(LinArgs a) {
   // every tile from a freshly computed lane index, so that they are not live
   // (and spilled) across the epilogue, where the accumulators need the
   // registers.
-  uint32_t woff[4], xoff[4], fa0, fa1, fb0, fb1;
+  uint32_t woff[8], xoff[8], fk[2][4];  // fk[ks] = {fa0, fa1, fb0, fb1} of K step ks
 #define LIN_LANE_SETUP()                                                                      \
   do {                                                                                        \
     const int ln_ = fresh_lane_id();                                                          \
-    /* copies: wave w moves rows 64w .. 64w+63 of both halves, 16 rows per instruction;       \
-       lane l lands in slot l%4 of row l/4 (the swizzle is an involution) */                  \
-    _Pragma("unroll") for (int i_ = 0; i_ < 4; ++i_) {                                        \
-      const int row_ = 64 * wv + 16 * i_ + (ln_ >> 2);                                        \
-      const int c_ = swz64(row_, ln_ & 3);                                                    \
+    /* copies: wave w moves rows 64w .. 64w+63 of both halves, 8 rows per instruction;        \
+       lane l lands in slot l%8 of row l/8 (the swizzle is an involution) */                  \
+    _Pragma("unroll") for (int i_ = 0; i_ < 8; ++i_) {                                        \
+      const int row_ = 64 * wv + 8 * i_ + (ln_ >> 3);                                         \
+      const int c_ = swz128(row_, ln_ & 7);                                                   \
       woff[i_] = (uint32_t)(row_ * a.ldw + 16 * c_);                                          \
       xoff[i_] = (uint32_t)(row_ * a.ldx + 16 * c_);                                          \
     }                                                                                         \
     /* fragments: A (weights) row 128 wn + 32 i + l32, B (activations) row 128 wm + 32 j +    \
-       l32; bytes 32 g .. 32 g + 31 = logical chunks 2g, 2g + 1; the swizzle term             \
-       (row >> 2) & 3 depends on l32 only */                                                  \
-    const int g_ = ln_ >> 5, l_ = ln_ & 31, s1_ = (l_ >> 2) & 3;                              \
-    fa0 = (uint32_t)((128 * wn + l_) * kBK + 16 * ((2 * g_) ^ s1_));                          \
-    fa1 = (uint32_t)((128 * wn + l_) * kBK + 16 * ((2 * g_ + 1) ^ s1_));                      \
-    fb0 = (uint32_t)(kHalfBytes + (128 * wm + l_) * kBK + 16 * ((2 * g_) ^ s1_));             \
-    fb1 = (uint32_t)(kHalfBytes + (128 * wm + l_) * kBK + 16 * ((2 * g_ + 1) ^ s1_));         \
+       l32; K step ks, bytes 64 ks + 32 g .. + 31 = logical chunks 4 ks + 2 g, + 1; the       \
+       swizzle term (row >> 1) & 7 depends on l32 only */                                     \
+    const int g_ = ln_ >> 5, l_ = ln_ & 31, s1_ = (l_ >> 1) & 7;                              \
+    _Pragma("unroll") for (int ks_ = 0; ks_ < 2; ++ks_) {                                     \
+      const int c0_ = 4 * ks_ + 2 * g_;                                                       \
+      fk[ks_][0] = (uint32_t)((128 * wn + l_) * kBK + 16 * (c0_ ^ s1_));                      \
+      fk[ks_][1] = (uint32_t)((128 * wn + l_) * kBK + 16 * ((c0_ + 1) ^ s1_));                \
+      fk[ks_][2] = (uint32_t)(kHalfBytes + (128 * wm + l_) * kBK + 16 * (c0_ ^ s1_));         \
+      fk[ks_][3] = (uint32_t)(kHalfBytes + (128 * wm + l_) * kBK + 16 * ((c0_ + 1) ^ s1_));   \
+    }                                                                                         \
   } while (0)
   LIN_LANE_SETUP();
 
@@ -314,9 +357,9 @@ __global__ __launch_bounds__(256) void linear_w8a8_kernel(LinArgs a) {
   auto xbytes = [&](int m) { return (uint32_t)(min(kBM, a.M - m) * a.ldx); };
 
   // Copy number q of the current tile (q >= S: stage q - S of the next one,
-  // which needs S >= 4; past the end a repeat of the last stage, into a
-  // buffer that is never read again): every stage issues the same 8 copies
-  // per wave, so every wait is one constant.
+  // which needs S >= 2; past the end a repeat of the last stage, into a
+  // buffer that is never read again): every stage issues the same 16 copies
+  // per wave.
 #define LIN_COPY(q, buf)                                                                      \
   do {                                                                                        \
     const bool cur_ = (q) < S;                                                                \
@@ -345,35 +388,42 @@ __global__ __launch_bounds__(256) void linear_w8a8_kernel(LinArgs a) {
   } while (0)
 
   f32x16 acc[4][4];
-  i32x8 fa_c[4], fb_c[4], fa_n[4], fb_n[4];
+  i32x8 fa0[4], fb0[4], fa1[4], fb1[4];  // fragments of K steps 0 and 1 of a stage
 
-  // prologue: stages 0..3 of the sequence
+  // prologue: stages 0 and 1 of the sequence, the first tile's scales
   LIN_COPY(0, 0);
   LIN_COPY(1, 1);
-  LIN_COPY(2, 2);
-  LIN_COPY(3, 3);
   LIN_COPY_SCALES();
-  wait_vm24();  // stage 0 landed (this wave's part); the rest may be in flight
+  wait_vm16();  // stage 0 landed (this wave's part); stage 1 and the scales may be in flight
   barrier_keep_loads();
-  read_frags(lds, fa0, fa1, fb0, fb1, fa_c, fb_c);
-  int j = 0;  // global stage number: stage s of the k-th tile is k S + s, in buffer j % 4
+  read_frags(lds, fk[0][0], fk[0][1], fk[0][2], fk[0][3], fa0, fb0);
+  int j = 0;  // global stage number: stage s of the k-th tile is k S + s, in buffer j % 2
 
-  // one stage: first half of the MFMAs; the wait for the next stage and the
-  // barrier that releases this one's buffer; its refill with the stage 4
-  // ahead; the next fragments; second half
+  // One stage (K = 128 bytes, two MFMA steps), starting with the fragments
+  // of its first step in registers.  Phase 0: the first step's 16 MFMAs,
+  // each followed by one part of the second step's fragment reads.  Then the
+  // wait for the next stage and the barrier that releases this one's buffer.
+  // Phase 1: the second step's MFMAs, each preceded by one of the 16 copies
+  // of the stage two ahead (into the released buffer) and followed by one
+  // part of the next stage's first-step fragments.  Spreading the copies
+  // keeps the texture addresser's queue short, so the wave never blocks on a
+  // copy while the matrix cores idle.
 #define LIN_STAGE(s, FIRST)                                                                   \
   do {                                                                                        \
-    mfma_half<FIRST>(acc, fa_c, fb_c, 0);                                                     \
-    wait_vm16();                                                                              \
+    phase0<0, FIRST>(acc, fa0, fb0, lds + (j & 1) * kStageBytes, fk[1], fa1, fb1);            \
+    wait_vm0();                                                                               \
     wait_lgkm0();                                                                             \
     barrier_keep_loads();                                                                     \
-    LIN_COPY((s) + kStages, j & (kStages - 1));                                               \
-    read_frags(lds + ((j + 1) & (kStages - 1)) * kStageBytes, fa0, fa1, fb0, fb1, fa_n, fb_n); \
-    mfma_half<FIRST>(acc, fa_c, fb_c, 1);                                                     \
-    _Pragma("unroll") for (int i_ = 0; i_ < 4; ++i_) {                                        \
-      fa_c[i_] = fa_n[i_];                                                                    \
-      fb_c[i_] = fb_n[i_];                                                                    \
-    }                                                                                         \
+    const int q_ = (s) + kStages;                                                             \
+    const bool cur_ = q_ < S;                                                                 \
+    const bool use_c_ = cur_ || !has_next;                                                    \
+    const int st_ = cur_ ? q_ : (has_next ? q_ - S : S - 1);                                  \
+    const int mo_ = use_c_ ? m0 : nm0, no_ = use_c_ ? n0 : nn0;                               \
+    phase1<0>(acc, fa1, fb1, lds + ((j + 1) & 1) * kStageBytes, fk[0], fa0, fb0,              \
+              cbase + (uint32_t)((j & 1) * kStageBytes),                                      \
+              make_rsrc(a.w + (int64_t)no_ * a.ldw, wbytes(no_)),                             \
+              make_rsrc(a.x + (int64_t)mo_ * a.ldx, xbytes(mo_)), woff, xoff,                 \
+              (uint32_t)(st_ * kBK));                                                         \
     ++j;                                                                                      \
   } while (0)
 
@@ -382,8 +432,8 @@ __global__ __launch_bounds__(256) void linear_w8a8_kernel(LinArgs a) {
     LIN_STAGE(0, true);
     for (int s = 1; s < S; ++s) LIN_STAGE(s, false);
 
-    // (The scale vectors of this tile were copied at its first stage; with
-    // S >= 4 stages the in-loop waits and barriers have covered them.)
+    // (The scale vectors of this tile were copied before its first stage,
+    // whose wait and barrier have covered them.)
     // Epilogue through LDS in 8 passes of 32 tokens x 64 output channels per
     // wave, each stored as 128-byte row segments.  acc[i][jj][4q + u] is
     // output channel 128 wn + 32 i + 8 q + 4 g + u of token 128 wm + 32 jj +

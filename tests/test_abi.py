@@ -208,7 +208,7 @@ def test_w8a8_linear_entry_points_reject_bad_arguments():
     assert call(N=0, ldy=0) == 0
     assert call(xq=None) == -1
     assert call(sw=None) == -1
-    assert call(K=288, ldx=384, ldw=384) == -1           # K % 64
+    assert call(K=320, ldx=384, ldw=384) == -1           # K % 128
     assert call(K=192, ldx=192, ldw=192) == -1           # K < 256
     assert call(K=0) == -1
     assert call(N=260, ldy=264) == -1                    # N % 8

@@ -136,13 +136,13 @@ def linear_case(M, N, K, seed, bias=True, pad_y=0):
 
 
 @pytest.mark.parametrize("M,N,K,bias,pad_y", [
-    (512, 512, 512, True, 0),     # 2 x 2 tiles, 8 stages
-    (300, 200, 256, True, 0),     # ragged tiles in both M and N, 4 stages (the pipeline depth)
-    (1, 8, 320, False, 0),        # one row, 5 stages
+    (512, 512, 512, True, 0),     # 2 x 2 tiles, 4 stages
+    (300, 200, 256, True, 0),     # ragged tiles in both M and N, 2 stages (the pipeline depth)
+    (1, 8, 384, False, 0),        # one row, 3 stages
     (777, 1032, 256, True, 16),   # row-strided output, ragged everywhere
-    (64, 256, 1088, False, 0),    # 17 stages (odd), single tile
-    (2304, 2560, 384, True, 0),   # 90 tiles: several tiles per workgroup on a small GPU share
-    (8192, 4096, 256, False, 0),  # 512 tiles of 4 stages: two per workgroup, tile changes inside the copy lookahead
+    (64, 256, 1152, False, 0),    # 9 stages (odd), single tile
+    (2304, 2560, 384, True, 0),   # 90 tiles
+    (8192, 4096, 256, False, 0),  # 512 tiles of 2 stages: two per workgroup, tile changes inside the copy lookahead
 ])
 def test_linear_small(M, N, K, bias, pad_y):
     y, a8, sa_, w8, sw, b = linear_case(M, N, K, seed=M + N + K, bias=bias, pad_y=pad_y)
@@ -150,7 +150,7 @@ def test_linear_small(M, N, K, bias, pad_y):
 
 
 def test_linear_deterministic_and_zero_rows():
-    M, N, K = 260, 264, 320
+    M, N, K = 260, 264, 384
     x, w, b = W.linear_inputs(M, K, N, seed=11)
     x[5] = 0
     xd, wd = x.to(DEV), w.to(DEV)
