@@ -75,6 +75,9 @@ def parse_args():
     ap.add_argument("--comp", choices=["on", "off"], default="on",
                     help="also time the compensation branch and gate epilogue on the bf16 "
                          "layer's inputs and sparse output")
+    ap.add_argument("--linear", choices=["on", "off"], default="on",
+                    help="also time the W8A8 fp8 linear layer (per-token quantisation + "
+                         "fp8 GEMM) at the 14B-720P q/k/v/o projection shape")
     ap.add_argument("--copy-calib", action="store_true",
                     help="also time a plain 1 GiB device copy (HBM counter calibration)")
     return ap.parse_args()
@@ -157,6 +160,89 @@ def bench_comp(args, sa, W, dev, wl, q, k, v, o_s, sparse_ms):
         "gbs": {"comp_state": round(gbs(st_bytes, st_ms), 1),
                 "comp_out": round(gbs(out_bytes, out_ms), 1)},
     }
+
+
+def bench_linear(args, sa, W, dev):
+    """W8A8 fp8 linear layer at the 14B-720P projection shape (75,600 tokens,
+    5120 -> 5120): per-token e4m3 quantisation of the bf16 activations in one
+    pass, then the fp8 GEMM with per-token x per-channel scales and bias to a
+    bf16 output.  The weights are quantised once beforehand (offline in the
+    paper) and not timed.  A library fp8 GEMM with the same row-wise scales
+    (torch._scaled_mm, hipBLASLt) is timed beside it for context when
+    available."""
+    name = "wan14b_720p_qkvo"
+    M, K, N = W.LINEAR_SHAPES[name]
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    x = torch.randn(M, K, device=dev, generator=g)
+    x[:, :max(1, K // 1000)] *= 20.0                   # channel outliers
+    x = x.to(torch.bfloat16)
+    w = (torch.randn(N, K, device=dev, generator=g) / K ** 0.5).to(torch.bfloat16)
+    bias = 0.1 * torch.randn(N, device=dev, generator=g)
+    wq, sw = sa.sparse_attn_quant_rows_fp8(w)
+    xq = torch.empty(M, K, dtype=torch.uint8, device=dev)
+    sx = torch.empty(M, dtype=torch.float32, device=dev)
+    y = torch.empty(M, N, dtype=torch.bfloat16, device=dev)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+
+    def step(e=None):
+        if e:
+            e[0].record()
+        sa.sparse_attn_quant_rows_fp8(x, xq, sx)
+        if e:
+            e[1].record()
+        sa.sparse_attn_linear_w8a8(xq, sx, wq, sw, bias, y)
+        if e:
+            e[2].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    for s_ in range(args.steps):
+        step(ev[s_])
+    torch.cuda.synchronize()
+    q_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    g_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    flops = 2.0 * M * N * K
+    q_bytes = M * K * 2 + M * K + M * 4
+    g_tf = flops / (g_ms * 1e-3) / 1e12
+    out = {
+        "shape": {"tokens": M, "in_features": K, "out_features": N},
+        "ms_per_call": {"quant_rows_fp8": round(q_ms, 4), "linear_w8a8": round(g_ms, 4)},
+        "ms_per_layer": round(q_ms + g_ms, 4),
+        "roofline": {
+            "kernel": "linear_w8a8_kernel", "bound": "mfma", "achieved": round(g_tf, 1),
+            "peak": PEAK_FP8_TFLOPS, "unit": "TFLOP/s", "frac": round(g_tf / PEAK_FP8_TFLOPS, 4),
+            "traffic": None, "flops_per_launch": flops,
+        },
+        "quant_roofline": {
+            "kernel": "quant_rows_kernel", "bound": "hbm",
+            "achieved": round(q_bytes / (q_ms * 1e-3) / 1e9, 1), "peak": PEAK_HBM_GBS,
+            "unit": "GB/s", "frac": round(q_bytes / (q_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+            "traffic": None, "algorithmic_bytes_per_launch": q_bytes,
+        },
+    }
+    try:
+        f = lambda: torch._scaled_mm(xq.view(torch.float8_e4m3fn),
+                                     wq.view(torch.float8_e4m3fn).t(),
+                                     scale_a=sx.view(-1, 1), scale_b=sw.view(1, -1),
+                                     bias=None, out_dtype=torch.bfloat16)
+        for _ in range(3):
+            f()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            f()
+        e1.record()
+        torch.cuda.synchronize()
+        lib_ms = e0.elapsed_time(e1) / args.steps
+        out["library_fp8_gemm"] = {"what": "torch._scaled_mm (hipBLASLt), row-wise scales, "
+                                           "no bias", "ms": round(lib_ms, 4),
+                                   "tflops": round(flops / (lib_ms * 1e-3) / 1e12, 1)}
+    except Exception as exc:  # pragma: no cover - depends on the torch build
+        out["library_fp8_gemm"] = {"error": str(exc)[:120]}
+    return out
 
 
 def bench_fp8(args, sa, W, dev):
@@ -326,6 +412,8 @@ def main():
         out["compensation"] = bench_comp(args, sa, W, dev, wl, q, kk, v, o, ms_step)
     if args.fp8 == "on":
         out["fp8"] = bench_fp8(args, sa, W, dev)
+    if args.linear == "on":
+        out["linear_w8a8"] = bench_linear(args, sa, W, dev)
 
     if args.copy_calib:
         a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
