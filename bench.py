@@ -78,6 +78,9 @@ def parse_args():
     ap.add_argument("--linear", choices=["on", "off"], default="on",
                     help="also time the W8A8 fp8 linear layer (per-token quantisation + "
                          "fp8 GEMM) at the 14B-720P q/k/v/o projection shape")
+    ap.add_argument("--causal", choices=["on", "off"], default="on",
+                    help="also time the causal-window variant (auto-regressive generation in "
+                         "chunks of 3 latent frames, full history) on the same layer")
     ap.add_argument("--copy-calib", action="store_true",
                     help="also time a plain 1 GiB device copy (HBM counter calibration)")
     return ap.parse_args()
@@ -159,6 +162,67 @@ def bench_comp(args, sa, W, dev, wl, q, k, v, o_s, sparse_ms):
         },
         "gbs": {"comp_state": round(gbs(st_bytes, st_ms), 1),
                 "comp_out": round(gbs(out_bytes, out_ms), 1)},
+    }
+
+
+def bench_causal(args, sa, W, dev, wl, q, k, v):
+    """The sparse branch restricted to a causal window: the same layer
+    generated auto-regressively in chunks of 3 latent frames (3 x 45 x 80 =
+    10,800 tokens), every earlier chunk visible.  Selection ranks only the
+    candidate key blocks (k = 36 of them where there are that many); the
+    forward masks keys outside each query's window."""
+    B, H, N, d, block = wl.batch, wl.heads, wl.seqlen, wl.head_dim, wl.block
+    nb = -(-N // block)
+    k_keep = sa.sparse_attn_keep_count(wl.keep_bp, nb)
+    chunk = 3 * wl.grid[1] * wl.grid[2]
+    causal = (chunk, 0)
+    idx = torch.empty(B, H, nb, k_keep, dtype=torch.int32, device=dev)
+    cnt = torch.empty(B, H, nb, dtype=torch.int32, device=dev)
+    o = torch.empty_like(q)
+    lse = torch.empty(B, H, N, dtype=torch.float32, device=dev)
+    desc = sa.make_desc(q, k, v, o, block=block, causal=causal)
+    ws_sel = torch.empty(sa.sparse_attn_workspace_size(desc, sa.SA_OP_SELECT, k_keep),
+                         dtype=torch.uint8, device=dev)
+    ws_sch = torch.empty(sa.sparse_attn_workspace_size(desc, sa.SA_OP_SCHEDULE, k_keep),
+                         dtype=torch.uint8, device=dev)
+    order = torch.empty(sa.sparse_attn_num_tiles(desc), dtype=torch.int32, device=dev)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+
+    def step(e=None):
+        if e:
+            e[0].record()
+        sa.sparse_attn_select(q, k, k_keep, block=block, idx=idx, cnt=cnt, ws=ws_sel,
+                              causal=causal)
+        if e:
+            e[1].record()
+        sa.sparse_attn_schedule(cnt, N, k_keep, block=block, order=order, ws=ws_sch)
+        if e:
+            e[2].record()
+        sa.sparse_attn_fwd(q, k, v, idx, cnt, block=block, order=order, o=o, lse=lse,
+                           causal=causal)
+        if e:
+            e[3].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    for s_ in range(args.steps):
+        step(ev[s_])
+    torch.cuda.synchronize()
+    ms = [float(np.mean([e[i].elapsed_time(e[i + 1]) for e in ev])) for i in range(3)]
+    flops = selected_flops(cnt.cpu().numpy(), idx.cpu().numpy(), N, block, d)
+    tf = flops / (ms[2] * 1e-3) / 1e12
+    return {
+        "chunk_tokens": chunk, "window_chunks": 0,
+        "ms_per_call": {"select": round(ms[0], 4), "schedule": round(ms[1], 4),
+                        "fwd": round(ms[2], 4)},
+        "ms_per_step": round(sum(ms), 4),
+        "mean_kept_blocks": round(float(cnt.float().mean().item()), 2),
+        "roofline": {"kernel": "fwd_bf16_kernel", "bound": "mfma", "achieved": round(tf, 2),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tf / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "flops_per_launch": flops,
+                     "note": "flops of the selected blocks; masked pairs counted"},
     }
 
 
@@ -412,6 +476,8 @@ def main():
         out["compensation"] = bench_comp(args, sa, W, dev, wl, q, kk, v, o, ms_step)
     if args.fp8 == "on":
         out["fp8"] = bench_fp8(args, sa, W, dev)
+    if args.causal == "on":
+        out["causal"] = bench_causal(args, sa, W, dev, wl, q, kk, v)
     if args.linear == "on":
         out["linear_w8a8"] = bench_linear(args, sa, W, dev)
 

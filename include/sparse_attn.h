@@ -74,6 +74,21 @@ typedef struct {
   int64_t v_stride[3];
   int64_t o_stride[3];
   float softmax_scale;
+  /* Causal window (paper §1: the sparse attention restricted to a causal
+   * window for auto-regressive generation).  Tokens form chunks of
+   * causal_chunk consecutive tokens (the latent frames generated together);
+   * query t in chunk c = t / causal_chunk attends only keys of chunks
+   * [c - causal_window + 1, c] (causal_window 0: every earlier chunk).
+   * causal_chunk 0 (with causal_window 0) leaves attention unrestricted.
+   * With a window, sparse_attn_select (row mode) ranks only the candidate
+   * key blocks (those holding an allowed key of some query of the block) and
+   * keeps min(budget, candidates) of them (cnt says how many; the rest of the
+   * row is -1); the forward calls mask every score outside a query's allowed
+   * keys, and a row left with none gets O = 0 and LSE = -inf.  The whole-head
+   * selection mode and the compensation calls return SA_ERR_UNSUPPORTED with
+   * a window.  Negative values, or a window without chunks: SA_ERR_INVALID_ARG. */
+  int32_t causal_chunk;
+  int32_t causal_window;
 } sparse_attn_desc;
 
 /* SPARSE_ATTN_VERSION of the built library. */

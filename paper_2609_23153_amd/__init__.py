@@ -52,6 +52,7 @@ class SparseAttnDesc(ctypes.Structure):
         ("q_stride", ctypes.c_int64 * 3), ("k_stride", ctypes.c_int64 * 3),
         ("v_stride", ctypes.c_int64 * 3), ("o_stride", ctypes.c_int64 * 3),
         ("softmax_scale", ctypes.c_float),
+        ("causal_chunk", ctypes.c_int32), ("causal_window", ctypes.c_int32),
     ]
 
 
@@ -113,14 +114,19 @@ def _strides(t):
     return tuple(t.stride()[:3])
 
 
-def make_desc(q, k=None, v=None, o=None, block: int = 64, softmax_scale: float = 0.0):
-    """Descriptor for [B, H, N, d] tensors (strides in elements)."""
+def make_desc(q, k=None, v=None, o=None, block: int = 64, softmax_scale: float = 0.0,
+              causal=None):
+    """Descriptor for [B, H, N, d] tensors (strides in elements).  causal =
+    (chunk_tokens, window_chunks) restricts attention to a causal window
+    (window 0: every earlier chunk); None leaves it unrestricted."""
     B, H, N, d = q.shape
     desc = SparseAttnDesc()
     desc.batch, desc.heads, desc.seqlen, desc.head_dim, desc.block = B, H, N, d, block
     for field, t in (("q_stride", q), ("k_stride", k), ("v_stride", v), ("o_stride", o)):
         getattr(desc, field)[:] = _strides(t)
     desc.softmax_scale = softmax_scale
+    if causal is not None:
+        desc.causal_chunk, desc.causal_window = int(causal[0]), int(causal[1])
     return desc
 
 
@@ -177,14 +183,14 @@ def _workspace(desc, op, kmax, device):
 
 
 def sparse_attn_select(q, k, budget: int, block: int = 64, mode: int = SA_SELECT_ROW_TOPK,
-                       kmax: int | None = None, idx=None, cnt=None, ws=None):
+                       kmax: int | None = None, idx=None, cnt=None, ws=None, causal=None):
     """Block selection on bf16 q, k [B, H, N, 128].  Returns (idx, cnt):
     idx int32 [B, H, nb, kmax] (ascending, -1 padded), cnt int32 [B, H, nb]."""
     B, H, N, _ = q.shape
     nb = _num_blocks(N, block)
     if kmax is None:
         kmax = budget if mode == SA_SELECT_ROW_TOPK else nb
-    desc = make_desc(q, k, block=block)
+    desc = make_desc(q, k, block=block, causal=causal)
     if idx is None:
         idx = torch.empty(B, H, nb, kmax, dtype=torch.int32, device=q.device)
     if cnt is None:
@@ -221,7 +227,7 @@ def sparse_attn_schedule(cnt, seqlen: int, kmax: int, block: int = 64, order=Non
 
 
 def sparse_attn_fwd(q, k, v, idx, cnt, block: int = 64, softmax_scale: float = 0.0,
-                    with_lse: bool = True, order=None, o=None, lse=None):
+                    with_lse: bool = True, order=None, o=None, lse=None, causal=None):
     """Block-sparse attention forward on bf16 q, k, v [B, H, N, 128] with the
     lists from sparse_attn_select (and optionally the launch order from
     sparse_attn_schedule).  Returns (o bf16 [B, H, N, 128], lse fp32
@@ -233,7 +239,7 @@ def sparse_attn_fwd(q, k, v, idx, cnt, block: int = 64, softmax_scale: float = 0
         o = torch.empty_like(q, memory_format=torch.contiguous_format)
     if with_lse and lse is None:
         lse = torch.empty(B, H, N, dtype=torch.float32, device=q.device)
-    desc = make_desc(q, k, v, o, block=block, softmax_scale=softmax_scale)
+    desc = make_desc(q, k, v, o, block=block, softmax_scale=softmax_scale, causal=causal)
     st = library().sparse_attn_fwd(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(idx),
                                    _ptr(cnt), kmax, _ptr(order), _ptr(o),
                                    _ptr(lse if with_lse else None), _stream(q))
@@ -259,7 +265,7 @@ def sparse_attn_quant_fp8(x, block: int = 64, x8=None, scale=None):
 
 def sparse_attn_fwd_fp8(q8, sq, k8, sk, v8, sv, idx, cnt, block: int = 64,
                         softmax_scale: float = 0.0, with_lse: bool = True, order=None, o=None,
-                        lse=None):
+                        lse=None, causal=None):
     """Block-sparse attention forward on e4m3 operands from
     sparse_attn_quant_fp8.  Returns (o bf16 [B, H, N, 128], lse or None)."""
     B, H, N, d = q8.shape
@@ -273,7 +279,7 @@ def sparse_attn_fwd_fp8(q8, sq, k8, sk, v8, sv, idx, cnt, block: int = 64,
         o = torch.empty(B, H, N, d, dtype=torch.bfloat16, device=q8.device)
     if with_lse and lse is None:
         lse = torch.empty(B, H, N, dtype=torch.float32, device=q8.device)
-    desc = make_desc(o, o=o, block=block, softmax_scale=softmax_scale)
+    desc = make_desc(o, o=o, block=block, softmax_scale=softmax_scale, causal=causal)
     st = library().sparse_attn_fwd_fp8(ctypes.byref(desc), _ptr(q8), _ptr(sq), _ptr(k8),
                                        _ptr(sk), _ptr(v8), _ptr(sv), _ptr(idx), _ptr(cnt), kmax,
                                        _ptr(order), _ptr(o), _ptr(lse if with_lse else None),

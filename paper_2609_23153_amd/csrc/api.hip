@@ -33,6 +33,12 @@ int check_desc(const sparse_attn_desc* d, Shape* s) {
   // query tiles (and so launch slots) must fit the 32-bit tile index
   const int64_t ntiles = (d->seqlen + 63) / 64;
   if ((int64_t)d->batch * d->heads * ntiles > (int64_t)1 << 30) return SA_ERR_UNSUPPORTED;
+  // causal window: chunk >= 0 tokens (0: none), window >= 0 chunks (0: all
+  // earlier chunks), and no window without chunks
+  if (d->causal_chunk < 0 || d->causal_window < 0) return SA_ERR_INVALID_ARG;
+  if (d->causal_chunk == 0 && d->causal_window != 0) return SA_ERR_INVALID_ARG;
+  s->causal_chunk = d->causal_chunk;
+  s->causal_window = d->causal_window;
   s->B = d->batch;
   s->H = d->heads;
   s->N = d->seqlen;
@@ -128,6 +134,7 @@ int sparse_attn_select(const sparse_attn_desc* desc, const void* q, const void* 
     if (budget < 1 || budget > s.nb || kmax < budget) return SA_ERR_INVALID_ARG;
   } else if (mode == SA_SELECT_HEAD_TOPK) {
     if (budget < s.nb || budget > (int64_t)s.nb * s.nb) return SA_ERR_INVALID_ARG;
+    if (s.causal_chunk > 0) return SA_ERR_UNSUPPORTED;  // whole-head budget: no causal window
   } else {
     return SA_ERR_INVALID_ARG;
   }
@@ -279,6 +286,7 @@ int sparse_attn_comp_state(const sparse_attn_desc* desc, int32_t rank, const voi
   Shape s;
   int st = check_desc(desc, &s);
   if (st != SA_OK) return st;
+  if (s.causal_chunk > 0) return SA_ERR_UNSUPPORTED;  // the state is not chunk-causal
   if (rank != 64) return SA_ERR_UNSUPPORTED;
   if (!k_norm || !kn_stride || !v || !pk || !rope || !state || !ws) return SA_ERR_INVALID_ARG;
   if (!aligned16(k_norm) || !aligned16(v) || !aligned16(pk) || !aligned16(rope) ||
@@ -307,6 +315,7 @@ int sparse_attn_comp_out(const sparse_attn_desc* desc, int32_t rank, const void*
   Shape s;
   int st = check_desc(desc, &s);
   if (st != SA_OK) return st;
+  if (s.causal_chunk > 0) return SA_ERR_UNSUPPORTED;  // the state is not chunk-causal
   if (rank != 64) return SA_ERR_UNSUPPORTED;
   if (!q_norm || !qn_stride || !pq || !rope || !state || !gate || !o_s || !o)
     return SA_ERR_INVALID_ARG;

@@ -65,6 +65,7 @@ struct Params {
   const int32_t* order;
   int kmax, H, N, block, nb, ntiles;  // ntiles = ceil(N / 64) query tiles per head
   float scale_log2;                   // tau * log2(e)
+  Shape cs;                           // causal window (causal_chunk 0: none)
 };
 
 // Start row of the n-th 64-key tile of a query block's list, or -1 when the
@@ -178,6 +179,14 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int rh = wave & 1, kh = wave >> 1;
   const int g = lane >> 5, l32 = lane & 31;
+
+  // Allowed keys [key_lo, key_hi) of this lane's query (the causal window,
+  // and the sequence end); a tile needs the per-score mask unless it lies
+  // inside every row's range: [lo of the tile's last row, hi of its first).
+  const int qtok = min(q0 + rh * 32 + l32, p.N - 1);
+  const int key_lo = causal_lo(p.cs, qtok), key_hi = causal_hi(p.cs, qtok);
+  const int tile_lo = causal_lo(p.cs, min(q0 + kTile - 1, p.N - 1));
+  const int tile_hi = causal_hi(p.cs, q0);
 
   // Per-head buffer resources covering rows [0, N): rows past N read zero.
   const uint32_t kst = (uint32_t)p.ks.n * 2, vst = (uint32_t)p.vs.n * 2, qst = (uint32_t)p.qs.n * 2;
@@ -300,11 +309,11 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
     for (int ks = 0; ks < 8; ++ks)
       s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], qf[ks], s, 0, 0, 0);
     // lane holds keys kh*32 + 8*(r>>2) + 4*g + (r&3) of query l32
-    if (s0 + kTile > p.N) {
+    if (s0 + kTile > tile_hi || s0 < tile_lo) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int key = s0 + kh * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
-        if (key >= p.N) s[r] = -INFINITY;
+        if (key >= key_hi || key < key_lo) s[r] = -INFINITY;
       }
     }
 
@@ -454,6 +463,7 @@ hipError_t launch_fwd_bf16(const Shape& s, const FwdArgs& a, hipStream_t stream)
   p.nb = s.nb;
   p.ntiles = (s.N + kTile - 1) / kTile;
   p.scale_log2 = a.softmax_scale * 1.4426950408889634f;
+  p.cs = s;
   const int grid = s.B * s.H * p.ntiles;
   fwd_bf16_kernel<<<grid, kThreads, 0, stream>>>(p);
   return hipGetLastError();

@@ -67,6 +67,7 @@ struct Params {
   const int32_t* order;
   int kmax, H, N, block, nb, ntiles;
   float scale_log2;
+  Shape cs;  // causal window (causal_chunk 0: none)
 };
 
 __device__ __forceinline__ int tile_start(list_ptr list, int n, int spb, int block, int nb,
@@ -131,6 +132,14 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int rh = wave & 1, par = wave >> 1;  // row half, tile parity
   const int g = lane >> 5, l32 = lane & 31;
+
+  // Allowed keys [key_lo, key_hi) of this lane's query (the causal window,
+  // and the sequence end); a tile needs the per-score mask unless it lies
+  // inside every row's range: [lo of the tile's last row, hi of its first).
+  const int qtok = min(q0 + rh * 32 + l32, p.N - 1);
+  const int key_lo = causal_lo(p.cs, qtok), key_hi = causal_hi(p.cs, qtok);
+  const int tile_lo = causal_lo(p.cs, min(q0 + kTile - 1, p.N - 1));
+  const int tile_hi = causal_hi(p.cs, q0);
 
   const int64_t head = (int64_t)bh * p.N * kRowBytes;
   const uint32_t bytes = (uint32_t)p.N * kRowBytes;
@@ -321,13 +330,13 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
                                                                  0, sk_code, 0, sq_code);
     }
     // lane holds keys 32*rt + 8*(r>>2) + 4*g + (r&3) of query l32
-    if (start + kTile > p.N) {
+    if (start + kTile > tile_hi || start < tile_lo) {
 #pragma unroll
       for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int key = start + 32 * rt + 8 * (r >> 2) + 4 * g + (r & 3);
-          if (key >= p.N) s[rt][r] = -INFINITY;
+          if (key >= key_hi || key < key_lo) s[rt][r] = -INFINITY;
         }
     }
 
@@ -489,6 +498,7 @@ hipError_t launch_fwd_fp8(const Shape& s, const FwdArgs& a, hipStream_t stream) 
   p.nb = s.nb;
   p.ntiles = (s.N + kTile - 1) / kTile;
   p.scale_log2 = a.softmax_scale * 1.4426950408889634f;
+  p.cs = s;
   fwd_fp8_kernel<<<s.B * s.H * p.ntiles, kThreads, 0, stream>>>(p);
   return hipGetLastError();
 }

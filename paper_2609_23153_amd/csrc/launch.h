@@ -15,7 +15,23 @@ struct Strides {
 
 struct Shape {
   int B, H, N, block, nb;  // nb = ceil(N / block) query blocks = key blocks
+  // causal window: query t (chunk t / causal_chunk) sees the keys of chunks
+  // [c - causal_window + 1, c] (causal_window 0: every earlier chunk);
+  // causal_chunk 0: no restriction
+  int causal_chunk = 0, causal_window = 0;
 };
+
+// Allowed key tokens [lo, hi) of query token t under the causal window.
+__host__ __device__ inline int causal_lo(const Shape& s, int t) {
+  if (s.causal_chunk <= 0 || s.causal_window == 0) return 0;
+  const int c = t / s.causal_chunk - s.causal_window + 1;
+  return c > 0 ? c * s.causal_chunk : 0;
+}
+__host__ __device__ inline int causal_hi(const Shape& s, int t) {
+  if (s.causal_chunk <= 0) return s.N;
+  const long long h = (long long)(t / s.causal_chunk + 1) * s.causal_chunk;
+  return h < s.N ? (int)h : s.N;
+}
 
 // ---- selection -----------------------------------------------------------
 // Workspace layout: qhat [B*H*nb*128] f64 | khat [same] | scores [B*H*nb*nb] f64

@@ -230,20 +230,33 @@ __device__ __forceinline__ uint32_t kth_largest32(const uint32_t (&v)[KPL], cons
 template <int KPL>
 __global__ __launch_bounds__(256) void topk_row_kernel(const double* __restrict__ scores,
                                                        int nb, int rows, int k_all, int kmax,
-                                                       bool k_per_row, int32_t* __restrict__ idx,
+                                                       bool k_per_row, Shape cs,
+                                                       int32_t* __restrict__ idx,
                                                        int32_t* __restrict__ cnt) {
   const int lane = threadIdx.x & (kWave - 1);
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= rows) return;  // uniform per wave
-  // the row's k: one value for all rows, or (ragged mode) read from cnt
-  const int k = k_per_row ? __builtin_amdgcn_readfirstlane(cnt[row]) : k_all;
+  // Candidate key blocks [jlo, jhi): under a causal window those holding an
+  // allowed key of some query of the block (the allowed ranges never move
+  // back as the query advances, so the first query's lower end and the last
+  // query's upper end bound them); otherwise every block.
+  int jlo = 0, jhi = nb;
+  if (cs.causal_chunk > 0) {
+    const int first = (row % nb) * cs.block;
+    const int last = min(first + cs.block, cs.N) - 1;
+    jlo = causal_lo(cs, first) / cs.block;
+    jhi = (causal_hi(cs, last) + cs.block - 1) / cs.block;
+  }
+  // the row's k: one value for all rows, or (ragged mode) read from cnt;
+  // never more than the candidates
+  const int k = min(k_per_row ? __builtin_amdgcn_readfirstlane(cnt[row]) : k_all, jhi - jlo);
   const double* s = scores + (int64_t)row * nb;
   uint32_t hi[KPL], lo[KPL];
   bool valid[KPL];
 #pragma unroll
   for (int t = 0; t < KPL; ++t) {
     const int j = lane + kWave * t;
-    valid[t] = j < nb;
+    valid[t] = j >= jlo && j < jhi;
     const uint64_t key = valid[t] ? order_key(s[j]) : 0ull;
     hi[t] = (uint32_t)(key >> 32);
     lo[t] = (uint32_t)key;
@@ -296,22 +309,24 @@ __global__ __launch_bounds__(256) void topk_row_kernel(const double* __restrict_
 
 template <int KPL>
 hipError_t launch_topk(const double* scores, int nb, int rows, int k, int kmax, bool k_per_row,
+                       const Shape& cs,
                        int32_t* idx, int32_t* cnt, hipStream_t stream) {
   topk_row_kernel<KPL><<<(rows + 3) / 4, 256, 0, stream>>>(scores, nb, rows, k, kmax, k_per_row,
-                                                            idx, cnt);
+                                                            cs, idx, cnt);
   return hipGetLastError();
 }
 
 // Row top-k over the score matrix with the register tile that fits nb.
 hipError_t launch_topk_any(const double* scores, int nb, int rows, int k, int kmax,
-                           bool k_per_row, int32_t* idx, int32_t* cnt, hipStream_t stream) {
+                           bool k_per_row, const Shape& cs, int32_t* idx, int32_t* cnt,
+                           hipStream_t stream) {
   const int kpl = (nb + kWave - 1) / kWave;
 #define SA_TOPK(n) \
-  if (kpl <= n) return launch_topk<n>(scores, nb, rows, k, kmax, k_per_row, idx, cnt, stream);
+  if (kpl <= n) return launch_topk<n>(scores, nb, rows, k, kmax, k_per_row, cs, idx, cnt, stream);
   SA_TOPK(1) SA_TOPK(2) SA_TOPK(4) SA_TOPK(8) SA_TOPK(12) SA_TOPK(16) SA_TOPK(20) SA_TOPK(24)
   SA_TOPK(32)
 #undef SA_TOPK
-  return launch_topk<64>(scores, nb, rows, k, kmax, k_per_row, idx, cnt, stream);
+  return launch_topk<64>(scores, nb, rows, k, kmax, k_per_row, cs, idx, cnt, stream);
 }
 
 // ---- whole-head ragged selection ------------------------------------------
@@ -553,7 +568,7 @@ hipError_t launch_select_row(const Shape& s, const void* q, Strides qs, const vo
   hipError_t e = launch_pool_score(s, q, qs, k, ks, ws, &scores, stream);
   if (e != hipSuccess) return e;
   const int rows = s.B * s.H * s.nb;
-  return launch_topk_any(scores, s.nb, rows, topk, kmax, false, idx, cnt, stream);
+  return launch_topk_any(scores, s.nb, rows, topk, kmax, false, s, idx, cnt, stream);
 }
 
 hipError_t launch_select_head(const Shape& s, const void* q, Strides qs, const void* k,
@@ -581,7 +596,10 @@ hipError_t launch_select_head(const Shape& s, const void* q, Strides qs, const v
   head_count_kernel<<<(rows + 3) / 4, 256, 0, stream>>>(scores, s.nb, rows, w);
   head_rowk_kernel<<<bh, kRowKThreads, 0, stream>>>(s.nb, kmax, w, cnt);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  return launch_topk_any(scores, s.nb, rows, 0, kmax, true, idx, cnt, stream);
+  Shape unrestricted = s;  // the whole-head mode has no causal window
+  unrestricted.causal_chunk = 0;
+  unrestricted.causal_window = 0;
+  return launch_topk_any(scores, s.nb, rows, 0, kmax, true, unrestricted, idx, cnt, stream);
 }
 
 }  // namespace sa

@@ -221,3 +221,29 @@ def test_w8a8_linear_entry_points_reject_bad_arguments():
     assert call(bias=MIS) == -1                          # misaligned bias
     assert call(M=-5) == -1
     assert call(ldx=1 << 24) == -2                       # 256 * ldx does not fit 32 bits
+
+
+def test_causal_window_fields_are_checked():
+    lib = sa.library()
+    st3 = (ctypes.c_int64 * 3)(2 * 4096 * 128, 4096 * 128, 128)
+    need = lib.sparse_attn_workspace_size(ctypes.byref(desc()), sa.SA_OP_SELECT, 7)
+
+    def sel(chunk, window, mode=sa.SA_SELECT_ROW_TOPK, budget=7):
+        ds = desc()
+        ds.causal_chunk, ds.causal_window = chunk, window
+        return lib.sparse_attn_select(ctypes.byref(ds), P, P, mode, budget, P, P, 64, P, need,
+                                      None)
+
+    assert sel(-1, 0) == -1                       # negative chunk
+    assert sel(1024, -2) == -1                    # negative window
+    assert sel(0, 3) == -1                        # window without chunks
+    assert sel(1024, 2, mode=sa.SA_SELECT_HEAD_TOPK, budget=500) == -2   # whole-head mode
+    ds = desc()
+    ds.causal_chunk, ds.causal_window = 1024, 2
+    cneed = lib.sparse_attn_workspace_size(ctypes.byref(ds), sa.SA_OP_COMP_STATE, 1)
+    assert lib.sparse_attn_comp_state(ctypes.byref(ds), 64, P, st3, P, P, P, P, P, cneed,
+                                      None) == -2
+    g3 = (ctypes.c_int64 * 3)(2 * 4096, 4096, 1)
+    assert lib.sparse_attn_comp_out(ctypes.byref(ds), 64, P, st3, P, P, P, None, 1e-6, P, g3,
+                                    P, P, None) == -2
+    assert ctypes.sizeof(sa.SparseAttnDesc) == 136   # the C struct with the two int32 fields
