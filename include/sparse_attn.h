@@ -54,7 +54,7 @@ enum {
 };
 
 /* Workspace consumers (second argument of sparse_attn_workspace_size). */
-enum { SA_OP_SELECT = 0, SA_OP_SCHEDULE = 1, SA_OP_COMP_STATE = 2 };
+enum { SA_OP_SELECT = 0, SA_OP_SCHEDULE = 1, SA_OP_COMP_STATE = 2, SA_OP_BWD = 3 };
 
 /*
  * Problem descriptor (host struct).
@@ -236,6 +236,29 @@ int sparse_attn_comp_out(const sparse_attn_desc* desc, int32_t rank, const void*
                          const int64_t qn_stride[3], const void* pq, const float* rope,
                          const float* state, const float* gamma, float eps, const float* gate,
                          const int64_t gate_stride[3], const void* o_s, void* o, void* stream);
+
+/*
+ * Backward of the sparse branch (the gradients that the sparse model's
+ * training needs, paper §4 Stage 1): for the lists idx/cnt that the forward
+ * used, and its output o and log-sum-exp lse, with P = softmax(tau Q K_U^T)
+ * over each query block's selected keys U:
+ *   dV_U += P^T dO,  dS = P o (dO V_U^T - D),  D = rowsum(dO o O),
+ *   dQ = tau dS K_U,  dK_U += tau dS^T Q.
+ * Every key is covered: keys that no query block selected get dK = dV = 0,
+ * query blocks with an empty list get dQ = 0.  Products are bf16 MFMA with
+ * fp32 accumulation; P and dS enter the second products as bf16; outputs are
+ * bf16.  Deterministic (no floating-point atomics).
+ *  q, k, v, o, d_o   bf16 via desc strides (d_o laid out like o)
+ *  lse               fp32 [B][H][L] natural log, as the forward wrote it
+ *  idx, cnt, kmax    the forward's lists
+ *  dq, dk, dv        bf16 out, laid out like q, k, v (desc strides)
+ *  ws                ws_bytes >= sparse_attn_workspace_size(SA_OP_BWD)
+ * Errors: SA_ERR_UNSUPPORTED with a causal window; SA_ERR_INVALID_ARG for
+ * null or misaligned pointers and bad strides; SA_ERR_WORKSPACE. */
+int sparse_attn_bwd(const sparse_attn_desc* desc, const void* q, const void* k, const void* v,
+                    const void* o, const void* d_o, const float* lse, const int32_t* idx,
+                    const int32_t* cnt, int32_t kmax, void* dq, void* dk, void* dv, void* ws,
+                    size_t ws_bytes, void* stream);
 
 /*
  * W8A8 FP8 linear layers (paper §4.3: the attention and feed-forward

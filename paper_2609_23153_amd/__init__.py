@@ -20,14 +20,14 @@ __all__ = [
     "sparse_attn_num_tiles", "sparse_attn_select", "sparse_attn_schedule", "sparse_attn_fwd",
     "sparse_attn_quant_fp8", "sparse_attn_fwd_fp8", "sparse_attn_comp_state",
     "sparse_attn_comp_out", "SA_OP_COMP_STATE", "COMP_RANK", "make_desc", "EXPORTED_SYMBOLS",
-    "sparse_attn_quant_rows_fp8", "sparse_attn_linear_w8a8",
+    "sparse_attn_quant_rows_fp8", "sparse_attn_linear_w8a8", "sparse_attn_bwd", "SA_OP_BWD",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsparseattn.so")
 
 SA_SELECT_ROW_TOPK = 0
 SA_SELECT_HEAD_TOPK = 1
-SA_OP_SELECT, SA_OP_SCHEDULE, SA_OP_COMP_STATE = 0, 1, 2
+SA_OP_SELECT, SA_OP_SCHEDULE, SA_OP_COMP_STATE, SA_OP_BWD = 0, 1, 2, 3
 COMP_RANK = 64
 
 EXPORTED_SYMBOLS = (
@@ -35,7 +35,7 @@ EXPORTED_SYMBOLS = (
     "sparse_attn_workspace_size", "sparse_attn_num_tiles", "sparse_attn_select",
     "sparse_attn_schedule", "sparse_attn_fwd", "sparse_attn_quant_fp8", "sparse_attn_fwd_fp8",
     "sparse_attn_comp_state", "sparse_attn_comp_out", "sparse_attn_quant_rows_fp8",
-    "sparse_attn_linear_w8a8",
+    "sparse_attn_linear_w8a8", "sparse_attn_bwd",
 )
 
 
@@ -93,6 +93,9 @@ def library() -> ctypes.CDLL:
                                                     _P, ctypes.c_float, _P, _I64P, _P, _P, _P]),
             "sparse_attn_quant_rows_fp8": (ctypes.c_int, [_P, ctypes.c_int64, ctypes.c_int64,
                                                           ctypes.c_int64, _P, _P, _P]),
+            "sparse_attn_bwd": (ctypes.c_int, [D, _P, _P, _P, _P, _P, _P, _P, _P,
+                                               ctypes.c_int32, _P, _P, _P, _P, ctypes.c_size_t,
+                                               _P]),
             "sparse_attn_linear_w8a8": (ctypes.c_int, [_P, _P, ctypes.c_int64, _P, _P,
                                                        ctypes.c_int64, _P, _P, ctypes.c_int64,
                                                        ctypes.c_int64, ctypes.c_int64,
@@ -386,3 +389,28 @@ def sparse_attn_linear_w8a8(xq, sx, wq, sw, bias=None, y=None):
         None if bias is None else _ptr(bias), _ptr(y), y.stride(0), M, N, K, _stream(xq))
     _check(st, "sparse_attn_linear_w8a8")
     return y
+
+
+# ---------------------------------------------------------------- backward
+def sparse_attn_bwd(q, k, v, o, d_o, lse, idx, cnt, block: int = 64,
+                    softmax_scale: float = 0.0, dq=None, dk=None, dv=None, ws=None):
+    """Gradients (dq, dk, dv) bf16 of the sparse forward for upstream d_o
+    (laid out like o), given the forward's lists, output and lse."""
+    kmax = idx.shape[-1]
+    _dense(idx, "idx"), _dense(cnt, "cnt"), _dense(lse, "lse", torch.float32)
+    if tuple(d_o.stride()) != tuple(o.stride()):
+        raise ValueError("d_o must be laid out like o")
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    for name, a, ref in (("dq", dq, q), ("dk", dk, k), ("dv", dv, v)):
+        if tuple(a.stride()) != tuple(ref.stride()):
+            raise ValueError(f"{name} must be laid out like its input")
+    desc = make_desc(q, k, v, o, block=block, softmax_scale=softmax_scale)
+    if ws is None:
+        ws = _workspace(desc, SA_OP_BWD, kmax, q.device)
+    st = library().sparse_attn_bwd(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(o),
+                                   _ptr(d_o), _ptr(lse), _ptr(idx), _ptr(cnt), kmax, _ptr(dq),
+                                   _ptr(dk), _ptr(dv), _ptr(ws), ws.numel(), _stream(q))
+    _check(st, "sparse_attn_bwd")
+    return dq, dk, dv

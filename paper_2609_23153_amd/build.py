@@ -18,7 +18,7 @@ OUT_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libsparseattn.so")
 
 SOURCES = ["api.hip", "select.hip", "sched.hip", "fwd_bf16.hip", "fwd_fp8.hip", "quant_fp8.hip",
-           "comp.hip", "linear_fp8.hip"]
+           "comp.hip", "linear_fp8.hip", "bwd.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -98,6 +98,7 @@ size_t sparse_attn_workspace_size(const sparse_attn_desc* desc, int32_t op, int3
     case SA_OP_SELECT: return sa::select_workspace_bytes(s);
     case SA_OP_SCHEDULE: return kmax >= 1 ? sa::schedule_workspace_bytes(s) : 0;
     case SA_OP_COMP_STATE: return sa::comp_state_workspace_bytes(s);
+    case SA_OP_BWD: return sa::bwd_workspace_bytes(s);
     default: return 0;
   }
 }
@@ -267,6 +268,44 @@ int sparse_attn_linear_w8a8(const uint8_t* xq, const float* sx, int64_t ldx, con
   in.K = K;
   in.group_m = 0;
   return launch_status(sa::launch_linear_w8a8(in, static_cast<hipStream_t>(stream)));
+}
+
+int sparse_attn_bwd(const sparse_attn_desc* desc, const void* q, const void* k, const void* v,
+                    const void* o, const void* d_o, const float* lse, const int32_t* idx,
+                    const int32_t* cnt, int32_t kmax, void* dq, void* dk, void* dv, void* ws,
+                    size_t ws_bytes, void* stream) {
+  Shape s;
+  int st = check_desc(desc, &s);
+  if (st != SA_OK) return st;
+  if (s.causal_chunk > 0) return SA_ERR_UNSUPPORTED;  // no causal window in the backward
+  if (!q || !k || !v || !o || !d_o || !lse || !dq || !dk || !dv || !ws) return SA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(d_o) ||
+      !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
+    return SA_ERR_INVALID_ARG;
+  if (!strides_ok(desc->q_stride) || !strides_ok(desc->k_stride) ||
+      !strides_ok(desc->v_stride) || !strides_ok(desc->o_stride))
+    return SA_ERR_INVALID_ARG;
+  if ((st = check_lists(s, idx, cnt, kmax)) != SA_OK) return st;
+  if (ws_bytes < sa::bwd_workspace_bytes(s)) return SA_ERR_WORKSPACE;
+  sa::BwdIn in{};
+  in.q = q;
+  in.k = k;
+  in.v = v;
+  in.o = o;
+  in.dout = d_o;
+  in.lse = lse;
+  in.idx = idx;
+  in.cnt = cnt;
+  in.dq = dq;
+  in.dk = dk;
+  in.dv = dv;
+  in.qs = to_strides(desc->q_stride);
+  in.ks = to_strides(desc->k_stride);
+  in.vs = to_strides(desc->v_stride);
+  in.os = to_strides(desc->o_stride);
+  in.kmax = kmax;
+  in.softmax_scale = effective_scale(desc);
+  return launch_status(sa::launch_bwd(s, in, ws, static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

@@ -95,6 +95,27 @@ hipError_t launch_comp_state(const Shape& s, const CompStateIn& in, float* state
                              hipStream_t stream);
 hipError_t launch_comp_out(const Shape& s, const CompOutIn& in, hipStream_t stream);
 
+// ---- backward ------------------------------------------------------------
+struct BwdIn {
+  const void* q;
+  const void* k;
+  const void* v;
+  const void* o;
+  const void* dout;   // laid out like o
+  const float* lse;   // [B][H][N] natural log, from the forward
+  const int32_t* idx;
+  const int32_t* cnt;
+  void* dq;           // laid out like q
+  void* dk;           // like k
+  void* dv;           // like v
+  Strides qs, ks, vs, os;
+  int kmax;
+  float softmax_scale;
+};
+// Workspace: D fp32 [B*H*N] (256-byte aligned) | bitmap u32 [B*H][nb][ceil(nb/32)]
+size_t bwd_workspace_bytes(const Shape& s);
+hipError_t launch_bwd(const Shape& s, const BwdIn& in, void* ws, hipStream_t stream);
+
 // ---- fp8 quantisation ----------------------------------------------------
 hipError_t launch_quant_fp8(const Shape& s, const void* x, Strides xs, uint8_t* x8,
                             float* scale, hipStream_t stream);

@@ -1,0 +1,123 @@
+"""GPU parity of the sparse-branch backward through the C ABI against the
+fp64 oracle on identical seeded inputs.
+
+The GPU takes the forward's own bf16 O and fp32 LSE, rounds P and dS to bf16
+for the second products and rounds dQ, dK, dV to bf16, each a relative
+error of at most 2^-9 per term; these average out in the sums, and the
+measured rel-L2 is a few 1e-3.  Bars per gradient and head: rel-L2 <= 1e-2
+(the forward's bf16 bar) and max |err| <= 2e-2 max |ref| (the forward's
+max-abs bar relative to the gradient's scale, which the inputs do not fix)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2609_23153_amd as sa
+import workloads as W
+from gpu_helpers import rel_l2, say, widen
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+TAU = W.softmax_scale(128)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    sa.library()
+    yield
+    torch.cuda.synchronize()
+
+
+def run_bwd(q, k, v, idx, cnt, block, seed):
+    g = torch.Generator().manual_seed(seed)
+    do = torch.randn(q.shape, generator=g).to(torch.bfloat16)
+    qd, kd, vd, dod = (t.to(DEV) for t in (q, k, v, do))
+    idxd, cntd = idx.to(DEV), cnt.to(DEV)
+    o, lse = sa.sparse_attn_fwd(qd, kd, vd, idxd, cntd, block=block)
+    dq, dk, dv = sa.sparse_attn_bwd(qd, kd, vd, o, dod, lse, idxd, cntd, block=block)
+    torch.cuda.synchronize()
+    return do, dq.cpu(), dk.cpu(), dv.cpu()
+
+
+def check_grads(q, k, v, do, idx, cnt, block, dq, dk, dv, what, heads=None):
+    B, H = q.shape[:2]
+    idx_c, cnt_c = idx.numpy(), cnt.numpy()
+    for b in range(B):
+        for h in (range(H) if heads is None else heads):
+            ref = O.sparse_attention_backward(widen(q[b, h]), widen(k[b, h]), widen(v[b, h]),
+                                              widen(do[b, h]), idx_c[b, h], cnt_c[b, h], block,
+                                              TAU)
+            msg = []
+            for name, got, r in zip(("dq", "dk", "dv"), (dq, dk, dv), ref):
+                gg = got[b, h].to(torch.float64).numpy()
+                e = rel_l2(gg, r)
+                scale = float(np.abs(r).max()) or 1.0
+                m = float(np.abs(gg - r).max()) / scale
+                msg.append(f"{name} rel_l2={e:.2e} max/scale={m:.2e}")
+                assert e <= 1e-2 and m <= 2e-2, (what, b, h, name, e, m)
+                # exact zeros where the oracle has no contribution
+                zero = np.all(r == 0, axis=1)
+                assert np.all(gg[zero] == 0), (what, name, "nonzero where nothing contributes")
+            say(f"  {what} b{b} h{h}: " + "  ".join(msg))
+
+
+def test_bwd_tiny():
+    wl = W.WORKLOADS["tiny"]
+    q, k, v = W.make_inputs(wl)
+    nb = O.block_count(wl.seqlen, wl.block)
+    kk = O.keep_count(wl.keep_bp, nb)
+    idx, cnt = sa.sparse_attn_select(q.to(DEV), k.to(DEV), kk, block=wl.block)
+    idx, cnt = idx.cpu(), cnt.cpu()
+    do, dq, dk, dv = run_bwd(q, k, v, idx, cnt, wl.block, 1)
+    check_grads(q, k, v, do, idx, cnt, wl.block, dq, dk, dv, "tiny")
+
+
+@pytest.mark.parametrize("N,block", [(1000, 64), (1000, 128), (200, 64), (4096, 128)])
+def test_bwd_ragged_lists_with_empty_rows(N, block):
+    """Random ragged lists (about 15% empty), ragged last block: dQ = 0 for
+    empty lists, dK = dV = 0 for keys nobody selected."""
+    g = torch.Generator().manual_seed(N * 3 + block)
+    q, k, v = (torch.randn(1, 2, N, 128, generator=g).to(torch.bfloat16) for _ in range(3))
+    nb = O.block_count(N, block)
+    kmax = min(nb, 7)
+    idx = np.full((1, 2, nb, kmax), -1, dtype=np.int32)
+    cnt = np.zeros((1, 2, nb), dtype=np.int32)
+    for h in range(2):
+        ii, cc = W.random_block_lists(nb, nb, kmax, seed=N + block + h, p_empty=0.15)
+        idx[0, h], cnt[0, h] = ii, cc
+    idx, cnt = torch.from_numpy(idx), torch.from_numpy(cnt)
+    do, dq, dk, dv = run_bwd(q, k, v, idx, cnt, block, 2)
+    check_grads(q, k, v, do, idx, cnt, block, dq, dk, dv, f"ragged N={N} b={block}")
+
+
+def test_bwd_deterministic():
+    wl = W.WORKLOADS["tiny"]
+    q, k, v = (t.to(DEV) for t in W.make_inputs(wl))
+    kk = O.keep_count(wl.keep_bp, O.block_count(wl.seqlen, wl.block))
+    idx, cnt = sa.sparse_attn_select(q, k, kk)
+    o, lse = sa.sparse_attn_fwd(q, k, v, idx, cnt)
+    do = torch.randn_like(q)
+    a = sa.sparse_attn_bwd(q, k, v, o, do, lse, idx, cnt)
+    b = sa.sparse_attn_bwd(q, k, v, o, do, lse, idx, cnt)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x.view(torch.int16), y.view(torch.int16))
+
+
+def test_bwd_full_size_one_head():
+    """The 14B-720P layer (40 heads, 75,600 tokens, 36 of 1182 blocks): the
+    whole backward runs in one launch; head 0 is checked against the oracle
+    (all its query blocks, since dK and dV gather from every one), every
+    gradient checked finite."""
+    wl = W.WORKLOADS["wan14b_720p"]
+    q, k, v = W.make_inputs(wl)
+    kk = O.keep_count(wl.keep_bp, O.block_count(wl.seqlen, wl.block))
+    idx, cnt = sa.sparse_attn_select(q.to(DEV), k.to(DEV), kk, block=wl.block)
+    idx, cnt = idx.cpu(), cnt.cpu()
+    do, dq, dk, dv = run_bwd(q, k, v, idx, cnt, wl.block, 3)
+    for t in (dq, dk, dv):
+        assert torch.isfinite(t.float()).all()
+    check_grads(q, k, v, do, idx, cnt, wl.block, dq, dk, dv, "14B-720P", heads=[0])
