@@ -162,10 +162,77 @@ __global__ __launch_bounds__(kThreads) void bwd_bits_set_kernel(BwdParams p) {
   }
 }
 
+// ---- copy pipeline ---------------------------------------------------------
+// Tiles of 64 rows x 256 bytes move global -> LDS with buffer_load ... lds
+// (issued from inline asm, so every wait on them is explicit): each wave
+// moves rows 16 w .. 16 w + 15 in 4 instructions of 4 rows, lane l landing
+// in slot l % 16 of its row, i.e. fetching the logical chunk that swz() puts
+// there.  Rows past the resource range (the sequence end) read zero.
+struct TileDma {
+  uint32_t off[4];  // per-lane byte offsets within a tile (row stride applied)
+};
+__device__ __forceinline__ TileDma tile_dma(uint32_t row_bytes) {
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  TileDma t;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = 16 * w + 4 * i + (l >> 4);
+    t.off[i] = (uint32_t)row * row_bytes + (uint32_t)swz(row, l & 15) * 16u;
+  }
+  return t;
+}
+__device__ __forceinline__ void dma_tile(uint8_t* dst, __amdgpu_buffer_rsrc_t r, const TileDma& t,
+                                         uint32_t soff) {
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const uint32_t base = lds_addr(dst) + (uint32_t)(16 * w) * kRowBytes;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) dma16(base + 4 * i * kRowBytes, r, t.off[i], soff);
+}
+__device__ __forceinline__ void wait_vm0() {
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+}
+__device__ __forceinline__ void wait_vm8() {
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_waitcnt(0x0F78);
+}
+__device__ __forceinline__ void wait_vm9() {
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_waitcnt(0x0F79);
+}
+__device__ __forceinline__ void wait_lgkm0() {
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_waitcnt(0xC07F);
+}
+
+// Start row of the n-th 64-key tile of a query block's list (skipping
+// entries out of range and sub-tiles past the end), or N when exhausted.
+__device__ __forceinline__ int list_tile(list_ptr list, int n, int total, int spb, int block,
+                                         int nb, int N, int* next) {
+  for (; n < total; ++n) {
+    const int e = n / spb;
+    const int j = list[e];
+    if (j < 0 || j >= nb) continue;
+    const int st = j * block + (n - e * spb) * kTile;
+    if (st < N) {
+      *next = n + 1;
+      return st;
+    }
+  }
+  *next = total;
+  return N;
+}
+
 // ---- dQ -------------------------------------------------------------------
+// Two workgroups per CU (80 KB of LDS each): the dO tile stays in LDS, K and
+// V tiles are double-buffered, and the copies of tile n + 2 are issued once
+// every wave is done with tile n.
 __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p) {
-  __shared__ __attribute__((aligned(1024))) uint8_t kt[kTileBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t vt[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t kb0[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t kb1[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t vb0[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t vb1[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t db[kTileBytes];
 
   const int bh = blockIdx.x / p.ntiles;
   const int qt = blockIdx.x - bh * p.ntiles;
@@ -175,28 +242,41 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p) {
   const int spb = p.block / kTile;
   const list_ptr list = (list_ptr)(p.idx + ((int64_t)bh * p.nb + iblk) * p.kmax);
   const int c = min(max(p.cnt[(int64_t)bh * p.nb + iblk], 0), p.kmax);
+  const int total = c * spb;
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int rh = wave & 1, kh = wave >> 1;
   const int g = lane >> 5, l32 = lane & 31;
-  const uint16_t* qh_ = p.q + b * p.qs.b + h * p.qs.h;
-  const uint16_t* kh_ = p.k + b * p.ks.b + h * p.ks.h;
-  const uint16_t* vh_ = p.v + b * p.vs.b + h * p.vs.h;
-  const uint16_t* doh = p.dout + b * p.os.b + h * p.os.h;
 
-  // Q and dO fragments of this lane's query (B operands), staged through LDS
-  bf16x8 qf[8], df[8];
-  stage_tile(kt, qh_, p.qs.n, q0, p.N);
-  stage_tile(vt, doh, p.os.n, q0, p.N);
-  __syncthreads();
+  const uint32_t qst = (uint32_t)p.qs.n * 2, kst = (uint32_t)p.ks.n * 2, vst = (uint32_t)p.vs.n * 2,
+                 ost = (uint32_t)p.os.n * 2;
+  const auto kr = make_rsrc(p.k + b * p.ks.b + h * p.ks.h, (uint32_t)(p.N - 1) * kst + 256u);
+  const auto vr = make_rsrc(p.v + b * p.vs.b + h * p.vs.h, (uint32_t)(p.N - 1) * vst + 256u);
+  const TileDma kd = tile_dma(kst), vd = tile_dma(vst);
+
+  // prologue: Q through kb1, dO into db, tiles 0 and 1 of the list
+  int nx = 0;
+  int s0 = list_tile(list, nx, total, spb, p.block, p.nb, p.N, &nx);
+  int s1 = list_tile(list, nx, total, spb, p.block, p.nb, p.N, &nx);
   {
-    const int row = rh * 32 + l32;
-#pragma unroll
-    for (int ks = 0; ks < 8; ++ks) {
-      qf[ks] = row_frag(kt, row, ks, g);
-      df[ks] = row_frag(vt, row, ks, g);
-    }
+    const auto qr = make_rsrc(p.q + b * p.qs.b + h * p.qs.h, (uint32_t)(p.N - 1) * qst + 256u);
+    const auto dr = make_rsrc(p.dout + b * p.os.b + h * p.os.h, (uint32_t)(p.N - 1) * ost + 256u);
+    dma_tile(kb1, qr, tile_dma(qst), (uint32_t)q0 * qst);
+    dma_tile(db, dr, tile_dma(ost), (uint32_t)q0 * ost);
   }
+  dma_tile(kb0, kr, kd, (uint32_t)s0 * kst);
+  dma_tile(vb0, vr, vd, (uint32_t)s0 * vst);
+  wait_vm8();  // Q and dO landed (this wave's rows)
+  barrier_keep_loads();
+  bf16x8 qf[8];
+  const int drow = rh * 32 + l32;  // this lane's dO row in db
+#pragma unroll
+  for (int ks = 0; ks < 8; ++ks) qf[ks] = row_frag(kb1, drow, ks, g);
+  wait_lgkm0();
+  barrier_keep_loads();  // kb1 free
+  dma_tile(kb1, kr, kd, (uint32_t)s1 * kst);
+  dma_tile(vb1, vr, vd, (uint32_t)s1 * vst);
+
   const int qtok = q0 + rh * 32 + l32;
   const int qc = min(qtok, p.N - 1);
   const float lse2 = p.lse[(int64_t)bh * p.N + qc] * kLog2e;
@@ -209,49 +289,65 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[dt][r] = 0.f;
 
-  for (int n = 0; n < c * spb; ++n) {
-    const int j = list[n / spb];
-    if (j < 0 || j >= p.nb) continue;                     // uniform
-    const int s0 = j * p.block + (n % spb) * kTile;
-    if (s0 >= p.N) continue;
-    __syncthreads();  // previous tile fully read
-    stage_tile(kt, kh_, p.ks.n, s0, p.N);
-    stage_tile(vt, vh_, p.vs.n, s0, p.N);
-    __syncthreads();
-    // S^T (keys x queries) and dP^T
+  // One tile from buffers (kt, vt); once every wave is done reading them they
+  // receive the tile two ahead, whose start is returned.
+  auto step = [&](uint8_t* kt, uint8_t* vt, int st) {
+    wait_vm8();  // this tile landed; the next one may still fly
+    barrier_keep_loads();
     f32x16 s, dp;
 #pragma unroll
     for (int r = 0; r < 16; ++r) s[r] = dp[r] = 0.f;
     const int krow = kh * 32 + l32;
 #pragma unroll
-    for (int ks = 0; ks < 8; ++ks) {
+    for (int ks = 0; ks < 8; ++ks)
       s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(kt, krow, ks, g), qf[ks], s, 0, 0, 0);
-      dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(vt, krow, ks, g), df[ks], dp, 0, 0, 0);
-    }
-    // lane: query qtok, keys s0 + kh*32 + 8(r>>2) + 4g + (r&3)
+    __builtin_amdgcn_sched_barrier(0);  // bound the fragments in flight
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks)
+      dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(vt, krow, ks, g),
+                                                   row_frag(db, drow, ks, g), dp, 0, 0, 0);
+    // lane: query qtok, keys st + kh*32 + 8(r>>2) + 4g + (r&3)
     float ds[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int key = s0 + kh * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
+      const int key = st + kh * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
       const float pr = key < p.N ? __builtin_amdgcn_exp2f(fmaf(s[r], c2, -lse2)) : 0.f;
       ds[r] = pr * (dp[r] - dq_d);
     }
     bf16x8 pk[2];
     pack_b(ds, pk);
-    // dQ^T += K^T dS^T
+    __builtin_amdgcn_sched_barrier(0);
     u32x4 kf[8];
     trans_frags(kt, kh * 32, lane, kf);
+    wait_lgkm0();
+    barrier_keep_loads();  // every wave is done reading kt / vt
+    const int s2 = list_tile(list, nx, total, spb, p.block, p.nb, p.N, &nx);
+    dma_tile(kt, kr, kd, (uint32_t)s2 * kst);
+    dma_tile(vt, vr, vd, (uint32_t)s2 * vst);
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
       for (int cs = 0; cs < 2; ++cs)
         acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[2 * dt + cs]), pk[cs],
                                                           acc[dt], 0, 0, 0);
+    return s2;
+  };
+  // tile n sits in buffer n % 2; (st, stn) = starts of tiles n, n + 1
+  int st = s0, stn = s1;
+  while (st < p.N) {
+    const int s2 = step(kb0, vb0, st);
+    st = stn;
+    stn = s2;
+    if (st >= p.N) break;
+    const int s3 = step(kb1, vb1, st);
+    st = stn;
+    stn = s3;
   }
+  wait_vm0();
+  barrier_keep_loads();
 
   // sum the two key halves, scale by tau, store
-  __syncthreads();
-  float* mrg = reinterpret_cast<float*>(rh ? vt : kt);  // 64 x 64 floats per row-half
+  float* mrg = reinterpret_cast<float*>(rh ? vb0 : kb0);  // 64 x 64 floats per row-half
   if (kh == 1) {
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
@@ -278,159 +374,275 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p) {
 }
 
 // ---- dK, dV ---------------------------------------------------------------
-__global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p) {
-  __shared__ __attribute__((aligned(1024))) uint8_t qt_[kTileBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t dt_[kTileBytes];
-  __shared__ float lse_s[kTile];
-  __shared__ float d_s[kTile];
+// One workgroup per 64-key tile (two per CU: 80 KB of LDS, at most 256
+// registers a lane); the query tiles of the query blocks that selected its
+// key block (set bits of its bitmap row, ascending) stream through
+// double-buffered Q and dO tiles, the copies of tile n + 2 issued once every
+// wave is done with tile n.  Each step has two phases:
+//  1. wave (kh, qh): S^T = K Q^T and dP^T = V dO^T for keys 32 kh.. and
+//     query rows 32 qh.. (K, V fragments held in registers), so a lane holds
+//     one query row and needs only its LSE and D; P and dS go to LDS as bf16;
+//  2. wave (kh, ch): dV^T += dO^T P and dK^T += Q^T dS for keys 32 kh.. and
+//     channels 64 ch.., over all 64 rows of the tile (dO^T, Q^T, P and dS by
+//     transposed LDS reads).
+// P and dS are kept in four 2 KB blocks, one per phase-1 wave (kh, qh): 32
+// query rows of 64 B (32 keys), 8-byte unit u of row r at slot
+// u ^ ((r >> 2) & 7), conflict-free both for the row writes of phase 1 and
+// the transposed reads of phase 2.
+constexpr int kPBlock = 2048;
+
+// Lane id read afresh, so that offsets derived from it are recomputed where
+// they are used instead of being held in registers across the loop.
+__device__ __forceinline__ int fresh_lane() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+
+// Transposed reads (ds_read_b64_tr_b16) of the 16 rows r16.. (r16 a multiple
+// of 16) of a 64-row tile: lane 16 G + 4 e + q reads the 8 bytes of row
+// r16 + 8 hf + 4 (G >> 1) + e at channels 32 dtg + 16 (G & 1) + 4 q, so that
+// lane l holds channel 32 dtg + (l & 31) of rows r16 + 4 g + {0..3} (hf = 0)
+// and r16 + 8 + 4 g + {0..3} (hf = 1): an A operand over those 16 rows.
+// The row's swizzle depends on row & 15 only, so the lane's byte offset is
+// the same for every r16.
+__device__ __forceinline__ uint32_t trans_off(int lane, int hf, int dtg) {
+  const int G = lane >> 4, e4 = (lane >> 2) & 3, q4 = lane & 3;
+  const int row = 8 * hf + 4 * (G >> 1) + e4;
+  const int lc = 4 * dtg + 2 * (G & 1) + (q4 >> 1);
+  return (uint32_t)(row * kRowBytes + swz(row, lc) * 16 + (q4 & 1) * 8);
+}
+__device__ __forceinline__ u32x2 tr_read(const uint8_t* p) {
+  const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p);
+  return __builtin_bit_cast(u32x2, v);
+}
+__device__ __forceinline__ bf16x8 tr_pair(const uint8_t* p0, const uint8_t* p1) {
+  const u32x2 a = tr_read(p0), b = tr_read(p1);
+  const u32x4 f = {a[0], a[1], b[0], b[1]};
+  return as_bf16x8(f);
+}
+
+// P and dS: byte offset of the 8-byte unit u (keys 4u..4u+3 of key half kh)
+// of query row `row` (0..63).
+__device__ __forceinline__ int p_off(int kh, int row, int u) {
+  const int qq = row & 31;
+  return (kh + 2 * (row >> 5)) * kPBlock + qq * 64 + 8 * (u ^ ((qq >> 2) & 7));
+}
+// The same transposed read from a P / dS buffer: lane l gets key
+// 32 kh + (l & 31) of the rows r16 + 8 hf + 4 g + {0..3} (a B operand in the
+// k order of trans_off).  Offset for r16 with bit 4 = b4, before adding
+// (r16 >> 5) * 2 kPBlock + b4 * 16 * 64.
+__device__ __forceinline__ uint32_t ptr_off(int lane, int hf, int b4, int kh) {
+  const int G = lane >> 4, e4 = (lane >> 2) & 3, q4 = lane & 3;
+  const int qq = 16 * b4 + 8 * hf + 4 * (G >> 1) + e4;
+  return (uint32_t)(p_off(kh, qq, 4 * (G & 1) + q4) - b4 * 16 * 64);
+}
+
+__global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p) {
+  __shared__ __attribute__((aligned(1024))) uint8_t qb0[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t qb1[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t ob0[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t ob1[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t pbuf[4 * kPBlock];
+  __shared__ __attribute__((aligned(1024))) uint8_t sbuf[4 * kPBlock];
 
   const int bh = blockIdx.x / p.ntiles;
   const int kt0 = blockIdx.x - bh * p.ntiles;
   const int b = bh / p.H, h = bh - b * p.H;
   const int k0 = kt0 * kTile;
   const int jblk = k0 / p.block;
+  const int spb = p.block / kTile;
   const bits_ptr row_bits = (bits_ptr)(p.bits + ((int64_t)bh * p.nb + jblk) * p.nw);
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int kh = wave & 1, qh = wave >> 1;
+  const int kh = wave & 1, hh = wave >> 1;  // phase 1: query half hh, phase 2: channel half hh
   const int g = lane >> 5, l32 = lane & 31;
-  const uint16_t* qh_ = p.q + b * p.qs.b + h * p.qs.h;
-  const uint16_t* kh_ = p.k + b * p.ks.b + h * p.ks.h;
-  const uint16_t* vh_ = p.v + b * p.vs.b + h * p.vs.h;
-  const uint16_t* doh = p.dout + b * p.os.b + h * p.os.h;
 
-  // K and V fragments of this lane's key (B operands of S = Q K^T, dP = dO V^T)
+  const uint32_t qst = (uint32_t)p.qs.n * 2, ost = (uint32_t)p.os.n * 2;
+  const auto qr = make_rsrc(p.q + b * p.qs.b + h * p.qs.h, (uint32_t)(p.N - 1) * qst + 256u);
+  const auto dr = make_rsrc(p.dout + b * p.os.b + h * p.os.h, (uint32_t)(p.N - 1) * ost + 256u);
+  const TileDma qd = tile_dma(qst), od = tile_dma(ost);
+  const float* lse_h = p.lse + (int64_t)bh * p.N;
+  const float* d_h = p.dvec + (int64_t)bh * p.N;
+
+  // Cursor over the query tiles: set bits of the bitmap row (query blocks,
+  // ascending), then the block's 64-row sub-tiles; N once exhausted.
+  int cw = 0, ci = -1, csub = 0;
+  uint32_t cword = p.nw > 0 ? row_bits[0] : 0u;
+  auto next_start = [&]() {
+    if (ci >= 0 && ++csub < spb) {
+      const int st = ci * p.block + csub * kTile;
+      if (st < p.N) return st;
+    }
+    while (cword == 0u && cw + 1 < p.nw) cword = row_bits[++cw];
+    if (cword == 0u) return p.N;
+    ci = 32 * cw + __builtin_ctz(cword);
+    cword &= cword - 1u;
+    csub = 0;
+    return ci * p.block;  // i < nb, so this start is < N
+  };
+  // LSE and D of this lane's phase-1 query row of the tile starting at st
+  // (the row clamped into the sequence; see to_log2 for rows past its end)
+  auto load_vec = [&](int st, float& lv, float& dv) {
+    const int tc = min(st + hh * 32 + l32, p.N - 1);
+    lv = lse_h[tc];
+    dv = d_h[tc];
+  };
+  // LSE in log2 units, +inf for rows past the end (P = 0 there)
+  auto to_log2 = [&](int st, float lv) {
+    return st + hh * 32 + l32 < p.N ? lv * kLog2e : INFINITY;
+  };
+
+  // K and V fragments of this lane's key (A operands of S^T and dP^T)
+  const int key = k0 + kh * 32 + l32;
   bf16x8 kf[8], vf[8];
-  stage_tile(qt_, kh_, p.ks.n, k0, p.N);
-  stage_tile(dt_, vh_, p.vs.n, k0, p.N);
-  __syncthreads();
   {
-    const int row = kh * 32 + l32;
+    const uint16_t* kp = p.k + b * p.ks.b + h * p.ks.h + (int64_t)min(key, p.N - 1) * p.ks.n;
+    const uint16_t* vp = p.v + b * p.vs.b + h * p.vs.h + (int64_t)min(key, p.N - 1) * p.vs.n;
+    const u32x4 z = {0u, 0u, 0u, 0u};
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) {
-      kf[ks] = row_frag(qt_, row, ks, g);
-      vf[ks] = row_frag(dt_, row, ks, g);
+      kf[ks] = as_bf16x8(key < p.N ? ld16(kp + 16 * ks + 8 * g) : z);
+      vf[ks] = as_bf16x8(key < p.N ? ld16(vp + 16 * ks + 8 * g) : z);
     }
   }
-  const float c2 = p.tau * kLog2e;
+  const int s0 = next_start();
+  const int s1 = next_start();
+  float lse2, dd;
+  load_vec(s0, lse2, dd);
+  asm volatile("" : "+v"(lse2), "+v"(dd) : "v"(kf[0]), "v"(kf[7]), "v"(vf[0]), "v"(vf[7]));
+  lse2 = to_log2(s0, lse2);
+  dma_tile(qb0, qr, qd, (uint32_t)s0 * qst);
+  dma_tile(ob0, dr, od, (uint32_t)s0 * ost);
+  dma_tile(qb1, qr, qd, (uint32_t)s1 * qst);
+  dma_tile(ob1, dr, od, (uint32_t)s1 * ost);
 
-  f32x16 acck[4], accv[4];
+  const float c2 = p.tau * kLog2e;
+  f32x16 acck[2], accv[2];
 #pragma unroll
-  for (int dt = 0; dt < 4; ++dt)
+  for (int dt = 0; dt < 2; ++dt)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acck[dt][r] = accv[dt][r] = 0.f;
 
-  const int spb = p.block / kTile;
-  for (int w = 0; w < p.nw; ++w) {
-    uint32_t word = row_bits[w];
-    while (word) {
-      const int i = 32 * w + __builtin_ctz(word);  // query block, ascending
-      word &= word - 1;
-      for (int sub = 0; sub < spb; ++sub) {
-        const int r0 = i * p.block + sub * kTile;
-        if (r0 >= p.N) break;
-        __syncthreads();  // previous query tile fully read
-        stage_tile(qt_, qh_, p.qs.n, r0, p.N);
-        stage_tile(dt_, doh, p.os.n, r0, p.N);
-        if (threadIdx.x < kTile) {
-          const int t = r0 + threadIdx.x;
-          const bool live = t < p.N;
-          lse_s[threadIdx.x] = live ? p.lse[(int64_t)bh * p.N + t] * kLog2e : INFINITY;
-          d_s[threadIdx.x] = live ? p.dvec[(int64_t)bh * p.N + t] : 0.f;
+  // One query tile from (qt, ot) starting at st; stn starts the next one.
+  // Once every wave is done reading (qt, ot) they receive the tile two
+  // ahead, whose start is returned.
+  auto step = [&](uint8_t* qt, uint8_t* ot, int st, int stn) {
+    wait_vm8();  // this tile landed; the next one may still fly
+    barrier_keep_loads();
+    float lsen, ddn;
+    load_vec(stn, lsen, ddn);  // waited for before the next copies are issued
+    // phase 1: lane holds query row 32 hh + l32, keys 32 kh + 8(r>>2) + 4g + (r&3)
+    f32x16 s, dp;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s[r] = dp[r] = 0.f;
+    {
+      const int ln = fresh_lane(), g1 = ln >> 5;
+      const int qrow = hh * 32 + (ln & 31);
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks)
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], row_frag(qt, qrow, ks, g1), s, 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks)
+        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[ks], row_frag(ot, qrow, ks, g1), dp, 0, 0,
+                                                     0);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float pv[4], dv[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          pv[e] = __builtin_amdgcn_exp2f(fmaf(s[4 * i + e], c2, -lse2));
+          dv[e] = pv[e] * (dp[4 * i + e] - dd);
         }
-        __syncthreads();
-        // S (queries x keys) and dP: lane holds key kh*32 + l32, queries
-        // qh*32 + 8(r>>2) + 4g + (r&3)
-        f32x16 s, dp;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[r] = dp[r] = 0.f;
-        const int qrow = qh * 32 + l32;
-#pragma unroll
-        for (int ks = 0; ks < 8; ++ks) {
-          s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(qt_, qrow, ks, g), kf[ks], s, 0, 0,
-                                                      0);
-          dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(dt_, qrow, ks, g), vf[ks], dp, 0,
-                                                       0, 0);
-        }
-        float pv[16], ds[16];
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int ql = qh * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
-          const float pr = __builtin_amdgcn_exp2f(fmaf(s[r], c2, -lse_s[ql]));
-          pv[r] = pr;
-          ds[r] = pr * (dp[r] - d_s[ql]);
-        }
-        bf16x8 pp[2], pd[2];
-        pack_b(pv, pp);
-        pack_b(ds, pd);
-        u32x4 tf[8];
-        trans_frags(dt_, qh * 32, lane, tf);  // dO^T
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-          for (int cs = 0; cs < 2; ++cs)
-            accv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(tf[2 * dt + cs]), pp[cs],
-                                                               accv[dt], 0, 0, 0);
-        trans_frags(qt_, qh * 32, lane, tf);  // Q^T
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-          for (int cs = 0; cs < 2; ++cs)
-            acck[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(tf[2 * dt + cs]), pd[cs],
-                                                               acck[dt], 0, 0, 0);
+        const int off = p_off(kh, qrow, 2 * i + g1);
+        u32x2 wp, wd;
+        wp[0] = pack_bf16x2(pv[0], pv[1]);
+        wp[1] = pack_bf16x2(pv[2], pv[3]);
+        wd[0] = pack_bf16x2(dv[0], dv[1]);
+        wd[1] = pack_bf16x2(dv[2], dv[3]);
+        *reinterpret_cast<u32x2*>(pbuf + off) = wp;
+        *reinterpret_cast<u32x2*>(sbuf + off) = wd;
       }
     }
-  }
-
-  // sum the two query halves, store dK = tau * acck, dV = accv
-  __syncthreads();
-  float* mk = reinterpret_cast<float*>(kh ? dt_ : qt_);  // 64 x 64 floats per key half
-  if (qh == 1) {
+    wait_lgkm0();
+    barrier_keep_loads();  // P and dS of the whole tile in LDS
+    // phase 2: keys 32 kh.., channels 64 hh.. (MFMA output: lane holds key
+    // 32 kh + l32, channels 64 hh + 32 dt + 8(r>>2) + 4g + (r&3))
+    {
+      const int ln = fresh_lane();
+      uint32_t to[2][2], po[2][2];
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
+      for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mk[(dt * 16 + r) * kWave + lane] = acck[dt][r];
-  }
-  __syncthreads();
-  const int key = k0 + kh * 32 + l32;
-  if (qh == 0 && key < p.N) {
-    uint16_t* out = p.dk + b * p.ks.b + h * p.ks.h + (int64_t)key * p.ks.n;
+        for (int x = 0; x < 2; ++x) {
+          to[hf][x] = trans_off(ln, hf, 2 * hh + x);
+          po[hf][x] = ptr_off(ln, hf, x, kh);
+        }
+#define PFRAG(buf, r16)                                                                     \
+  tr_pair(buf + ((r16) >> 5) * 2 * kPBlock + ((r16)&16) * 64 + po[0][((r16) >> 4) & 1],     \
+          buf + ((r16) >> 5) * 2 * kPBlock + ((r16)&16) * 64 + po[1][((r16) >> 4) & 1])
+#define TFRAG(t, r16, dt) tr_pair(t + (r16)*kRowBytes + to[0][dt], t + (r16)*kRowBytes + to[1][dt])
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
+      for (int r16 = 0; r16 < kTile; r16 += 16) {
+        const bf16x8 pf = PFRAG(pbuf, r16);
 #pragma unroll
-      for (int jq = 0; jq < 4; ++jq) {
-        float x[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          x[r] = p.tau * (acck[dt][4 * jq + r] + mk[(dt * 16 + 4 * jq + r) * kWave + lane]);
-        u32x2 w;
-        w[0] = pack_bf16x2(x[0], x[1]);
-        w[1] = pack_bf16x2(x[2], x[3]);
-        *reinterpret_cast<u32x2*>(out + dt * 32 + 8 * jq + 4 * g) = w;
+        for (int dt = 0; dt < 2; ++dt)
+          accv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(TFRAG(ot, r16, dt), pf, accv[dt], 0, 0,
+                                                             0);
       }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int r16 = 0; r16 < kTile; r16 += 16) {
+        const bf16x8 sf = PFRAG(sbuf, r16);
+#pragma unroll
+        for (int dt = 0; dt < 2; ++dt)
+          acck[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(TFRAG(qt, r16, dt), sf, acck[dt], 0, 0,
+                                                             0);
+      }
+#undef PFRAG
+#undef TFRAG
+    }
+    wait_lgkm0();
+    barrier_keep_loads();  // every wave is done reading qt / ot / pbuf / sbuf
+    // the loads of the next tile's LSE and D complete here, before the copies
+    // (a wait for them after the copies would wait for the copies too)
+    asm volatile("" : "+v"(lsen), "+v"(ddn));
+    const int s2 = next_start();
+    dma_tile(qt, qr, qd, (uint32_t)s2 * qst);
+    dma_tile(ot, dr, od, (uint32_t)s2 * ost);
+    lse2 = to_log2(stn, lsen);
+    dd = ddn;
+    return s2;
+  };
+  int st = s0, stn = s1;
+  while (st < p.N) {
+    const int s2 = step(qb0, ob0, st, stn);
+    st = stn;
+    stn = s2;
+    if (st >= p.N) break;
+    const int s3 = step(qb1, ob1, st, stn);
+    st = stn;
+    stn = s3;
   }
-  __syncthreads();
-  if (qh == 1) {
+  wait_vm0();
+
+  // store dK = tau * acck, dV = accv (lane: key, 4 channels at a time)
+  if (key < p.N) {
+    uint16_t* ok = p.dk + b * p.ks.b + h * p.ks.h + (int64_t)key * p.ks.n + 64 * hh;
+    uint16_t* ov = p.dv + b * p.vs.b + h * p.vs.h + (int64_t)key * p.vs.n + 64 * hh;
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mk[(dt * 16 + r) * kWave + lane] = accv[dt][r];
-  }
-  __syncthreads();
-  if (qh == 0 && key < p.N) {
-    uint16_t* out = p.dv + b * p.vs.b + h * p.vs.h + (int64_t)key * p.vs.n;
-#pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
+    for (int dt = 0; dt < 2; ++dt)
 #pragma unroll
       for (int jq = 0; jq < 4; ++jq) {
-        float x[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          x[r] = accv[dt][4 * jq + r] + mk[(dt * 16 + 4 * jq + r) * kWave + lane];
-        u32x2 w;
-        w[0] = pack_bf16x2(x[0], x[1]);
-        w[1] = pack_bf16x2(x[2], x[3]);
-        *reinterpret_cast<u32x2*>(out + dt * 32 + 8 * jq + 4 * g) = w;
+        const int c = dt * 32 + 8 * jq + 4 * g;
+        u32x2 wk, wv;
+        wk[0] = pack_bf16x2(p.tau * acck[dt][4 * jq], p.tau * acck[dt][4 * jq + 1]);
+        wk[1] = pack_bf16x2(p.tau * acck[dt][4 * jq + 2], p.tau * acck[dt][4 * jq + 3]);
+        wv[0] = pack_bf16x2(accv[dt][4 * jq], accv[dt][4 * jq + 1]);
+        wv[1] = pack_bf16x2(accv[dt][4 * jq + 2], accv[dt][4 * jq + 3]);
+        *reinterpret_cast<u32x2*>(ok + c) = wk;
+        *reinterpret_cast<u32x2*>(ov + c) = wv;
       }
   }
 }
