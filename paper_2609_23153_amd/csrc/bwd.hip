@@ -223,11 +223,60 @@ __device__ __forceinline__ int list_tile(list_ptr list, int n, int total, int sp
   return N;
 }
 
+constexpr int kPBlock = 2048;  // one P or dS block of the dK/dV kernel
+
+// Lane id read afresh, so that offsets derived from it are recomputed where
+// they are used instead of being held in registers across the loop.
+__device__ __forceinline__ int fresh_lane() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+
+// Transposed reads (ds_read_b64_tr_b16) of the 16 rows r16.. (r16 a multiple
+// of 16) of a 64-row tile: lane 16 G + 4 e + q reads the 8 bytes of row
+// r16 + 8 hf + 4 (G >> 1) + e at channels 32 dtg + 16 (G & 1) + 4 q, so that
+// lane l holds channel 32 dtg + (l & 31) of rows r16 + 4 g + {0..3} (hf = 0)
+// and r16 + 8 + 4 g + {0..3} (hf = 1): an A operand over those 16 rows.
+// The row's swizzle depends on row & 15 only, so the lane's byte offset is
+// the same for every r16.
+__device__ __forceinline__ uint32_t trans_off(int lane, int hf, int dtg) {
+  const int G = lane >> 4, e4 = (lane >> 2) & 3, q4 = lane & 3;
+  const int row = 8 * hf + 4 * (G >> 1) + e4;
+  const int lc = 4 * dtg + 2 * (G & 1) + (q4 >> 1);
+  return (uint32_t)(row * kRowBytes + swz(row, lc) * 16 + (q4 & 1) * 8);
+}
+__device__ __forceinline__ u32x2 tr_read(const uint8_t* p) {
+  const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p);
+  return __builtin_bit_cast(u32x2, v);
+}
+__device__ __forceinline__ bf16x8 tr_pair(const uint8_t* p0, const uint8_t* p1) {
+  const u32x2 a = tr_read(p0), b = tr_read(p1);
+  const u32x4 f = {a[0], a[1], b[0], b[1]};
+  return as_bf16x8(f);
+}
+
+// P and dS: byte offset of the 8-byte unit u (keys 4u..4u+3 of key half kh)
+// of query row `row` (0..63).
+__device__ __forceinline__ int p_off(int kh, int row, int u) {
+  const int qq = row & 31;
+  return (kh + 2 * (row >> 5)) * kPBlock + qq * 64 + 8 * (u ^ ((qq >> 2) & 7));
+}
+// The same transposed read from a P / dS buffer: lane l gets key
+// 32 kh + (l & 31) of the rows r16 + 8 hf + 4 g + {0..3} (a B operand in the
+// k order of trans_off).  Offset for r16 with bit 4 = b4, before adding
+// (r16 >> 5) * 2 kPBlock + b4 * 16 * 64.
+__device__ __forceinline__ uint32_t ptr_off(int lane, int hf, int b4, int kh) {
+  const int G = lane >> 4, e4 = (lane >> 2) & 3, q4 = lane & 3;
+  const int qq = 16 * b4 + 8 * hf + 4 * (G >> 1) + e4;
+  return (uint32_t)(p_off(kh, qq, 4 * (G & 1) + q4) - b4 * 16 * 64);
+}
+
 // ---- dQ -------------------------------------------------------------------
 // Two workgroups per CU (80 KB of LDS each): the dO tile stays in LDS, K and
 // V tiles are double-buffered, and the copies of tile n + 2 are issued once
 // every wave is done with tile n.
-__global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p) {
+__global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
   __shared__ __attribute__((aligned(1024))) uint8_t kb0[kTileBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t kb1[kTileBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t vb0[kTileBytes];
@@ -254,6 +303,19 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p) {
   const auto vr = make_rsrc(p.v + b * p.vs.b + h * p.vs.h, (uint32_t)(p.N - 1) * vst + 256u);
   const TileDma kd = tile_dma(kst), vd = tile_dma(vst);
 
+  // this lane's query row: its LSE (log2 units) and D, loaded and waited for
+  // before any copy is issued (a later wait for them would drain the copies)
+  const int qtok = q0 + rh * 32 + l32;
+  float lse2, dq_d;
+  {
+    const int qc = min(qtok, p.N - 1);
+    lse2 = p.lse[(int64_t)bh * p.N + qc];
+    dq_d = p.dvec[(int64_t)bh * p.N + qc];
+    asm volatile("" : "+v"(lse2), "+v"(dq_d));
+    lse2 *= kLog2e;
+  }
+  const float c2 = p.tau * kLog2e;
+
   // prologue: Q through kb1, dO into db, tiles 0 and 1 of the list
   int nx = 0;
   int s0 = list_tile(list, nx, total, spb, p.block, p.nb, p.N, &nx);
@@ -277,12 +339,6 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p) {
   dma_tile(kb1, kr, kd, (uint32_t)s1 * kst);
   dma_tile(vb1, vr, vd, (uint32_t)s1 * vst);
 
-  const int qtok = q0 + rh * 32 + l32;
-  const int qc = min(qtok, p.N - 1);
-  const float lse2 = p.lse[(int64_t)bh * p.N + qc] * kLog2e;
-  const float dq_d = p.dvec[(int64_t)bh * p.N + qc];
-  const float c2 = p.tau * kLog2e;
-
   f32x16 acc[4];
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt)
@@ -297,15 +353,16 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p) {
     f32x16 s, dp;
 #pragma unroll
     for (int r = 0; r < 16; ++r) s[r] = dp[r] = 0.f;
-    const int krow = kh * 32 + l32;
+    const int ln = fresh_lane(), g1 = ln >> 5;
+    const int krow = kh * 32 + (ln & 31), drow1 = rh * 32 + (ln & 31);
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks)
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(kt, krow, ks, g), qf[ks], s, 0, 0, 0);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(kt, krow, ks, g1), qf[ks], s, 0, 0, 0);
     __builtin_amdgcn_sched_barrier(0);  // bound the fragments in flight
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks)
-      dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(vt, krow, ks, g),
-                                                   row_frag(db, drow, ks, g), dp, 0, 0, 0);
+      dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(vt, krow, ks, g1),
+                                                   row_frag(db, drow1, ks, g1), dp, 0, 0, 0);
     // lane: query qtok, keys st + kh*32 + 8(r>>2) + 4g + (r&3)
     float ds[16];
 #pragma unroll
@@ -317,8 +374,20 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p) {
     bf16x8 pk[2];
     pack_b(ds, pk);
     __builtin_amdgcn_sched_barrier(0);
-    u32x4 kf[8];
-    trans_frags(kt, kh * 32, lane, kf);
+    // K^T fragments: channels 32 dt.., keys 32 kh + 16 cs..
+    bf16x8 kf[4][2];
+    {
+      const int ln2 = fresh_lane();
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) {
+        const uint32_t o0 = trans_off(ln2, 0, dt), o1 = trans_off(ln2, 1, dt);
+#pragma unroll
+        for (int cs = 0; cs < 2; ++cs) {
+          const uint8_t* base = kt + (kh * 32 + 16 * cs) * kRowBytes;
+          kf[dt][cs] = tr_pair(base + o0, base + o1);
+        }
+      }
+    }
     wait_lgkm0();
     barrier_keep_loads();  // every wave is done reading kt / vt
     const int s2 = list_tile(list, nx, total, spb, p.block, p.nb, p.N, &nx);
@@ -328,8 +397,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p) {
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
       for (int cs = 0; cs < 2; ++cs)
-        acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[2 * dt + cs]), pk[cs],
-                                                          acc[dt], 0, 0, 0);
+        acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[dt][cs], pk[cs], acc[dt], 0, 0, 0);
     return s2;
   };
   // tile n sits in buffer n % 2; (st, stn) = starts of tiles n, n + 1
@@ -389,55 +457,6 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p) {
 // query rows of 64 B (32 keys), 8-byte unit u of row r at slot
 // u ^ ((r >> 2) & 7), conflict-free both for the row writes of phase 1 and
 // the transposed reads of phase 2.
-constexpr int kPBlock = 2048;
-
-// Lane id read afresh, so that offsets derived from it are recomputed where
-// they are used instead of being held in registers across the loop.
-__device__ __forceinline__ int fresh_lane() {
-  int l;
-  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
-  return l;
-}
-
-// Transposed reads (ds_read_b64_tr_b16) of the 16 rows r16.. (r16 a multiple
-// of 16) of a 64-row tile: lane 16 G + 4 e + q reads the 8 bytes of row
-// r16 + 8 hf + 4 (G >> 1) + e at channels 32 dtg + 16 (G & 1) + 4 q, so that
-// lane l holds channel 32 dtg + (l & 31) of rows r16 + 4 g + {0..3} (hf = 0)
-// and r16 + 8 + 4 g + {0..3} (hf = 1): an A operand over those 16 rows.
-// The row's swizzle depends on row & 15 only, so the lane's byte offset is
-// the same for every r16.
-__device__ __forceinline__ uint32_t trans_off(int lane, int hf, int dtg) {
-  const int G = lane >> 4, e4 = (lane >> 2) & 3, q4 = lane & 3;
-  const int row = 8 * hf + 4 * (G >> 1) + e4;
-  const int lc = 4 * dtg + 2 * (G & 1) + (q4 >> 1);
-  return (uint32_t)(row * kRowBytes + swz(row, lc) * 16 + (q4 & 1) * 8);
-}
-__device__ __forceinline__ u32x2 tr_read(const uint8_t* p) {
-  const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p);
-  return __builtin_bit_cast(u32x2, v);
-}
-__device__ __forceinline__ bf16x8 tr_pair(const uint8_t* p0, const uint8_t* p1) {
-  const u32x2 a = tr_read(p0), b = tr_read(p1);
-  const u32x4 f = {a[0], a[1], b[0], b[1]};
-  return as_bf16x8(f);
-}
-
-// P and dS: byte offset of the 8-byte unit u (keys 4u..4u+3 of key half kh)
-// of query row `row` (0..63).
-__device__ __forceinline__ int p_off(int kh, int row, int u) {
-  const int qq = row & 31;
-  return (kh + 2 * (row >> 5)) * kPBlock + qq * 64 + 8 * (u ^ ((qq >> 2) & 7));
-}
-// The same transposed read from a P / dS buffer: lane l gets key
-// 32 kh + (l & 31) of the rows r16 + 8 hf + 4 g + {0..3} (a B operand in the
-// k order of trans_off).  Offset for r16 with bit 4 = b4, before adding
-// (r16 >> 5) * 2 kPBlock + b4 * 16 * 64.
-__device__ __forceinline__ uint32_t ptr_off(int lane, int hf, int b4, int kh) {
-  const int G = lane >> 4, e4 = (lane >> 2) & 3, q4 = lane & 3;
-  const int qq = 16 * b4 + 8 * hf + 4 * (G >> 1) + e4;
-  return (uint32_t)(p_off(kh, qq, 4 * (G & 1) + q4) - b4 * 16 * 64);
-}
-
 __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p) {
   __shared__ __attribute__((aligned(1024))) uint8_t qb0[kTileBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t qb1[kTileBytes];
