@@ -81,6 +81,9 @@ def parse_args():
     ap.add_argument("--causal", choices=["on", "off"], default="on",
                     help="also time the causal-window variant (auto-regressive generation in "
                          "chunks of 3 latent frames, full history) on the same layer")
+    ap.add_argument("--bwd", choices=["on", "off"], default="on",
+                    help="also time the backward of the sparse branch (dQ, dK, dV) on the "
+                         "bf16 layer's inputs, output and LSE with a synthetic upstream dO")
     ap.add_argument("--copy-calib", action="store_true",
                     help="also time a plain 1 GiB device copy (HBM counter calibration)")
     return ap.parse_args()
@@ -223,6 +226,50 @@ def bench_causal(args, sa, W, dev, wl, q, k, v):
                      "frac": round(tf / PEAK_BF16_TFLOPS, 4), "traffic": None,
                      "flops_per_launch": flops,
                      "note": "flops of the selected blocks; masked pairs counted"},
+    }
+
+
+def bench_bwd(args, sa, dev, wl, q, k, v, o, lse, idx, cnt):
+    """Backward of the sparse branch at the layer's shape and lists: the
+    forward's O and LSE, a seeded normal upstream gradient.  One call runs
+    D = rowsum(dO o O), the transposed selection bitmap, the dQ kernel (S, dP
+    and dQ products per query tile) and the dK/dV kernel (S, dP, dV and dK
+    products per key tile): 7 products of the forward's 2-product size.  The
+    algorithmic count is 5 products (S, dP, dV, dK, dQ: 2.5x the forward)."""
+    B, H, N, d, block = wl.batch, wl.heads, wl.seqlen, wl.head_dim, wl.block
+    g = torch.Generator(device=dev).manual_seed(11)
+    do = torch.randn(q.shape, generator=g, device=dev).to(torch.bfloat16)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    desc = sa.make_desc(q, k, v, o, block=block)
+    ws = torch.empty(sa.sparse_attn_workspace_size(desc, sa.SA_OP_BWD, idx.shape[-1]),
+                     dtype=torch.uint8, device=dev)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+
+    def step(e=None):
+        if e:
+            e[0].record()
+        sa.sparse_attn_bwd(q, k, v, o, do, lse, idx, cnt, block=block, dq=dq, dk=dk, dv=dv, ws=ws)
+        if e:
+            e[1].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    for s_ in range(args.steps):
+        step(ev[s_])
+    torch.cuda.synchronize()
+    ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    fwd_flops = selected_flops(cnt.cpu().numpy(), idx.cpu().numpy(), N, block, d)
+    alg = fwd_flops * 5 // 2
+    tf = alg / (ms * 1e-3) / 1e12
+    return {
+        "ms_per_call": round(ms, 4),
+        "executed_tflops": round(fwd_flops * 7 / 2 / (ms * 1e-3) / 1e12, 2),
+        "roofline": {"kernel": "bwd (dot, bitmap, dq, dkdv)", "bound": "mfma",
+                     "achieved": round(tf, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tf / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "flops_per_launch": alg,
+                     "note": "algorithmic flops: 2.5x the forward's over the selected blocks"},
     }
 
 
@@ -478,6 +525,8 @@ def main():
         out["fp8"] = bench_fp8(args, sa, W, dev)
     if args.causal == "on":
         out["causal"] = bench_causal(args, sa, W, dev, wl, q, kk, v)
+    if args.bwd == "on":
+        out["backward"] = bench_bwd(args, sa, dev, wl, q, kk, v, o, lse, idx, cnt)
     if args.linear == "on":
         out["linear_w8a8"] = bench_linear(args, sa, W, dev)
 

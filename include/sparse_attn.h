@@ -239,8 +239,8 @@ int sparse_attn_comp_out(const sparse_attn_desc* desc, int32_t rank, const void*
 
 /*
  * Backward of the sparse branch (the gradients that the sparse model's
- * training needs, paper §4 Stage 1): for the lists idx/cnt that the forward
- * used, and its output o and log-sum-exp lse, with P = softmax(tau Q K_U^T)
+ * training needs, paper §2 and the Stage-1 warm-up of §4.4): for the lists
+ * idx/cnt that the forward used, and its output o and log-sum-exp lse, with P = softmax(tau Q K_U^T)
  * over each query block's selected keys U:
  *   dV_U += P^T dO,  dS = P o (dO V_U^T - D),  D = rowsum(dO o O),
  *   dQ = tau dS K_U,  dK_U += tau dS^T Q.

@@ -6,8 +6,8 @@ The forward (paper §2 Eq. comp-sparse, §3: exact softmax attention over the
 key blocks each query block selected) is, per query block i with key set U_i
 (the union of its selected blocks' tokens),
     Z = tau Q_i K_U^T,  P = softmax_rows(Z),  O_i = P V_U.
-Its gradients for an upstream dO (the training that needs them is §4, the
-Stage-1 warm-up of the sparse model):
+Its gradients for an upstream dO (the training that needs them: §2 "Training
+sparse attention" and the Stage-1 warm-up of §4.4):
     dV_U += P^T dO_i
     dP    = dO_i V_U^T
     dZ    = P o (dP - D 1^T),  D = rowsum(dO_i o O_i) = rowsum(P o dP)

@@ -1,5 +1,6 @@
 // Backward pass of the block-sparse attention forward (the sparse branch of
-// paper §2 Eq. comp-sparse; its gradients serve the Stage-1 training of §4),
+// paper §2 Eq. comp-sparse; its gradients serve the training of the sparse
+// model, §2 "Training sparse attention" and the Stage-1 warm-up of §4.4),
 // bf16 operands, gfx950.  Per query block i with key set U_i (its selected
 // blocks), with P = softmax(tau Q_i K_U^T) rebuilt from the forward's LSE:
 //   dV_U += P^T dO_i,  dP = dO_i V_U^T,  dS = P o (dP - D_i),
@@ -16,14 +17,14 @@
 //      dQ^T += K^T dS^T (8 MFMAs, K^T by transposed LDS reads);
 //    the two key halves are summed at the end;
 //  * bwd_dkdv_kernel: one workgroup per 64-key tile walks the query blocks
-//    that selected its key block (set bits of its bitmap row, ascending);
-//    wave (kh, qh): keys 32 kh.., query rows 32 qh.. of each query tile:
-//      S = Q K^T, dP = dO V^T, P and dS per lane,
-//      dV^T += dO^T P, dK^T += Q^T dS (dO^T, Q^T by transposed reads);
-//    the two query halves are summed at the end.
+//    that selected its key block (set bits of its bitmap row, ascending) in
+//    two phases per query tile: S^T and dP^T per (key half, query half),
+//    P and dS through LDS, then dV^T += dO^T P and dK^T += Q^T dS per (key
+//    half, channel half) over the whole tile.
 // Every product is a bf16 32x32x16 MFMA with fp32 accumulation; P and dS
-// enter the second products as bf16.  Tiles are staged into LDS by plain
-// loads (rows past the sequence end read as zero) between barriers.
+// enter the second products as bf16.  Q, K, V, dO tiles move global -> LDS
+// by buffer_load ... lds (rows past the sequence end read as zero), double
+// buffered, two workgroups per CU; no floating-point atomics anywhere.
 #include "common.h"
 #include "launch.h"
 
@@ -44,51 +45,10 @@ __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast
 // 16-byte chunk c of tile row r sits at slot c ^ (r & 15).
 __device__ __forceinline__ int swz(int row, int c) { return c ^ (row & 15); }
 
-// Stage rows [r0, r0 + 64) of a bf16 [rows][128] matrix (row stride `st`
-// elements) into a 16 KB LDS tile; rows at or past `n` read as zero.
-__device__ __forceinline__ void stage_tile(uint8_t* dst, const uint16_t* src, int64_t st, int r0,
-                                           int n) {
-#pragma unroll
-  for (int m = 0; m < 4; ++m) {
-    const int e = threadIdx.x + kThreads * m, row = e >> 4, c = e & 15;
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (r0 + row < n) v = ld16(src + (int64_t)(r0 + row) * st + 8 * c);
-    *reinterpret_cast<u32x4*>(dst + row * kRowBytes + swz(row, c) * 16) = v;
-  }
-}
-
 // Row fragment (A or B operand of a 32x32x16 product over the 128 channels):
 // tile row `row`, channels 16 ks + 8 g .. +7.
 __device__ __forceinline__ bf16x8 row_frag(const uint8_t* t, int row, int ks, int g) {
   return as_bf16x8(*reinterpret_cast<const u32x4*>(t + row * kRowBytes + swz(row, 2 * ks + g) * 16));
-}
-
-// Transposed fragments (A operand, rows = the 128 channels, k = 32 tile rows
-// starting at `r_half`): lane 16G + 4e + q reads the 8 bytes of row
-// r_half + 16 cs + 8 hf + 4 (G >> 1) + e at channels 32 dt + 16 (G & 1) + 4 q;
-// lane l then holds channel 32 dt + (l & 31) of rows r_half + 16 cs + 8 hf +
-// 4 g + {0..3}, the order in which the MFMA output leaves its 16 values.
-__device__ __forceinline__ void trans_frags(const uint8_t* t, int r_half, int lane,
-                                            u32x4 (&f)[8]) {
-  const int G = lane >> 4, e4 = (lane >> 2) & 3, q4 = lane & 3;
-  const int row0 = r_half + 4 * (G >> 1) + e4;
-#pragma unroll
-  for (int dt = 0; dt < 4; ++dt) {
-    const int lc = 4 * dt + 2 * (G & 1) + (q4 >> 1);
-    const int half = (q4 & 1) * 8;
-#pragma unroll
-    for (int cs = 0; cs < 2; ++cs)
-#pragma unroll
-      for (int hf = 0; hf < 2; ++hf) {
-        const int row = row0 + 16 * cs + 8 * hf;
-        const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) i16x4*)(t + row * kRowBytes + swz(row, lc) * 16 +
-                                                       half));
-        const u32x2 w = __builtin_bit_cast(u32x2, v);
-        f[2 * dt + cs][2 * hf] = w[0];
-        f[2 * dt + cs][2 * hf + 1] = w[1];
-      }
-  }
 }
 
 // A lane's 16 values packed as the bf16 B operand of the two 16-deep
@@ -195,10 +155,6 @@ __device__ __forceinline__ void wait_vm0() {
 __device__ __forceinline__ void wait_vm8() {
   __builtin_amdgcn_sched_barrier(0);
   __builtin_amdgcn_s_waitcnt(0x0F78);
-}
-__device__ __forceinline__ void wait_vm9() {
-  __builtin_amdgcn_sched_barrier(0);
-  __builtin_amdgcn_s_waitcnt(0x0F79);
 }
 __device__ __forceinline__ void wait_lgkm0() {
   __builtin_amdgcn_sched_barrier(0);
