@@ -42,6 +42,13 @@ typedef const __attribute__((address_space(4))) uint32_t* bits_ptr;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+// Two floats to packed bf16, round to nearest even (one v_cvt_pk_bf16_f32).
+typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2_t;
+__device__ __forceinline__ uint32_t cvt_bf16x2(float lo, float hi) {
+  const bf16x2_t t = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, t);
+}
+
 // 16-byte chunk c of tile row r sits at slot c ^ (r & 15).
 __device__ __forceinline__ int swz(int row, int c) { return c ^ (row & 15); }
 
@@ -58,7 +65,7 @@ __device__ __forceinline__ void pack_b(const float (&x)[16], bf16x8 (&pk)[2]) {
   for (int cs = 0; cs < 2; ++cs) {
     u32x4 w;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(x[8 * cs + 2 * e], x[8 * cs + 2 * e + 1]);
+    for (int e = 0; e < 4; ++e) w[e] = cvt_bf16x2(x[8 * cs + 2 * e], x[8 * cs + 2 * e + 1]);
     pk[cs] = __builtin_bit_cast(bf16x8, w);
   }
 }
@@ -390,8 +397,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
         for (int r = 0; r < 4; ++r)
           x[r] = p.tau * (acc[dt][4 * jq + r] + mrg[(dt * 16 + 4 * jq + r) * kWave + lane]);
         u32x2 w;
-        w[0] = pack_bf16x2(x[0], x[1]);
-        w[1] = pack_bf16x2(x[2], x[3]);
+        w[0] = cvt_bf16x2(x[0], x[1]);
+        w[1] = cvt_bf16x2(x[2], x[3]);
         *reinterpret_cast<u32x2*>(out + dt * 32 + 8 * jq + 4 * g) = w;
       }
   }
@@ -532,10 +539,10 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p) {
         }
         const int off = p_off(kh, qrow, 2 * i + g1);
         u32x2 wp, wd;
-        wp[0] = pack_bf16x2(pv[0], pv[1]);
-        wp[1] = pack_bf16x2(pv[2], pv[3]);
-        wd[0] = pack_bf16x2(dv[0], dv[1]);
-        wd[1] = pack_bf16x2(dv[2], dv[3]);
+        wp[0] = cvt_bf16x2(pv[0], pv[1]);
+        wp[1] = cvt_bf16x2(pv[2], pv[3]);
+        wd[0] = cvt_bf16x2(dv[0], dv[1]);
+        wd[1] = cvt_bf16x2(dv[2], dv[3]);
         *reinterpret_cast<u32x2*>(pbuf + off) = wp;
         *reinterpret_cast<u32x2*>(sbuf + off) = wd;
       }
@@ -612,10 +619,10 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p) {
       for (int jq = 0; jq < 4; ++jq) {
         const int c = dt * 32 + 8 * jq + 4 * g;
         u32x2 wk, wv;
-        wk[0] = pack_bf16x2(p.tau * acck[dt][4 * jq], p.tau * acck[dt][4 * jq + 1]);
-        wk[1] = pack_bf16x2(p.tau * acck[dt][4 * jq + 2], p.tau * acck[dt][4 * jq + 3]);
-        wv[0] = pack_bf16x2(accv[dt][4 * jq], accv[dt][4 * jq + 1]);
-        wv[1] = pack_bf16x2(accv[dt][4 * jq + 2], accv[dt][4 * jq + 3]);
+        wk[0] = cvt_bf16x2(p.tau * acck[dt][4 * jq], p.tau * acck[dt][4 * jq + 1]);
+        wk[1] = cvt_bf16x2(p.tau * acck[dt][4 * jq + 2], p.tau * acck[dt][4 * jq + 3]);
+        wv[0] = cvt_bf16x2(accv[dt][4 * jq], accv[dt][4 * jq + 1]);
+        wv[1] = cvt_bf16x2(accv[dt][4 * jq + 2], accv[dt][4 * jq + 3]);
         *reinterpret_cast<u32x2*>(ok + c) = wk;
         *reinterpret_cast<u32x2*>(ov + c) = wv;
       }
