@@ -236,15 +236,14 @@ __device__ __forceinline__ uint32_t ptr_off(int lane, int hf, int b4, int kh) {
 }
 
 // ---- dQ -------------------------------------------------------------------
-// Two workgroups per CU (80 KB of LDS each): the dO tile stays in LDS, K and
-// V tiles are double-buffered, and the copies of tile n + 2 are issued once
-// every wave is done with tile n.
+// Two workgroups per CU (64 KB of LDS each): the Q and dO fragments of the
+// wave's query rows are held in registers, K and V tiles are double-buffered,
+// and the copies of tile n + 2 are issued once every wave is done with tile n.
 __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
   __shared__ __attribute__((aligned(1024))) uint8_t kb0[kTileBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t kb1[kTileBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t vb0[kTileBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t vb1[kTileBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t db[kTileBytes];
 
   const int bh = blockIdx.x / p.ntiles;
   const int qt = blockIdx.x - bh * p.ntiles;
@@ -279,7 +278,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
   }
   const float c2 = p.tau * kLog2e;
 
-  // prologue: Q through kb1, dO into db, tiles 0 and 1 of the list
+  // prologue: Q through kb1, dO through vb1, tiles 0 and 1 of the list
   int nx = 0;
   int s0 = list_tile(list, nx, total, spb, p.block, p.nb, p.N, &nx);
   int s1 = list_tile(list, nx, total, spb, p.block, p.nb, p.N, &nx);
@@ -287,18 +286,23 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
     const auto qr = make_rsrc(p.q + b * p.qs.b + h * p.qs.h, (uint32_t)(p.N - 1) * qst + 256u);
     const auto dr = make_rsrc(p.dout + b * p.os.b + h * p.os.h, (uint32_t)(p.N - 1) * ost + 256u);
     dma_tile(kb1, qr, tile_dma(qst), (uint32_t)q0 * qst);
-    dma_tile(db, dr, tile_dma(ost), (uint32_t)q0 * ost);
+    dma_tile(vb1, dr, tile_dma(ost), (uint32_t)q0 * ost);
   }
   dma_tile(kb0, kr, kd, (uint32_t)s0 * kst);
   dma_tile(vb0, vr, vd, (uint32_t)s0 * vst);
   wait_vm8();  // Q and dO landed (this wave's rows)
   barrier_keep_loads();
-  bf16x8 qf[8];
-  const int drow = rh * 32 + l32;  // this lane's dO row in db
+  bf16x8 qf[8], df[8];  // B operands: this lane's query row of Q and dO
+  {
+    const int qrow = rh * 32 + l32;
 #pragma unroll
-  for (int ks = 0; ks < 8; ++ks) qf[ks] = row_frag(kb1, drow, ks, g);
+    for (int ks = 0; ks < 8; ++ks) {
+      qf[ks] = row_frag(kb1, qrow, ks, g);
+      df[ks] = row_frag(vb1, qrow, ks, g);
+    }
+  }
   wait_lgkm0();
-  barrier_keep_loads();  // kb1 free
+  barrier_keep_loads();  // kb1, vb1 free
   dma_tile(kb1, kr, kd, (uint32_t)s1 * kst);
   dma_tile(vb1, vr, vd, (uint32_t)s1 * vst);
 
@@ -317,15 +321,14 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) s[r] = dp[r] = 0.f;
     const int ln = fresh_lane(), g1 = ln >> 5;
-    const int krow = kh * 32 + (ln & 31), drow1 = rh * 32 + (ln & 31);
+    const int krow = kh * 32 + (ln & 31);
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks)
       s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(kt, krow, ks, g1), qf[ks], s, 0, 0, 0);
     __builtin_amdgcn_sched_barrier(0);  // bound the fragments in flight
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks)
-      dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(vt, krow, ks, g1),
-                                                   row_frag(db, drow1, ks, g1), dp, 0, 0, 0);
+      dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(vt, krow, ks, g1), df[ks], dp, 0, 0, 0);
     // lane: query qtok, keys st + kh*32 + 8(r>>2) + 4g + (r&3)
     float ds[16];
 #pragma unroll
@@ -337,18 +340,30 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
     bf16x8 pk[2];
     pack_b(ds, pk);
     __builtin_amdgcn_sched_barrier(0);
-    // K^T fragments: channels 32 dt.., keys 32 kh + 16 cs..
-    bf16x8 kf[4][2];
+    // dQ^T += K^T dS^T, the K^T fragments (channels 32 dt.., keys 32 kh +
+    // 16 cs..) read and used in two halves to bound the registers they hold
     {
       const int ln2 = fresh_lane();
 #pragma unroll
-      for (int dt = 0; dt < 4; ++dt) {
-        const uint32_t o0 = trans_off(ln2, 0, dt), o1 = trans_off(ln2, 1, dt);
+      for (int hd = 0; hd < 2; ++hd) {
+        bf16x8 kf[2][2];
 #pragma unroll
-        for (int cs = 0; cs < 2; ++cs) {
-          const uint8_t* base = kt + (kh * 32 + 16 * cs) * kRowBytes;
-          kf[dt][cs] = tr_pair(base + o0, base + o1);
+        for (int d2 = 0; d2 < 2; ++d2) {
+          const int dt = 2 * hd + d2;
+          const uint32_t o0 = trans_off(ln2, 0, dt), o1 = trans_off(ln2, 1, dt);
+#pragma unroll
+          for (int cs = 0; cs < 2; ++cs) {
+            const uint8_t* base = kt + (kh * 32 + 16 * cs) * kRowBytes;
+            kf[d2][cs] = tr_pair(base + o0, base + o1);
+          }
         }
+#pragma unroll
+        for (int d2 = 0; d2 < 2; ++d2)
+#pragma unroll
+          for (int cs = 0; cs < 2; ++cs)
+            acc[2 * hd + d2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[d2][cs], pk[cs],
+                                                                       acc[2 * hd + d2], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
     wait_lgkm0();
@@ -356,11 +371,6 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
     const int s2 = list_tile(list, nx, total, spb, p.block, p.nb, p.N, &nx);
     dma_tile(kt, kr, kd, (uint32_t)s2 * kst);
     dma_tile(vt, vr, vd, (uint32_t)s2 * vst);
-#pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-      for (int cs = 0; cs < 2; ++cs)
-        acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[dt][cs], pk[cs], acc[dt], 0, 0, 0);
     return s2;
   };
   // tile n sits in buffer n % 2; (st, stn) = starts of tiles n, n + 1
