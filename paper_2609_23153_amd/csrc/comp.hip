@@ -16,7 +16,7 @@
 //                 waves' partials are summed through LDS in a fixed order.
 //   comp_reduce : the chunk partials of a head summed in chunk order -> C^T
 //                 (fp32, d-major: row d holds the r values of C[.][d]).
-//   comp_out    : per (head, 128 tokens) the projection P_q q_norm^T in the
+//   comp_out    : per (head, 1024 tokens, in tiles of 128) the projection P_q q_norm^T in the
 //                 layout that keeps one token per lane, silu and rotation,
 //                 O_lr^T = C^T q~^T against a bf16 hi + lo copy of C^T in LDS, then
 //                 RMSNorm, the gate and the sum with O_s, all per lane.
@@ -45,7 +45,32 @@ constexpr int kCtStride = 72;           // bf16 per C^T row in LDS (64 + 8 paddi
 typedef __attribute__((__vector_size__(4 * sizeof(short)))) short i16x4;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
-__device__ __forceinline__ float silu(float x) { return x / (1.f + __expf(-x)); }
+// silu(x) = x sigmoid(x), the reciprocal by v_rcp_f32 (1 ulp) rather than
+// a full-precision division
+__device__ __forceinline__ float silu(float x) {
+  return x * __builtin_amdgcn_rcpf(1.f + __expf(-x));
+}
+
+// Exchange words 0, 1 of lanes 32..63 with words 2, 3 of lanes 0..31
+// (v_permlane32_swap).  With lane l (< 32) holding channels c..c+7 of a row
+// and lane l + 32 channels c+8..c+15, afterwards lane l holds c..c+3 and
+// c+8..c+11, lane l + 32 holds c+4..c+7 and c+12..c+15; applied again it
+// restores the contiguous halves.
+__device__ __forceinline__ u32x4 swap_quads(u32x4 w) {
+  const auto s0 = __builtin_amdgcn_permlane32_swap(w[0], w[2], false, false);
+  const auto s1 = __builtin_amdgcn_permlane32_swap(w[1], w[3], false, false);
+  const u32x4 r = {s0[0], s1[0], s0[1], s1[1]};
+  return r;
+}
+
+// Lane id read afresh: LDS addresses derived from it inside a loop are not
+// loop invariants, so the compiler cannot hoist every read of data that
+// stays in LDS out of the loop (and hold it all in registers).
+__device__ __forceinline__ int fresh_lane() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
 
 // 16-byte-chunk swizzle of the V rows in LDS (as in the forward): conflict-free
 // for the transpose reads of 4 rows x 4 chunks per half-wave.
@@ -267,33 +292,53 @@ __device__ __forceinline__ int ct_pos(int r) {
   return (r & ~15) + 4 * nq + (q & 3);
 }
 
-__global__ __launch_bounds__(256) void comp_out_kernel(OutArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t ct[kHeadDim * kCtStride];   // C^T hi
-  __shared__ __attribute__((aligned(16))) uint16_t ctl[kHeadDim * kCtStride];  // C^T lo
-  const int bh = blockIdx.x, tile = blockIdx.y;
-  const int b = bh / a.H, h = bh - b * a.H;
-  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
-  const int g = lane >> 5, l32 = lane & 31;
-
-  // every per-token load is issued first, so its latency overlaps the staging of C^T
-  const int tok = tile * kSub + 32 * wave + l32;  // this lane's token
-  const bool live = tok < a.N;
-  const int tokc = live ? tok : a.N - 1;  // clamped for the loads
-  // q_norm as B operand: column token, k = channels 16 ks + 8 g .. +7
+// Per-token inputs of one 128-token tile for this lane's token `tok`
+// (clamped into the sequence): q_norm as the B operand of the projection
+// (channels 16 ks + 8 g .. +7), O_s (after swap_quads: channels
+// 32 dt + 8 j + 4 g + {0..3} in osw[dt][j]) and the gate.
+__device__ __forceinline__ void load_tok(const OutArgs& a, int b, int h, int tokc, int g,
+                                         bf16x8 (&qf)[8], u32x2 (&osw)[4][4], float& gv) {
   const uint16_t* qrow = a.qn + b * a.qns.b + h * a.qns.h + (int64_t)tokc * a.qns.n;
-  bf16x8 qf[8];
 #pragma unroll
   for (int ks = 0; ks < 8; ++ks) qf[ks] = as_bf16x8(ld16(qrow + 16 * ks + 8 * g));
-
-  // O_s of this lane's token: channels 32 dt + 8 j + 4 g + {0..3}
+  // 16-byte loads of channels 32 dt + 16 jp + 8 g .. +7, regrouped across
+  // the lane pair by swap_quads (done by the caller once the loads landed)
   const uint16_t* osrow = a.os + b * a.oss.b + h * a.oss.h + (int64_t)tokc * a.oss.n;
-  u32x2 osw[4][4];
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      osw[dt][j] = *reinterpret_cast<const u32x2*>(osrow + 32 * dt + 8 * j + 4 * g);
-  const float gv = a.gate[b * a.gs.b + h * a.gs.h + (int64_t)tokc * a.gs.n];
+    for (int jp = 0; jp < 2; ++jp) {
+      const u32x4 w = ld16(osrow + 32 * dt + 16 * jp + 8 * g);
+      osw[dt][2 * jp] = u32x2{w[0], w[1]};
+      osw[dt][2 * jp + 1] = u32x2{w[2], w[3]};
+    }
+  gv = a.gate[b * a.gs.b + h * a.gs.h + (int64_t)tokc * a.gs.n];
+}
+
+// One workgroup per (head, kOutTiles tiles of 128 tokens): C^T (as bf16 hi +
+// lo) and P_q are staged into LDS once, then the tiles stream through, the
+// next tile's per-token loads issued before the current tile is computed.
+constexpr int kOutTiles = 8;
+
+__global__ __launch_bounds__(256, 2) void comp_out_kernel(OutArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t ct[kHeadDim * kCtStride];   // C^T hi
+  __shared__ __attribute__((aligned(16))) uint16_t ctl[kHeadDim * kCtStride];  // C^T lo
+  // P_q rows (r, 256 bytes each); 16-byte chunk c of row r at slot c ^ (r & 15)
+  __shared__ __attribute__((aligned(16))) uint8_t pqs[kRank * kHeadDim * 2];
+  __shared__ __attribute__((aligned(16))) float gam_s[kHeadDim];  // RMSNorm weight (1 if none)
+  const int bh = blockIdx.x;
+  const int b = bh / a.H, h = bh - b * a.H;
+  const int ntiles = (a.N + kSub - 1) / kSub;
+  const int tile0 = blockIdx.y * kOutTiles, tile_end = min(tile0 + kOutTiles, ntiles);
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  const int g = lane >> 5, l32 = lane & 31;
+
+  // the first tile's per-token loads are issued first, so their latency
+  // overlaps the staging of C^T and P_q
+  bf16x8 qf[8];
+  u32x2 osw[4][4];
+  float gv;
+  load_tok(a, b, h, min(tile0 * kSub + 32 * wave + l32, a.N - 1), g, qf, osw, gv);
 
   // C^T of this head as bf16 hi + lo into LDS: thread t converts quads of
   // 4 consecutive r (16-byte loads) and stores each as 8 bytes at its
@@ -317,114 +362,155 @@ __global__ __launch_bounds__(256) void comp_out_kernel(OutArgs a) {
     *reinterpret_cast<u32x2*>(ct + d * kCtStride + ct_pos(r)) = hw;
     *reinterpret_cast<u32x2*>(ctl + d * kCtStride + ct_pos(r)) = lw;
   }
-
-
-  // P_q as A operand of P_q q_norm^T: row r = l32 + 32 rb, k = d 16 ks + 8 g .. +7
-  bf16x8 pqf[2][8];
+  // P_q of this head: thread t moves 16-byte chunks e = t + 256 m
   const uint16_t* pqh = a.pq + (int64_t)h * kStateElems;
 #pragma unroll
-  for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-    for (int ks = 0; ks < 8; ++ks)
-      pqf[rb][ks] = as_bf16x8(ld16(pqh + (l32 + 32 * rb) * kHeadDim + 16 * ks + 8 * g));
-
-  // projection: lane holds token `tok`, rank indices 32 rb + 8 j + 4 g + rr
-  f32x16 pr[2];
-#pragma unroll
-  for (int rb = 0; rb < 2; ++rb) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) pr[rb][r] = 0.f;
-#pragma unroll
-    for (int ks = 0; ks < 8; ++ks)
-      pr[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pqf[rb][ks], qf[ks], pr[rb], 0, 0, 0);
+  for (int m = 0; m < kRank * 16 / 256; ++m) {
+    const int e = t + 256 * m, r = e >> 4, c = e & 15;
+    *reinterpret_cast<u32x4*>(pqs + r * 256 + ((c ^ (r & 15)) << 4)) = ld16(pqh + 8 * e);
   }
-  // silu and rotation: pairs (rr = 0, 1) and (2, 3) of each (rb, j) are pairs
-  // m = 16 rb + 4 j + 2 g + {0, 1}, whose (cos, sin) are 16 contiguous bytes
-  const float* rope_t = a.rope + (int64_t)tokc * (kRank / 2) * 2;
-  // q~^T as B operand split hi + lo, k-step s: indices 16 s + 4 g + rr, 16 s + 8 + 4 g + rr
-  bf16x8 qt[4], ql[4];
+  if (t < kHeadDim) gam_s[t] = a.gamma ? a.gamma[(int64_t)h * kHeadDim + t] : 1.f;
+  __syncthreads();  // C^T, P_q and the RMSNorm weight are in LDS
+
+  for (int tile = tile0; tile < tile_end; ++tile) {
+    const int tok = tile * kSub + 32 * wave + l32;  // this lane's token
+    // (cos, sin) of this lane's pairs: pairs (rr = 0, 1) and (2, 3) of each
+    // (rb, j) are pairs m = 16 rb + 4 j + 2 g + {0, 1}, 16 contiguous bytes.
+    // Issued before the next tile's loads, so waiting for them does not wait
+    // for those.
+    const float* rope_t = a.rope + (int64_t)min(tok, a.N - 1) * (kRank / 2) * 2;
+    f32x4 csn[2][4];
 #pragma unroll
-  for (int rb = 0; rb < 2; ++rb)
+    for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const f32x4 csn = *reinterpret_cast<const f32x4*>(rope_t + 2 * (16 * rb + 4 * j + 2 * g));
-      float y[4];
+      for (int j = 0; j < 4; ++j)
+        csn[rb][j] = *reinterpret_cast<const f32x4*>(rope_t + 2 * (16 * rb + 4 * j + 2 * g));
+    // the next tile's per-token inputs (on the last tile the current one's
+    // again, L2-resident: the loads are issued on every path, so the waits
+    // the compiler places for the loads above count them)
+    bf16x8 qn[8];
+    u32x2 on[4][4];
+    float gn;
+    load_tok(a, b, h, min(tile + 1 < tile_end ? tok + kSub : tok, a.N - 1), g, qn, on, gn);
+
+    // projection P_q q_norm^T: lane holds token `tok`, rank indices
+    // 32 rb + 8 j + 4 g + rr (P_q rows r = l32 + 32 rb as the A operand)
+    const int ln = fresh_lane(), fl32 = ln & 31, fg = ln >> 5;
+    f32x16 pr[2];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) y[u] = silu(pr[rb][4 * j + u]);
-      const float r0 = fmaf(y[0], csn[0], -y[1] * csn[1]);
-      const float r1 = fmaf(y[0], csn[1], y[1] * csn[0]);
-      const float r2 = fmaf(y[2], csn[2], -y[3] * csn[3]);
-      const float r3 = fmaf(y[2], csn[3], y[3] * csn[2]);
-      const int s = 2 * rb + (j >> 1), half = 4 * (j & 1);
-      const float rv[4] = {r0, r1, r2, r3};
+    for (int rb = 0; rb < 2; ++rb) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const __bf16 hi = (__bf16)rv[u];
-        qt[s][half + u] = hi;
-        ql[s][half + u] = (__bf16)(rv[u] - (float)hi);
+      for (int r = 0; r < 16; ++r) pr[rb][r] = 0.f;
+      const int prow = fl32 + 32 * rb;
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) {
+        const bf16x8 pf = as_bf16x8(*reinterpret_cast<const u32x4*>(
+            pqs + prow * 256 + (((2 * ks + fg) ^ (prow & 15)) << 4)));
+        pr[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pf, qf[ks], pr[rb], 0, 0, 0);
       }
     }
-  __syncthreads();  // C^T is in LDS
+    // silu and rotation; q~^T as B operand split hi + lo, k-step s: indices 16 s + 4 g + rr, 16 s + 8 + 4 g + rr
+    bf16x8 qt[4], ql[4];
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const f32x4 cj = csn[rb][j];
+        float y[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) y[u] = silu(pr[rb][4 * j + u]);
+        const float r0 = fmaf(y[0], cj[0], -y[1] * cj[1]);
+        const float r1 = fmaf(y[0], cj[1], y[1] * cj[0]);
+        const float r2 = fmaf(y[2], cj[2], -y[3] * cj[3]);
+        const float r3 = fmaf(y[2], cj[3], y[3] * cj[2]);
+        const int s2 = 2 * rb + (j >> 1), half = 4 * (j & 1);
+        const float rv[4] = {r0, r1, r2, r3};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const __bf16 hi = (__bf16)rv[u];
+          qt[s2][half + u] = hi;
+          ql[s2][half + u] = (__bf16)(rv[u] - (float)hi);
+        }
+      }
 
-  // O_lr^T = C^T q~^T: lane holds token `tok`, channels 32 dt + 8 j + 4 g + rr
-  f32x16 y[4];
+    // O_lr^T = C^T q~^T: lane holds token `tok`, channels 32 dt + 8 j + 4 g + rr
+    f32x16 y[4];
 #pragma unroll
-  for (int dt = 0; dt < 4; ++dt) {
+    for (int dt = 0; dt < 4; ++dt) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) y[dt][r] = 0.f;
-    const uint16_t* crow = ct + (32 * dt + l32) * kCtStride;
-    const uint16_t* clrow = ctl + (32 * dt + l32) * kCtStride;
+      for (int r = 0; r < 16; ++r) y[dt][r] = 0.f;
+      const uint16_t* crow = ct + (32 * dt + fl32) * kCtStride;
+      const uint16_t* clrow = ctl + (32 * dt + fl32) * kCtStride;
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const bf16x8 cf = as_bf16x8(*reinterpret_cast<const u32x4*>(crow + 16 * s + 8 * g));
-      const bf16x8 cl = as_bf16x8(*reinterpret_cast<const u32x4*>(clrow + 16 * s + 8 * g));
-      y[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cl, qt[s], y[dt], 0, 0, 0);
-      y[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cf, ql[s], y[dt], 0, 0, 0);
-      y[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cf, qt[s], y[dt], 0, 0, 0);
-    }
-  }
-
-  // RMSNorm of O_lr and rms of O_s over the 128 channels (64 here, 64 in lane l ^ 32)
-  float osv[4][16];
-  float ss_y = 0.f, ss_o = 0.f;
-#pragma unroll
-  for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const u32x2 w = osw[dt][j];
-      osv[dt][4 * j + 0] = bf16_lo(w[0]);
-      osv[dt][4 * j + 1] = bf16_hi(w[0]);
-      osv[dt][4 * j + 2] = bf16_lo(w[1]);
-      osv[dt][4 * j + 3] = bf16_hi(w[1]);
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        ss_y = fmaf(y[dt][4 * j + u], y[dt][4 * j + u], ss_y);
-        ss_o = fmaf(osv[dt][4 * j + u], osv[dt][4 * j + u], ss_o);
+      for (int s2 = 0; s2 < 4; ++s2) {
+        const bf16x8 cf = as_bf16x8(*reinterpret_cast<const u32x4*>(crow + 16 * s2 + 8 * fg));
+        const bf16x8 cl = as_bf16x8(*reinterpret_cast<const u32x4*>(clrow + 16 * s2 + 8 * fg));
+        y[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cl, qt[s2], y[dt], 0, 0, 0);
+        y[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cf, ql[s2], y[dt], 0, 0, 0);
+        y[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cf, qt[s2], y[dt], 0, 0, 0);
       }
     }
-  ss_y += __shfl_xor(ss_y, 32, kWave);
-  ss_o += __shfl_xor(ss_o, 32, kWave);
-  const float rstd = 1.f / sqrtf(ss_y * (1.f / kHeadDim) + a.eps);
-  const float rms_o = sqrtf(ss_o * (1.f / kHeadDim));
-  const float coef = gv * rms_o * rstd;
-  if (!live) return;
-  uint16_t* orow = a.o + b * a.oss.b + h * a.oss.h + (int64_t)tok * a.oss.n;
-  const float* gam = a.gamma ? a.gamma + (int64_t)h * kHeadDim : nullptr;
+
+    // RMSNorm of O_lr and rms of O_s over the 128 channels (64 here, 64 in lane l ^ 32)
 #pragma unroll
-  for (int dt = 0; dt < 4; ++dt)
+    for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int d0 = 32 * dt + 8 * j + 4 * g;
-      f32x4 gm = {1.f, 1.f, 1.f, 1.f};
-      if (gam) gm = *reinterpret_cast<const f32x4*>(gam + d0);
-      float x[4];
+      for (int jp = 0; jp < 2; ++jp) {
+        const u32x4 w = swap_quads(u32x4{osw[dt][2 * jp][0], osw[dt][2 * jp][1],
+                                         osw[dt][2 * jp + 1][0], osw[dt][2 * jp + 1][1]});
+        osw[dt][2 * jp] = u32x2{w[0], w[1]};
+        osw[dt][2 * jp + 1] = u32x2{w[2], w[3]};
+      }
+    float ss_y = 0.f, ss_o = 0.f;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) x[u] = fmaf(coef * y[dt][4 * j + u], gm[u], osv[dt][4 * j + u]);
-      u32x2 w;
-      w[0] = pack_bf16x2(x[0], x[1]);
-      w[1] = pack_bf16x2(x[2], x[3]);
-      *reinterpret_cast<u32x2*>(orow + d0) = w;
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const u32x2 w = osw[dt][j];
+        const float o4[4] = {bf16_lo(w[0]), bf16_hi(w[0]), bf16_lo(w[1]), bf16_hi(w[1])};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          ss_y = fmaf(y[dt][4 * j + u], y[dt][4 * j + u], ss_y);
+          ss_o = fmaf(o4[u], o4[u], ss_o);
+        }
+      }
+    ss_y += __shfl_xor(ss_y, 32, kWave);
+    ss_o += __shfl_xor(ss_o, 32, kWave);
+    const float rstd = 1.f / sqrtf(ss_y * (1.f / kHeadDim) + a.eps);
+    const float rms_o = sqrtf(ss_o * (1.f / kHeadDim));
+    const float coef = gv * rms_o * rstd;
+    if (tok < a.N) {
+      uint16_t* orow = a.o + b * a.oss.b + h * a.oss.h + (int64_t)tok * a.oss.n;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int jp = 0; jp < 2; ++jp) {
+          u32x4 wo;
+#pragma unroll
+          for (int jj = 0; jj < 2; ++jj) {
+            const int j = 2 * jp + jj;
+            const int d0 = 32 * dt + 8 * j + 4 * g;
+            const f32x4 gm = *reinterpret_cast<const f32x4*>(gam_s + d0);
+            const u32x2 w = osw[dt][j];
+            const float o4[4] = {bf16_lo(w[0]), bf16_hi(w[0]), bf16_lo(w[1]), bf16_hi(w[1])};
+            float x[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) x[u] = fmaf(coef * y[dt][4 * j + u], gm[u], o4[u]);
+            wo[2 * jj] = pack_bf16x2(x[0], x[1]);
+            wo[2 * jj + 1] = pack_bf16x2(x[2], x[3]);
+          }
+          // back to 8 contiguous channels per lane: 32 dt + 16 jp + 8 g ..
+          st16(orow + 32 * dt + 16 * jp + 8 * g, swap_quads(wo));
+        }
     }
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) qf[ks] = qn[ks];
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) osw[dt][j] = on[dt][j];
+    gv = gn;
+  }
 }
 
 }  // namespace
@@ -471,7 +557,8 @@ hipError_t launch_comp_out(const Shape& s, const CompOutIn& in, hipStream_t stre
   a.H = s.H;
   a.N = s.N;
   a.eps = in.eps;
-  comp_out_kernel<<<dim3(s.B * s.H, (s.N + kSub - 1) / kSub), 256, 0, stream>>>(a);
+  const int ntiles = (s.N + kSub - 1) / kSub;
+  comp_out_kernel<<<dim3(s.B * s.H, (ntiles + kOutTiles - 1) / kOutTiles), 256, 0, stream>>>(a);
   return hipGetLastError();
 }
 
