@@ -86,10 +86,25 @@ struct StateArgs {
   int H, N, chunks;
 };
 
+// K~ sub-tile in LDS: [token][r] bf16, 128-byte rows; 16-byte chunk c of
+// row t at slot c ^ kt_swz(t): conflict-free for the transposed reads
+// (4 rows x 4 chunks per half-wave: rows t, t + 2 land in opposite halves of
+// the row) and 2-way for the row writes (32 rows, one chunk each).
+__device__ __forceinline__ int kt_swz(int t) { return (((t >> 1) & 1) << 2) | ((t >> 2) & 3); }
+
 // partial element e = ((dt*2 + nb)*16 + reg)*64 + lane holds C^T[d][r] with
 // r = 32 nb + (lane & 31), d = 32 dt + 8 (reg >> 2) + 4 (lane >> 5) + (reg & 3).
-__global__ __launch_bounds__(256) void comp_state_kernel(StateArgs a) {
-  __shared__ __attribute__((aligned(16))) uint8_t vt[kSub * kVRow];
+//
+// Per 128-token sub-tile: wave w projects its 32 tokens (K~^T = P_k k_norm^T,
+// lane = token, so a rotation pair sits in one lane), applies silu and the
+// rotation and writes K~ as bf16 hi + lo to LDS; after a barrier wave w
+// accumulates the 32 rows d = 32 w .. of C^T = V^T K~ over all 128 tokens.
+__global__ __launch_bounds__(256, 2) void comp_state_kernel(StateArgs a) {
+  __shared__ __attribute__((aligned(16))) uint8_t vt[kSub * kVRow];        // V rows (swz_v)
+  __shared__ __attribute__((aligned(16))) uint8_t kth[kSub * kRank * 2];   // K~ hi
+  __shared__ __attribute__((aligned(16))) uint8_t ktl[kSub * kRank * 2];   // K~ lo
+  // P_k rows (r, 256 bytes each); 16-byte chunk c of row r at slot c ^ (r & 15)
+  __shared__ __attribute__((aligned(16))) uint8_t pks[kRank * kHeadDim * 2];
   const int bh = blockIdx.x, chunk = blockIdx.y;  // heads vary fastest: rope rows shared in L2
   const int b = bh / a.H, h = bh - b * a.H;
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
@@ -101,156 +116,163 @@ __global__ __launch_bounds__(256) void comp_state_kernel(StateArgs a) {
   const auto vr = make_rsrc(a.v + b * a.vs.b + h * a.vs.h, (uint32_t)(a.N - 1) * vst + 256u);
   const auto rr = make_rsrc(a.rope, (uint32_t)a.N * kRopeBytes);
 
-  // P_k as B operand of k_norm P_k^T: column r = l32 + 32 nb, k = d 16 ks + 8 g .. +7
-  bf16x8 pkf[2][8];
-  const uint16_t* pkh = a.pk + (int64_t)h * kStateElems;
-#pragma unroll
-  for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-    for (int ks = 0; ks < 8; ++ks)
-      pkf[nb][ks] = as_bf16x8(ld16(pkh + (l32 + 32 * nb) * kHeadDim + 16 * ks + 8 * g));
-
-  f32x16 acc[4][2];  // C^T: [dt][nb]
-#pragma unroll
-  for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[dt][nb][r] = 0.f;
-
-  // transpose-read addresses of V^T (rows = this wave's tokens, as the
-  // forward's keys): lane 16G + 4e + q reads the 8-byte chunk of token
-  // 32 wave + 16 s + 8 hf + 4 (G>>1) + e at channels 32 dt + 16 (G&1) + 4 q
-  const int G = lane >> 4, e4 = (lane >> 2) & 3, q4 = lane & 3;
-  const int vrow0 = 32 * wave + 4 * (G >> 1) + e4;
-
-  // k_norm as A operand (token tw + l32, channels 16 ks + 8 g .. +7) and the
-  // sub-tile's V rows (thread t moves chunks e = t + 256 m -> row e/16, chunk
-  // e%16); the next sub-tile's are fetched while the current one is computed
+  // k_norm as B operand of P_k k_norm^T (token tw + l32, channels
+  // 16 ks + 8 g .. +7) and the sub-tile's V rows (thread t moves chunks
+  // e = t + 256 m -> row e/16, chunk e%16); rows past N read zero
   bf16x8 kf[8];
   u32x4 vrow[8];
-  auto load_kv = [&](int t0) {
+  auto load_kv = [&](int t0, bf16x8 (&kd)[8], u32x4 (&vd)[8]) {
     const int tw = t0 + 32 * wave;
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks)
-      kf[ks] = as_bf16x8(buf_ld16(kr, (uint32_t)(tw + l32) * kst + (16 * ks + 8 * g) * 2));
+      kd[ks] = as_bf16x8(buf_ld16(kr, (uint32_t)(tw + l32) * kst + (16 * ks + 8 * g) * 2));
 #pragma unroll
     for (int m = 0; m < 8; ++m) {
       const int e = t + 256 * m, row = e >> 4, ch = e & 15;
-      vrow[m] = buf_ld16(vr, (uint32_t)(t0 + row) * vst + ch * 16);
+      vd[m] = buf_ld16(vr, (uint32_t)(t0 + row) * vst + ch * 16);
     }
   };
-  if (t_begin < t_end) load_kv(t_begin);
+  if (t_begin < t_end) load_kv(t_begin, kf, vrow);
+
+  // P_k of this head into LDS
+  const uint16_t* pkh = a.pk + (int64_t)h * kStateElems;
+#pragma unroll
+  for (int m = 0; m < kRank * 16 / 256; ++m) {
+    const int e = t + 256 * m, r = e >> 4, c = e & 15;
+    *reinterpret_cast<u32x4*>(pks + r * 256 + ((c ^ (r & 15)) << 4)) = ld16(pkh + 8 * e);
+  }
+
+  f32x16 acc[2];  // C^T rows d = 32 wave .., columns r = 32 nb + l32
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[nb][r] = 0.f;
 
   for (int t0 = t_begin; t0 < t_end; t0 += kSub) {
-    const int tw = t0 + 32 * wave;
-    // (cos, sin) of this lane's pair m = (32 nb + l32) / 2 at its 16 tokens
-    // tw + 8 j + 4 g + rr
-    float2 cs[2][16];
+    const int tok = t0 + 32 * wave + l32;  // this lane's token in the projection
+    // (cos, sin) of this lane's pairs m = 16 nb + 4 j + 2 g + {0, 1} at its
+    // token: 16 contiguous bytes per (nb, j); issued before the next
+    // sub-tile's loads, so waiting for them does not wait for those
+    f32x4 csn[2][4];
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int tok = tw + 8 * (i >> 2) + 4 * g + (i & 3);
-        const uint32_t off = (uint32_t)tok * kRopeBytes + (uint32_t)((32 * nb + l32) >> 1) * 8u;
-        const u32x2 w = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rr, off, 0, 0));
-        cs[nb][i] = make_float2(__uint_as_float(w[0]), __uint_as_float(w[1]));
-      }
-    __syncthreads();  // every wave is done reading the previous sub-tile's V
+      for (int j = 0; j < 4; ++j)
+        csn[nb][j] = __builtin_bit_cast(
+            f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                       rr, (uint32_t)tok * kRopeBytes + (uint32_t)(16 * nb + 4 * j + 2 * g) * 8u,
+                       0, 0));
+    __syncthreads();  // every wave is done reading the previous sub-tile's V and K~
 #pragma unroll
     for (int m = 0; m < 8; ++m) {
       const int e = t + 256 * m, row = e >> 4, ch = e & 15;
       *reinterpret_cast<u32x4*>(vt + row * kVRow + swz_v(row, ch) * 16) = vrow[m];
     }
-
-    // projection k_norm P_k^T: lane holds column r = 32 nb + l32 of tokens
-    // 8 j + 4 g + rr (register 4 j + rr)
+    // projection K~^T = P_k k_norm^T: lane holds token `tok`, rank indices
+    // 32 nb + 8 j + 4 g + rr (register 4 j + rr)
+    const int ln = fresh_lane(), fl32 = ln & 31, fg = ln >> 5;
     f32x16 pr[2];
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) pr[nb][r] = 0.f;
+      const int prow = fl32 + 32 * nb;
 #pragma unroll
-      for (int ks = 0; ks < 8; ++ks)
-        pr[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], pkf[nb][ks], pr[nb], 0, 0, 0);
-    }
-    if (t0 + kSub < t_end) load_kv(t0 + kSub);  // prefetch the next sub-tile
-    // silu, then the rotation of pair (r & ~1, r | 1): the partner column is
-    // the neighbouring lane (DPP quad_perm 1,0,3,2)
-    const bool odd = (l32 & 1) != 0;
-    // K~ as B operand, split hi + lo: [nb][k-step s], tokens 16 s + 4 g + rr, 16 s + 8 + 4 g + rr
-    bf16x8 kt[2][2], kl[2][2];
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-      float y[16];
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float x = silu(pr[nb][i]);
-        const float o = __int_as_float(
-            __builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xF, 0xF, false));
-        const float c = cs[nb][i].x, s = cs[nb][i].y;
-        // even r: (x, o) = (a, b) -> a c - b s;  odd r: (o, x) = (a, b) -> a s + b c
-        y[i] = odd ? fmaf(o, s, x * c) : fmaf(x, c, -o * s);
+      for (int ks = 0; ks < 8; ++ks) {
+        const bf16x8 pf = as_bf16x8(*reinterpret_cast<const u32x4*>(
+            pks + prow * 256 + (((2 * ks + fg) ^ (prow & 15)) << 4)));
+        pr[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pf, kf[ks], pr[nb], 0, 0, 0);
       }
-#pragma unroll
-      for (int sk = 0; sk < 2; ++sk)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const __bf16 hi = (__bf16)y[8 * sk + e];
-          kt[nb][sk][e] = hi;
-          kl[nb][sk][e] = (__bf16)(y[8 * sk + e] - (float)hi);
-        }
     }
-    __syncthreads();  // the sub-tile's V rows are in LDS
+    // the next sub-tile's k_norm and V (on the last sub-tile the current
+    // one's again: the loads are issued on every path)
+    load_kv(t0 + kSub < t_end ? t0 + kSub : t0, kf, vrow);
+    // silu, rotation of pairs (rr 0, 1) and (2, 3), K~ split hi + lo into LDS
+    const int trow = 32 * wave + fl32;  // this lane's token row in the sub-tile
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const f32x4 cj = csn[nb][j];
+        float y[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) y[u] = silu(pr[nb][4 * j + u]);
+        const float rv[4] = {fmaf(y[0], cj[0], -y[1] * cj[1]), fmaf(y[0], cj[1], y[1] * cj[0]),
+                             fmaf(y[2], cj[2], -y[3] * cj[3]), fmaf(y[2], cj[3], y[3] * cj[2])};
+        u32x2 wh, wl;
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const __bf16 h0 = (__bf16)rv[2 * u], h1 = (__bf16)rv[2 * u + 1];
+          const __bf16 l0 = (__bf16)(rv[2 * u] - (float)h0);
+          const __bf16 l1 = (__bf16)(rv[2 * u + 1] - (float)h1);
+          wh[u] = (uint32_t)__builtin_bit_cast(uint16_t, h0) |
+                  ((uint32_t)__builtin_bit_cast(uint16_t, h1) << 16);
+          wl[u] = (uint32_t)__builtin_bit_cast(uint16_t, l0) |
+                  ((uint32_t)__builtin_bit_cast(uint16_t, l1) << 16);
+        }
+        // r = 32 nb + 8 j + 4 g .. +3: bytes 64 nb + 16 j + 8 g of the row
+        const int c = 4 * nb + j;
+        const int off = trow * 128 + ((c ^ kt_swz(trow)) << 4) + 8 * fg;
+        *reinterpret_cast<u32x2*>(kth + off) = wh;
+        *reinterpret_cast<u32x2*>(ktl + off) = wl;
+      }
+    __syncthreads();  // the sub-tile's V rows and K~ are in LDS
 
-    // C^T += V^T K~ over this wave's 32 tokens
+    // C^T[32 wave ..][.] += V^T K~ over the 128 tokens: A = V^T (channels
+    // 32 wave + l32) and B = K~ (columns r), both by transposed reads whose
+    // lane 16 G + 4 e + q reads row (token) r16 + 8 hf + 4 (G >> 1) + e
+    {
+      const int ln2 = fresh_lane();
+      const int G = ln2 >> 4, e4 = (ln2 >> 2) & 3, q4 = ln2 & 3;
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt) {
-      const int lc = 4 * dt + 2 * (G & 1) + (q4 >> 1);
-      const int half = (q4 & 1) * 8;
-#pragma unroll
-      for (int sk = 0; sk < 2; ++sk) {
-        u32x4 vv;
+      for (int r16 = 0; r16 < kSub; r16 += 16) {
+        u32x4 va, kh2[2], kl2[2];
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf) {
-          const int row = vrow0 + 16 * sk + 8 * hf;
-          const i16x4 tr = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (__attribute__((address_space(3))) i16x4*)(vt + row * kVRow + swz_v(row, lc) * 16 +
-                                                         half));
-          const u32x2 tw2 = __builtin_bit_cast(u32x2, tr);
-          vv[2 * hf] = tw2[0];
-          vv[2 * hf + 1] = tw2[1];
+          const int row = r16 + 8 * hf + 4 * (G >> 1) + e4;
+          // V^T: channels 32 wave + 16 (G & 1) + 4 q .. +3
+          const int lc = 4 * wave + 2 * (G & 1) + (q4 >> 1);
+          const u32x2 v2 = __builtin_bit_cast(
+              u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                         (__attribute__((address_space(3))) i16x4*)(vt + row * kVRow +
+                                                                    swz_v(row, lc) * 16 +
+                                                                    (q4 & 1) * 8)));
+          va[2 * hf] = v2[0];
+          va[2 * hf + 1] = v2[1];
+#pragma unroll
+          for (int nb = 0; nb < 2; ++nb) {
+            // K~: r = 32 nb + 16 (G & 1) + 4 q .. +3 -> chunk 4 nb + 2 (G & 1) + q / 2
+            const int c = 4 * nb + 2 * (G & 1) + (q4 >> 1);
+            const int off = row * 128 + ((c ^ kt_swz(row)) << 4) + (q4 & 1) * 8;
+            const u32x2 h2 = __builtin_bit_cast(
+                u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                           (__attribute__((address_space(3))) i16x4*)(kth + off)));
+            const u32x2 l2 = __builtin_bit_cast(
+                u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                           (__attribute__((address_space(3))) i16x4*)(ktl + off)));
+            kh2[nb][2 * hf] = h2[0];
+            kh2[nb][2 * hf + 1] = h2[1];
+            kl2[nb][2 * hf] = l2[0];
+            kl2[nb][2 * hf + 1] = l2[1];
+          }
         }
 #pragma unroll
         for (int nb = 0; nb < 2; ++nb) {
-          acc[dt][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv), kt[nb][sk],
-                                                                acc[dt][nb], 0, 0, 0);
-          acc[dt][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv), kl[nb][sk],
-                                                                acc[dt][nb], 0, 0, 0);
+          acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(va), as_bf16x8(kh2[nb]),
+                                                            acc[nb], 0, 0, 0);
+          acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(va), as_bf16x8(kl2[nb]),
+                                                            acc[nb], 0, 0, 0);
         }
       }
     }
   }
 
-  // sum the four waves' partials in wave order through LDS, then store
-  float* red = reinterpret_cast<float*>(vt);  // 32 KB = kStateElems floats
-  for (int w = 0; w < 4; ++w) {
-    __syncthreads();
-    if (wave == w) {
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int e = ((dt * 2 + nb) * 16 + r) * 64 + lane;
-            red[e] = w == 0 ? acc[dt][nb][r] : red[e] + acc[dt][nb][r];
-          }
-    }
-  }
-  __syncthreads();
+  // this wave's rows of the chunk's partial C^T
   float* out = a.partial + ((int64_t)bh * a.chunks + chunk) * kStateElems;
-  for (int e = t; e < kStateElems; e += 256) out[e] = red[e];
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) out[((wave * 2 + nb) * 16 + r) * 64 + lane] = acc[nb][r];
 }
 
 // C^T[bh][d][r] = sum over chunks (in chunk order) of the partials; each
