@@ -7,19 +7,19 @@
 //
 // R_r rotates consecutive coordinate pairs (2m, 2m+1) by angles given as a
 // (cos, sin) table per token and pair.  Three launches:
-//   comp_state  : per (head, chunk of 2048 tokens) the projection k_norm P_k^T
-//                 on the matrix cores in the layout that keeps tokens inside a
-//                 lane (so k~ is directly the B operand of the next product),
-//                 silu and the rotation (the partner coordinate of a pair sits
-//                 in the neighbouring lane: one DPP swap), then
-//                 C^T += V^T K~ with V^T read transposed from LDS; the four
-//                 waves' partials are summed through LDS in a fixed order.
+//   comp_state  : per (head, chunk of 1024 tokens, in sub-tiles of 128) the
+//                 projection P_k k_norm^T on the matrix cores in the layout
+//                 that keeps one token per lane (both coordinates of a
+//                 rotation pair in one lane), silu and the rotation, K~ to
+//                 LDS, then C^T += V^T K~ with V^T and K~ read transposed
+//                 from LDS, wave w owning rows 32 w .. of C^T.
 //   comp_reduce : the chunk partials of a head summed in chunk order -> C^T
 //                 (fp32, d-major: row d holds the r values of C[.][d]).
-//   comp_out    : per (head, 1024 tokens, in tiles of 128) the projection P_q q_norm^T in the
-//                 layout that keeps one token per lane, silu and rotation,
-//                 O_lr^T = C^T q~^T against a bf16 hi + lo copy of C^T in LDS, then
-//                 RMSNorm, the gate and the sum with O_s, all per lane.
+//   comp_out    : per (head, 1024 tokens, in tiles of 128) the projection
+//                 P_q q_norm^T in the same one-token-per-lane layout, silu
+//                 and rotation, O_lr^T = C^T q~^T against a bf16 hi + lo copy
+//                 of C^T in LDS, then RMSNorm, the gate and the sum with O_s,
+//                 all per lane.
 // The projections multiply the bf16 inputs exactly (fp32 accumulation).  In
 // the two low-rank products the fp32 operands k~, q~ and C are each split as
 // hi + lo with hi = bf16(x) and lo = bf16(x - hi) (about 16 significant
