@@ -84,6 +84,10 @@ def parse_args():
     ap.add_argument("--bwd", choices=["on", "off"], default="on",
                     help="also time the backward of the sparse branch (dQ, dK, dV) on the "
                          "bf16 layer's inputs, output and LSE with a synthetic upstream dO")
+    ap.add_argument("--sweep", choices=["on", "off"], default="off",
+                    help="also time select + schedule + fwd over the sparsity sweep (blocks 64 "
+                         "and 128 x keep 3/10/25/100%%) on the locality inputs at the 14B-720P "
+                         "shape")
     ap.add_argument("--copy-calib", action="store_true",
                     help="also time a plain 1 GiB device copy (HBM counter calibration)")
     return ap.parse_args()
@@ -271,6 +275,63 @@ def bench_bwd(args, sa, dev, wl, q, k, v, o, lse, idx, cnt):
                      "flops_per_launch": alg,
                      "note": "algorithmic flops: 2.5x the forward's over the selected blocks"},
     }
+
+
+def bench_sweep(args, sa, W, dev):
+    """select + schedule + fwd (bf16, row top-k) at every point of the
+    sparsity sweep on the locality inputs (40 heads x 75,600 tokens): ms per
+    call and the forward's actual TFLOP/s over the selected blocks."""
+    wl = W.WORKLOADS["sweep"]
+    B, H, N, d = wl.batch, wl.heads, wl.seqlen, wl.head_dim
+    q, k, v = (t.to(dev) for t in W.make_inputs(wl))
+    o = torch.empty_like(q)
+    lse = torch.empty(B, H, N, dtype=torch.float32, device=dev)
+    dense = 4 * B * H * N * N * d
+    steps, warm = min(args.steps, 5), min(args.warmup, 2)
+    points = []
+    for block, keep in wl.sweep:
+        nb = -(-N // block)
+        kk = sa.sparse_attn_keep_count(keep, nb)
+        idx = torch.empty(B, H, nb, kk, dtype=torch.int32, device=dev)
+        cnt = torch.empty(B, H, nb, dtype=torch.int32, device=dev)
+        desc = sa.make_desc(q, k, v, o, block=block)
+        ws_sel = torch.empty(sa.sparse_attn_workspace_size(desc, sa.SA_OP_SELECT, kk),
+                             dtype=torch.uint8, device=dev)
+        ws_sch = torch.empty(sa.sparse_attn_workspace_size(desc, sa.SA_OP_SCHEDULE, kk),
+                             dtype=torch.uint8, device=dev)
+        order = torch.empty(sa.sparse_attn_num_tiles(desc), dtype=torch.int32, device=dev)
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+
+        def step(e=None):
+            if e:
+                e[0].record()
+            sa.sparse_attn_select(q, k, kk, block=block, idx=idx, cnt=cnt, ws=ws_sel)
+            if e:
+                e[1].record()
+            sa.sparse_attn_schedule(cnt, N, kk, block=block, order=order, ws=ws_sch)
+            if e:
+                e[2].record()
+            sa.sparse_attn_fwd(q, k, v, idx, cnt, block=block, order=order, o=o, lse=lse)
+            if e:
+                e[3].record()
+
+        for _ in range(warm):
+            step()
+        torch.cuda.synchronize()
+        for s_ in range(steps):
+            step(ev[s_])
+        torch.cuda.synchronize()
+        ms = [float(np.mean([e[i].elapsed_time(e[i + 1]) for e in ev])) for i in range(3)]
+        flops = selected_flops(cnt.cpu().numpy(), idx.cpu().numpy(), N, block, d)
+        tf = flops / (ms[2] * 1e-3) / 1e12
+        points.append({"block": block, "keep": keep / 10000, "k": kk, "key_blocks": nb,
+                       "ms_per_call": {"select": round(ms[0], 4), "schedule": round(ms[1], 4),
+                                       "fwd": round(ms[2], 4)},
+                       "fwd_actual_tflops": round(tf, 2),
+                       "fwd_mfma_frac": round(tf / PEAK_BF16_TFLOPS, 4),
+                       "step_dense_equiv_tflops": round(dense / (sum(ms) * 1e-3) / 1e12, 2)})
+        del idx, cnt, ws_sel, ws_sch, order
+    return {"workload": wl.name, "generator": wl.gen, "steps": steps, "points": points}
 
 
 def bench_linear(args, sa, W, dev):
@@ -529,6 +590,8 @@ def main():
         out["backward"] = bench_bwd(args, sa, dev, wl, q, kk, v, o, lse, idx, cnt)
     if args.linear == "on":
         out["linear_w8a8"] = bench_linear(args, sa, W, dev)
+    if args.sweep == "on":
+        out["sweep"] = bench_sweep(args, sa, W, dev)
 
     if args.copy_calib:
         a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
