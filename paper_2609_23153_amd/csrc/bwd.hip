@@ -305,6 +305,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
   barrier_keep_loads();  // kb1, vb1 free
   dma_tile(kb1, kr, kd, (uint32_t)s1 * kst);
   dma_tile(vb1, vr, vd, (uint32_t)s1 * vst);
+  wait_vm8();  // tile 0 landed (this wave's rows); tile 1 may still fly
+  barrier_keep_loads();
 
   f32x16 acc[4];
 #pragma unroll
@@ -312,11 +314,10 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[dt][r] = 0.f;
 
-  // One tile from buffers (kt, vt); once every wave is done reading them they
+  // One tile from buffers (kt, vt), which every wave sees landed; once every
+  // wave is done reading them and the next tile has landed (one barrier) they
   // receive the tile two ahead, whose start is returned.
   auto step = [&](uint8_t* kt, uint8_t* vt, int st) {
-    wait_vm8();  // this tile landed; the next one may still fly
-    barrier_keep_loads();
     f32x16 s, dp;
 #pragma unroll
     for (int r = 0; r < 16; ++r) s[r] = dp[r] = 0.f;
@@ -367,7 +368,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
       }
     }
     wait_lgkm0();
-    barrier_keep_loads();  // every wave is done reading kt / vt
+    wait_vm0();            // this wave's rows of the next tile landed
+    barrier_keep_loads();  // every wave is done reading kt / vt; the next tile is whole
     const int s2 = list_tile(list, nx, total, spb, p.block, p.nb, p.N, &nx);
     dma_tile(kt, kr, kd, (uint32_t)s2 * kst);
     dma_tile(vt, vr, vd, (uint32_t)s2 * vst);
@@ -508,6 +510,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p) {
   dma_tile(ob0, dr, od, (uint32_t)s0 * ost);
   dma_tile(qb1, qr, qd, (uint32_t)s1 * qst);
   dma_tile(ob1, dr, od, (uint32_t)s1 * ost);
+  wait_vm8();  // tile 0 landed (this wave's rows); tile 1 may still fly
+  barrier_keep_loads();
 
   const float c2 = p.tau * kLog2e;
   f32x16 acck[2], accv[2];
@@ -516,12 +520,11 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) acck[dt][r] = accv[dt][r] = 0.f;
 
-  // One query tile from (qt, ot) starting at st; stn starts the next one.
-  // Once every wave is done reading (qt, ot) they receive the tile two
-  // ahead, whose start is returned.
+  // One query tile from (qt, ot) starting at st, which every wave sees
+  // landed; stn starts the next one.  Once every wave is done reading
+  // (qt, ot) and the next tile has landed (one barrier) they receive the tile
+  // two ahead, whose start is returned.
   auto step = [&](uint8_t* qt, uint8_t* ot, int st, int stn) {
-    wait_vm8();  // this tile landed; the next one may still fly
-    barrier_keep_loads();
     float lsen, ddn;
     load_vec(stn, lsen, ddn);  // waited for before the next copies are issued
     // phase 1: lane holds query row 32 hh + l32, keys 32 kh + 8(r>>2) + 4g + (r&3)
@@ -596,10 +599,12 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p) {
 #undef TFRAG
     }
     wait_lgkm0();
-    barrier_keep_loads();  // every wave is done reading qt / ot / pbuf / sbuf
     // the loads of the next tile's LSE and D complete here, before the copies
-    // (a wait for them after the copies would wait for the copies too)
+    // (a wait for them after the copies would wait for the copies too), and
+    // so does this wave's share of the next tile
     asm volatile("" : "+v"(lsen), "+v"(ddn));
+    wait_vm0();
+    barrier_keep_loads();  // every wave is done reading qt / ot / pbuf / sbuf; next tile whole
     const int s2 = next_start();
     dma_tile(qt, qr, qd, (uint32_t)s2 * qst);
     dma_tile(ot, dr, od, (uint32_t)s2 * ost);
