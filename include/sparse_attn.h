@@ -245,16 +245,19 @@ int sparse_attn_comp_out(const sparse_attn_desc* desc, int32_t rank, const void*
  *   dV_U += P^T dO,  dS = P o (dO V_U^T - D),  D = rowsum(dO o O),
  *   dQ = tau dS K_U,  dK_U += tau dS^T Q.
  * Every key is covered: keys that no query block selected get dK = dV = 0,
- * query blocks with an empty list get dQ = 0.  Products are bf16 MFMA with
- * fp32 accumulation; P and dS enter the second products as bf16; outputs are
- * bf16.  Deterministic (no floating-point atomics).
+ * query blocks with an empty list get dQ = 0.  With a causal window in the
+ * descriptor (causal_chunk > 0) P is 0 outside each query's allowed keys, as
+ * in the forward, and rows left without allowed keys (LSE = -inf) contribute
+ * nothing.  Products are bf16 MFMA with fp32 accumulation; P and dS enter the
+ * second products as bf16; outputs are bf16.  Deterministic (no
+ * floating-point atomics).
  *  q, k, v, o, d_o   bf16 via desc strides (d_o laid out like o)
  *  lse               fp32 [B][H][L] natural log, as the forward wrote it
  *  idx, cnt, kmax    the forward's lists
  *  dq, dk, dv        bf16 out, laid out like q, k, v (desc strides)
  *  ws                ws_bytes >= sparse_attn_workspace_size(SA_OP_BWD)
- * Errors: SA_ERR_UNSUPPORTED with a causal window; SA_ERR_INVALID_ARG for
- * null or misaligned pointers and bad strides; SA_ERR_WORKSPACE. */
+ * Errors: SA_ERR_INVALID_ARG for null or misaligned pointers and bad
+ * strides or lists; SA_ERR_WORKSPACE. */
 int sparse_attn_bwd(const sparse_attn_desc* desc, const void* q, const void* k, const void* v,
                     const void* o, const void* d_o, const float* lse, const int32_t* idx,
                     const int32_t* cnt, int32_t kmax, void* dq, void* dk, void* dv, void* ws,

@@ -393,9 +393,11 @@ def sparse_attn_linear_w8a8(xq, sx, wq, sw, bias=None, y=None):
 
 # ---------------------------------------------------------------- backward
 def sparse_attn_bwd(q, k, v, o, d_o, lse, idx, cnt, block: int = 64,
-                    softmax_scale: float = 0.0, dq=None, dk=None, dv=None, ws=None):
+                    softmax_scale: float = 0.0, dq=None, dk=None, dv=None, ws=None,
+                    causal=None):
     """Gradients (dq, dk, dv) bf16 of the sparse forward for upstream d_o
-    (laid out like o), given the forward's lists, output and lse."""
+    (laid out like o), given the forward's lists, output and lse (and its
+    causal window (chunk, window), if any)."""
     kmax = idx.shape[-1]
     _dense(idx, "idx"), _dense(cnt, "cnt"), _dense(lse, "lse", torch.float32)
     if tuple(d_o.stride()) != tuple(o.stride()):
@@ -406,7 +408,7 @@ def sparse_attn_bwd(q, k, v, o, d_o, lse, idx, cnt, block: int = 64,
     for name, a, ref in (("dq", dq, q), ("dk", dk, k), ("dv", dv, v)):
         if tuple(a.stride()) != tuple(ref.stride()):
             raise ValueError(f"{name} must be laid out like its input")
-    desc = make_desc(q, k, v, o, block=block, softmax_scale=softmax_scale)
+    desc = make_desc(q, k, v, o, block=block, softmax_scale=softmax_scale, causal=causal)
     if ws is None:
         ws = _workspace(desc, SA_OP_BWD, kmax, q.device)
     st = library().sparse_attn_bwd(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(o),

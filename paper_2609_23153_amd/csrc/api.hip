@@ -277,7 +277,6 @@ int sparse_attn_bwd(const sparse_attn_desc* desc, const void* q, const void* k, 
   Shape s;
   int st = check_desc(desc, &s);
   if (st != SA_OK) return st;
-  if (s.causal_chunk > 0) return SA_ERR_UNSUPPORTED;  // no causal window in the backward
   if (!q || !k || !v || !o || !d_o || !lse || !dq || !dk || !dv || !ws) return SA_ERR_INVALID_ARG;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(d_o) ||
       !aligned16(dq) || !aligned16(dk) || !aligned16(dv))

@@ -87,6 +87,7 @@ struct BwdParams {
   Strides qs, ks, vs, os;
   int kmax, H, N, block, nb, nw, ntiles;
   float tau;
+  Shape cs;  // causal window (chunk 0: none) and N
 };
 
 // ---- D = rowsum(dO o O) -------------------------------------------------
@@ -268,6 +269,13 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
   // this lane's query row: its LSE (log2 units) and D, loaded and waited for
   // before any copy is issued (a later wait for them would drain the copies)
   const int qtok = q0 + rh * 32 + l32;
+  // allowed keys [key_lo, key_hi) of the lane's query (causal window and
+  // sequence end); a key tile needs the per-score mask unless it lies in
+  // every row's range: [lo of the tile's last row, hi of its first)
+  const int key_lo = causal_lo(p.cs, min(qtok, p.N - 1));
+  const int key_hi = causal_hi(p.cs, min(qtok, p.N - 1));
+  const int tile_lo = causal_lo(p.cs, min(q0 + kTile - 1, p.N - 1));
+  const int tile_hi = causal_hi(p.cs, q0);
   float lse2, dq_d;
   {
     const int qc = min(qtok, p.N - 1);
@@ -330,14 +338,22 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks)
       dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(vt, krow, ks, g1), df[ks], dp, 0, 0, 0);
-    // lane: query qtok, keys st + kh*32 + 8(r>>2) + 4g + (r&3)
-    float ds[16];
+    // lane: query qtok, keys st + kh*32 + 8(r>>2) + 4g + (r&3); P = 0 for
+    // keys outside the query's range, set after the exponential (a row
+    // without any allowed key has LSE = -inf and meets only tiles that take
+    // the mask, where all its keys are masked)
+    float pr[16], ds[16];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int key = st + kh * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
-      const float pr = key < p.N ? __builtin_amdgcn_exp2f(fmaf(s[r], c2, -lse2)) : 0.f;
-      ds[r] = pr * (dp[r] - dq_d);
+    for (int r = 0; r < 16; ++r) pr[r] = __builtin_amdgcn_exp2f(fmaf(s[r], c2, -lse2));
+    if (st + kTile > tile_hi || st < tile_lo) {  // wave-uniform
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = st + kh * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
+        if (key < key_lo || key >= key_hi) pr[r] = 0.f;
+      }
     }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) ds[r] = pr[r] * (dp[r] - dq_d);
     bf16x8 pk[2];
     pack_b(ds, pk);
     __builtin_amdgcn_sched_barrier(0);
@@ -534,6 +550,12 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p) {
     {
       const int ln = fresh_lane(), g1 = ln >> 5;
       const int qrow = hh * 32 + (ln & 31);
+      // the query's allowed keys; the key tile needs the per-score mask
+      // unless it lies in every row's range of this query tile
+      const int qc = min(st + qrow, p.N - 1);
+      const int key_lo = causal_lo(p.cs, qc), key_hi = causal_hi(p.cs, qc);
+      const bool edge = k0 + kTile > causal_hi(p.cs, st) ||
+                        k0 < causal_lo(p.cs, min(st + kTile - 1, p.N - 1));
 #pragma unroll
       for (int ks = 0; ks < 8; ++ks)
         s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], row_frag(qt, qrow, ks, g1), s, 0, 0, 0);
@@ -542,12 +564,22 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p) {
       for (int ks = 0; ks < 8; ++ks)
         dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[ks], row_frag(ot, qrow, ks, g1), dp, 0, 0,
                                                      0);
+      float pa[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) pa[r] = __builtin_amdgcn_exp2f(fmaf(s[r], c2, -lse2));
+      if (edge) {  // wave-uniform
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = k0 + kh * 32 + 8 * (r >> 2) + 4 * g1 + (r & 3);
+          if (key < key_lo || key >= key_hi) pa[r] = 0.f;
+        }
+      }
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         float pv[4], dv[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          pv[e] = __builtin_amdgcn_exp2f(fmaf(s[4 * i + e], c2, -lse2));
+          pv[e] = pa[4 * i + e];
           dv[e] = pv[e] * (dp[4 * i + e] - dd);
         }
         const int off = p_off(kh, qrow, 2 * i + g1);
@@ -677,6 +709,7 @@ hipError_t launch_bwd(const Shape& s, const BwdIn& in, void* ws, hipStream_t str
   p.nw = (s.nb + 31) / 32;
   p.ntiles = (s.N + kTile - 1) / kTile;
   p.tau = in.softmax_scale;
+  p.cs = s;
   uint8_t* w = static_cast<uint8_t*>(ws);
   p.dvec = reinterpret_cast<float*>(w);
   const size_t dbytes = ((size_t)s.B * s.H * s.N * sizeof(float) + 255) / 256 * 256;

@@ -6,7 +6,9 @@ for the second products and rounds dQ, dK, dV to bf16, each a relative
 error of at most 2^-9 per term; these average out in the sums, and the
 measured rel-L2 is a few 1e-3.  Bars per gradient and head: rel-L2 <= 1e-2
 (the forward's bf16 bar) and max |err| <= 2e-2 max |ref| (the forward's
-max-abs bar relative to the gradient's scale, which the inputs do not fix)."""
+max-abs bar relative to the gradient's scale, which the inputs do not fix).
+Under a causal window the forward and backward take the window from the
+descriptor and the oracle is its causal backward."""
 import numpy as np
 import pytest
 import torch
@@ -31,25 +33,27 @@ def _gpu():
     torch.cuda.synchronize()
 
 
-def run_bwd(q, k, v, idx, cnt, block, seed):
+def run_bwd(q, k, v, idx, cnt, block, seed, causal=None):
     g = torch.Generator().manual_seed(seed)
     do = torch.randn(q.shape, generator=g).to(torch.bfloat16)
     qd, kd, vd, dod = (t.to(DEV) for t in (q, k, v, do))
     idxd, cntd = idx.to(DEV), cnt.to(DEV)
-    o, lse = sa.sparse_attn_fwd(qd, kd, vd, idxd, cntd, block=block)
-    dq, dk, dv = sa.sparse_attn_bwd(qd, kd, vd, o, dod, lse, idxd, cntd, block=block)
+    o, lse = sa.sparse_attn_fwd(qd, kd, vd, idxd, cntd, block=block, causal=causal)
+    dq, dk, dv = sa.sparse_attn_bwd(qd, kd, vd, o, dod, lse, idxd, cntd, block=block,
+                                    causal=causal)
     torch.cuda.synchronize()
     return do, dq.cpu(), dk.cpu(), dv.cpu()
 
 
-def check_grads(q, k, v, do, idx, cnt, block, dq, dk, dv, what, heads=None):
+def check_grads(q, k, v, do, idx, cnt, block, dq, dk, dv, what, heads=None, causal=None):
     B, H = q.shape[:2]
     idx_c, cnt_c = idx.numpy(), cnt.numpy()
     for b in range(B):
         for h in (range(H) if heads is None else heads):
-            ref = O.sparse_attention_backward(widen(q[b, h]), widen(k[b, h]), widen(v[b, h]),
-                                              widen(do[b, h]), idx_c[b, h], cnt_c[b, h], block,
-                                              TAU)
+            args = (widen(q[b, h]), widen(k[b, h]), widen(v[b, h]), widen(do[b, h]),
+                    idx_c[b, h], cnt_c[b, h], block, TAU)
+            ref = (O.sparse_attention_backward(*args) if causal is None else
+                   O.sparse_attention_backward_causal(*args, *causal))
             msg = []
             for name, got, r in zip(("dq", "dk", "dv"), (dq, dk, dv), ref):
                 gg = got[b, h].to(torch.float64).numpy()
@@ -121,3 +125,62 @@ def test_bwd_full_size_one_head():
     for t in (dq, dk, dv):
         assert torch.isfinite(t.float()).all()
     check_grads(q, k, v, do, idx, cnt, wl.block, dq, dk, dv, "14B-720P", heads=[0])
+
+
+# ---- causal window ----------------------------------------------------------
+@pytest.mark.parametrize("causal", [(1024, 0), (1024, 2), (2048, 1)])
+def test_bwd_causal_tiny(causal):
+    """4 frames of 32 x 32 tokens in chunks of 1 or 2 frames, the lists from
+    the causal selection."""
+    wl = W.WORKLOADS["tiny"]
+    q, k, v = W.make_inputs(wl)
+    kk = O.keep_count(wl.keep_bp, O.block_count(wl.seqlen, wl.block))
+    idx, cnt = sa.sparse_attn_select(q.to(DEV), k.to(DEV), kk, block=wl.block, causal=causal)
+    idx, cnt = idx.cpu(), cnt.cpu()
+    do, dq, dk, dv = run_bwd(q, k, v, idx, cnt, wl.block, 4, causal=causal)
+    check_grads(q, k, v, do, idx, cnt, wl.block, dq, dk, dv, f"causal tiny {causal}",
+                causal=causal)
+
+
+@pytest.mark.parametrize("N,block,causal", [(1000, 64, (600, 1)), (1000, 128, (300, 0)),
+                                            (777, 64, (777, 0)), (3000, 64, (1000, 2))])
+def test_bwd_causal_unaligned_chunks(N, block, causal):
+    """Chunk boundaries inside blocks and a ragged last block, causal lists."""
+    g = torch.Generator().manual_seed(N + block + causal[0])
+    q, k, v = (torch.randn(1, 2, N, 128, generator=g).to(torch.bfloat16) for _ in range(3))
+    kk = O.keep_count(1500, O.block_count(N, block))
+    idx, cnt = sa.sparse_attn_select(q.to(DEV), k.to(DEV), kk, block=block, causal=causal)
+    idx, cnt = idx.cpu(), cnt.cpu()
+    do, dq, dk, dv = run_bwd(q, k, v, idx, cnt, block, 5, causal=causal)
+    check_grads(q, k, v, do, idx, cnt, block, dq, dk, dv, f"causal N={N} b={block} {causal}",
+                causal=causal)
+
+
+def test_bwd_causal_rows_without_allowed_keys():
+    """Chunk 96, window 1: query block 1 listing only key block 3 leaves all
+    its rows without allowed keys (LSE = -inf): dQ = 0 there and nothing
+    reaches dK, dV of block 3 from them."""
+    N, block, causal = 256, 64, (96, 1)
+    g = torch.Generator().manual_seed(6)
+    q, k, v = (torch.randn(1, 1, N, 128, generator=g).to(torch.bfloat16) for _ in range(3))
+    idx = torch.tensor([[[[0, -1], [3, -1], [1, 2], [2, 3]]]], dtype=torch.int32)
+    cnt = torch.tensor([[[1, 1, 2, 2]]], dtype=torch.int32)
+    do, dq, dk, dv = run_bwd(q, k, v, idx, cnt, block, 7, causal=causal)
+    assert torch.all(dq[0, 0, 64:128] == 0)
+    check_grads(q, k, v, do, idx, cnt, block, dq, dk, dv, "causal empty rows", causal=causal)
+
+
+def test_bwd_causal_full_chunk_equals_unrestricted():
+    """One chunk covering the sequence is no restriction: the gradients equal
+    the unrestricted call bit for bit."""
+    wl = W.WORKLOADS["tiny"]
+    q, k, v = (t.to(DEV) for t in W.make_inputs(wl))
+    kk = O.keep_count(wl.keep_bp, O.block_count(wl.seqlen, wl.block))
+    idx, cnt = sa.sparse_attn_select(q, k, kk)
+    o, lse = sa.sparse_attn_fwd(q, k, v, idx, cnt)
+    do = torch.randn_like(q)
+    a = sa.sparse_attn_bwd(q, k, v, o, do, lse, idx, cnt)
+    b = sa.sparse_attn_bwd(q, k, v, o, do, lse, idx, cnt, causal=(wl.seqlen, 0))
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x.view(torch.int16), y.view(torch.int16))
