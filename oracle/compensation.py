@@ -20,13 +20,19 @@ the design notes):
   * RMSNorm(y) = y / sqrt(mean(y^2) + eps) * gamma with a per-head weight
     gamma (ones when absent); rms(x) = sqrt(mean(x^2)) without epsilon.
   * The gate g_i is an input per (batch, head, token).
+  * Under a causal window (§1, auto-regressive extension; chunk and window
+    as in causal_window.py) the branch sees the same keys as the sparse
+    branch: the state of query t sums k~_j v_j^T over the keys j of chunks
+    [c(t) - W + 1, c(t)] (every earlier chunk when W = 0), so it depends only
+    on t's chunk: one state per chunk.
 """
 from __future__ import annotations
 
 import numpy as np
 
 __all__ = ["silu", "rope_rotate", "comp_features", "comp_state", "comp_lowrank",
-           "comp_combine", "compensated_output"]
+           "comp_combine", "compensated_output", "comp_state_causal", "comp_lowrank_causal",
+           "compensated_output_causal"]
 
 
 def silu(x):
@@ -82,3 +88,43 @@ def compensated_output(o_s, q_norm, k_norm, v, pq, pk, rope, gate, gamma=None, e
     """The full gated compensation of one head."""
     state = comp_state(k_norm, v, pk, rope)
     return comp_combine(o_s, comp_lowrank(q_norm, pq, rope, state, gamma, eps), gate)
+
+
+def comp_state_causal(k_norm, v, pk, rope, chunk: int, window: int):
+    """One state per query chunk c: the sum of k~_j v_j^T over the keys of
+    chunks [c - window + 1, c] (every chunk up to c if window == 0)
+    -> [nc, r, d], nc = ceil(N / chunk)."""
+    if chunk < 1 or window < 0:
+        raise ValueError("chunk >= 1 and window >= 0")
+    kt = comp_features(k_norm, pk, rope)
+    v = np.asarray(v, np.float64)
+    n = kt.shape[0]
+    nc = -(-n // chunk)
+    per = [kt[c * chunk:(c + 1) * chunk].T @ v[c * chunk:(c + 1) * chunk] for c in range(nc)]
+    out = np.zeros((nc,) + per[0].shape)
+    for c in range(nc):
+        lo = 0 if window == 0 else max(0, c - window + 1)
+        for c2 in range(lo, c + 1):
+            out[c] += per[c2]
+    return out
+
+
+def comp_lowrank_causal(q_norm, pq, rope, states, chunk: int, gamma=None, eps=1e-6):
+    """O_lr = RMSNorm(q~_t^T C_(t // chunk)) for every token -> [N, d]."""
+    qt = comp_features(q_norm, pq, rope)
+    y = np.empty((qt.shape[0], states.shape[2]))
+    for c in range(states.shape[0]):
+        y[c * chunk:(c + 1) * chunk] = qt[c * chunk:(c + 1) * chunk] @ states[c]
+    ms = np.mean(y * y, axis=1, keepdims=True)
+    out = y / np.sqrt(ms + eps)
+    if gamma is not None:
+        out = out * np.asarray(gamma, np.float64)[None, :]
+    return out
+
+
+def compensated_output_causal(o_s, q_norm, k_norm, v, pq, pk, rope, gate, chunk: int,
+                              window: int, gamma=None, eps=1e-6):
+    """The gated compensation of one head under the causal window."""
+    states = comp_state_causal(k_norm, v, pk, rope, chunk, window)
+    return comp_combine(o_s, comp_lowrank_causal(q_norm, pq, rope, states, chunk, gamma, eps),
+                        gate)

@@ -129,3 +129,63 @@ def test_rope_table_schedule():
     assert math.isclose(t[48, 1, 0], math.cos(2 * freq[1]), rel_tol=1e-6)
     assert math.isclose(t[48, 23, 1], math.sin(1 * freq[23]), rel_tol=1e-6)
     assert np.allclose(np.sum(t.astype(np.float64) ** 2, axis=-1), 1.0, atol=1e-6)
+
+
+# ---- causal window -----------------------------------------------------------
+def _causal_case(n=37, d=8, r=4, seed=21):
+    rng = np.random.default_rng(seed)
+    kn, v, qn = (rng.standard_normal((n, d)) for _ in range(3))
+    pk, pq = (rng.standard_normal((r, d)) / math.sqrt(d) for _ in range(2))
+    ang = rng.uniform(0, 2 * np.pi, (n, r // 2))
+    rope = np.stack([np.cos(ang), np.sin(ang)], axis=-1)
+    return qn, kn, v, pq, pk, rope
+
+
+@pytest.mark.parametrize("chunk,window", [(10, 0), (10, 1), (8, 2), (37, 0), (5, 3)])
+def test_causal_state_is_the_sum_over_each_querys_allowed_keys(chunk, window):
+    """Per token t, brute force over the pairs (t, j) with j in chunks
+    [c(t) - W + 1, c(t)]: the outer products summed one by one with fsum
+    equal the state the oracle keeps for t's chunk."""
+    qn, kn, v, pq, pk, rope = _causal_case()
+    n = kn.shape[0]
+    states = O.comp_state_causal(kn, v, pk, rope, chunk, window)
+    kt = O.comp_features(kn, pk, rope)
+    for t in (0, 9, 10, 19, 23, 36):
+        ct = t // chunk
+        keys = [j for j in range(n)
+                if j // chunk <= ct and (window == 0 or j // chunk > ct - window)]
+        ref = np.array([[math.fsum(kt[j, m] * v[j, c] for j in keys) for c in range(v.shape[1])]
+                        for m in range(kt.shape[1])])
+        assert np.allclose(states[ct], ref, rtol=1e-12, atol=1e-12), (t, chunk, window)
+
+
+def test_causal_one_chunk_is_the_unrestricted_branch():
+    qn, kn, v, pq, pk, rope = _causal_case(seed=22)
+    rng = np.random.default_rng(23)
+    o_s = rng.standard_normal(qn.shape)
+    gate = rng.standard_normal(qn.shape[0])
+    a = O.compensated_output_causal(o_s, qn, kn, v, pq, pk, rope, gate, qn.shape[0], 0)
+    b = O.compensated_output(o_s, qn, kn, v, pq, pk, rope, gate)
+    assert np.allclose(a, b, rtol=1e-13, atol=1e-13)
+
+
+def test_causal_window_one_is_block_diagonal():
+    """Window 1: each chunk's state is the unrestricted state of that chunk's
+    tokens alone, and the output of a chunk does not change when the other
+    chunks' keys and values change."""
+    qn, kn, v, pq, pk, rope = _causal_case(seed=24)
+    chunk = 10
+    states = O.comp_state_causal(kn, v, pk, rope, chunk, 1)
+    for c in range(states.shape[0]):
+        sl = slice(c * chunk, (c + 1) * chunk)
+        assert np.allclose(states[c], O.comp_state(kn[sl], v[sl], pk, rope[sl]),
+                           rtol=1e-13, atol=1e-13)
+    rng = np.random.default_rng(25)
+    o_s = rng.standard_normal(qn.shape)
+    gate = rng.standard_normal(qn.shape[0])
+    a = O.compensated_output_causal(o_s, qn, kn, v, pq, pk, rope, gate, chunk, 1)
+    kn2, v2 = kn.copy(), v.copy()
+    kn2[:10] += 1.0
+    v2[20:] -= 2.0
+    b = O.compensated_output_causal(o_s, qn, kn2, v2, pq, pk, rope, gate, chunk, 1)
+    assert np.array_equal(a[10:20], b[10:20])
