@@ -212,12 +212,18 @@ int sparse_attn_fwd_fp8(const sparse_attn_desc* desc, const uint8_t* q8, const f
  * backbone's 3D RoPE).  P_q, P_k are bf16 [H][r][d] row-major.  silu(x) =
  * x sigmoid(x); RMSNorm(y) = y / sqrt(mean_d y^2 + eps) * gamma; rms(x) =
  * sqrt(mean_d x^2).  Products run on bf16 operands with fp32 accumulation.
+ * Under a causal window in the descriptor (causal_chunk > 0) the branch sees
+ * the keys the sparse branch sees: query t in chunk c uses the state C_c
+ * summed over the keys of chunks [c - causal_window + 1, c] (every chunk up
+ * to c for causal_window 0), one state per chunk (paper §1, auto-regressive
+ * extension).
  */
 
-/* Low-rank state C for every (b, h), stored transposed.
+/* Low-rank state C for every (b, h) (and causal chunk), stored transposed.
  *  k_norm  bf16 [B][H][L][d] via kn_stride (the backbone's normalised keys)
  *  v       bf16 via desc->v_stride
- *  state   fp32 out, contiguous [B][H][d][r]: state[b][h][c][m] = C[m][c]
+ *  state   fp32 out, contiguous [B][H][nc][d][r]: state[b][h][k][c][m] =
+ *          C_k[m][c], nc = ceil(L / causal_chunk) under a window, else 1
  *  ws      ws_bytes >= sparse_attn_workspace_size(SA_OP_COMP_STATE)
  * Deterministic: partial sums over fixed token chunks added in a fixed order. */
 int sparse_attn_comp_state(const sparse_attn_desc* desc, int32_t rank, const void* k_norm,
@@ -227,7 +233,8 @@ int sparse_attn_comp_state(const sparse_attn_desc* desc, int32_t rank, const voi
 
 /* Gated output O = O_s + g * rms(O_s) * RMSNorm(q~^T C).
  *  q_norm  bf16 [B][H][L][d] via qn_stride
- *  state   fp32 [B][H][d][r] from sparse_attn_comp_state
+ *  state   fp32 [B][H][nc][d][r] from sparse_attn_comp_state (same descriptor
+ *          window)
  *  gamma   fp32 [H][d] RMSNorm weight, or NULL for ones; eps >= 0
  *  gate    fp32 [B][H][L] via gate_stride (elements; 0 broadcasts)
  *  o_s     bf16 sparse-branch output via desc->o_stride

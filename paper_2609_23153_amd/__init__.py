@@ -300,14 +300,18 @@ def _st3(strides):
     return (ctypes.c_int64 * 3)(*strides)
 
 
-def sparse_attn_comp_state(k_norm, v, pk, rope, state=None, ws=None):
+def sparse_attn_comp_state(k_norm, v, pk, rope, state=None, ws=None, causal=None):
     """Low-rank state C = sum_j k~_j v_j^T of the compensation branch.
     k_norm, v bf16 [B, H, N, 128]; pk bf16 [H, 64, 128]; rope fp32 [N, 32, 2].
-    Returns the state transposed, fp32 [B, H, 128, 64] (state[..., c, m] = C[m, c])."""
+    Returns the state transposed, fp32 [B, H, 128, 64] (state[..., c, m] =
+    C[m, c]); under a causal window (chunk, window) one state per chunk,
+    [B, H, ceil(N / chunk), 128, 64]."""
     B, H, N, d = k_norm.shape
-    desc = make_desc(k_norm, k_norm, v)
+    desc = make_desc(k_norm, k_norm, v, causal=causal)
     if state is None:
-        state = torch.empty(B, H, d, COMP_RANK, dtype=torch.float32, device=k_norm.device)
+        shape = (B, H, d, COMP_RANK) if causal is None else \
+            (B, H, -(-N // min(causal[0], N)), d, COMP_RANK)
+        state = torch.empty(shape, dtype=torch.float32, device=k_norm.device)
     for t, name, dt in ((pk, "pk", torch.bfloat16), (rope, "rope", torch.float32),
                         (state, "state", torch.float32)):
         _dense(t, name, dt)
@@ -321,15 +325,16 @@ def sparse_attn_comp_state(k_norm, v, pk, rope, state=None, ws=None):
 
 
 def sparse_attn_comp_out(q_norm, pq, rope, state, gate, o_s, gamma=None, eps: float = 1e-6,
-                         o=None):
+                         o=None, causal=None):
     """Gated output O = O_s + g * rms(O_s) * RMSNorm(q~^T C) (o may be o_s).
-    gate fp32 [B, H, N] (any strides, including 0); gamma fp32 [H, 128] or None."""
+    gate fp32 [B, H, N] (any strides, including 0); gamma fp32 [H, 128] or None;
+    causal (chunk, window) as for the state."""
     B, H, N, d = q_norm.shape
     if o is None:
         o = torch.empty_like(o_s)
     if _strides(o) != _strides(o_s):
         raise ValueError("o and o_s must share their strides")
-    desc = make_desc(q_norm, o=o_s)
+    desc = make_desc(q_norm, o=o_s, causal=causal)
     for t, name, dt in ((pq, "pq", torch.bfloat16), (rope, "rope", torch.float32),
                         (state, "state", torch.float32), (gamma, "gamma", torch.float32)):
         _dense(t, name, dt)

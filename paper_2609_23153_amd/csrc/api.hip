@@ -324,7 +324,6 @@ int sparse_attn_comp_state(const sparse_attn_desc* desc, int32_t rank, const voi
   Shape s;
   int st = check_desc(desc, &s);
   if (st != SA_OK) return st;
-  if (s.causal_chunk > 0) return SA_ERR_UNSUPPORTED;  // the state is not chunk-causal
   if (rank != 64) return SA_ERR_UNSUPPORTED;
   if (!k_norm || !kn_stride || !v || !pk || !rope || !state || !ws) return SA_ERR_INVALID_ARG;
   if (!aligned16(k_norm) || !aligned16(v) || !aligned16(pk) || !aligned16(rope) ||
@@ -353,7 +352,6 @@ int sparse_attn_comp_out(const sparse_attn_desc* desc, int32_t rank, const void*
   Shape s;
   int st = check_desc(desc, &s);
   if (st != SA_OK) return st;
-  if (s.causal_chunk > 0) return SA_ERR_UNSUPPORTED;  // the state is not chunk-causal
   if (rank != 64) return SA_ERR_UNSUPPORTED;
   if (!q_norm || !qn_stride || !pq || !rope || !state || !gate || !o_s || !o)
     return SA_ERR_INVALID_ARG;

@@ -81,9 +81,12 @@ struct StateArgs {
   const uint16_t* v;
   const uint16_t* pk;
   const float* rope;
-  float* partial;  // [BH][chunks][kStateElems], lane-register order
+  float* partial;  // [BH][nc * nsub][kStateElems], lane-register order
   Strides kns, vs;
-  int H, N, chunks;
+  int H, N;
+  int span;  // tokens per causal chunk (N without a window)
+  int nc;    // causal chunks, ceil(N / span)
+  int nsub;  // 1024-token sub-chunks per causal chunk, ceil(span / 1024)
 };
 
 // K~ sub-tile in LDS: [token][r] bf16, 128-byte rows; 16-byte chunk c of
@@ -109,11 +112,17 @@ __global__ __launch_bounds__(256, 2) void comp_state_kernel(StateArgs a) {
   const int b = bh / a.H, h = bh - b * a.H;
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
   const int g = lane >> 5, l32 = lane & 31;
-  const int t_begin = chunk * kChunk, t_end = min(t_begin + kChunk, a.N);
+  // tokens [t_begin, t_end): sub-chunk `sub` of causal chunk `cc`
+  const int cc = chunk / a.nsub, sub = chunk - cc * a.nsub;
+  const int t_begin = cc * a.span + sub * kChunk;
+  const int t_end = min(min(t_begin + kChunk, (cc + 1) * a.span), a.N);
 
+  // resources end at t_end: rows past it (the next chunk, or past N) read
+  // zero and so add nothing to the state
   const uint32_t kst = (uint32_t)a.kns.n * 2, vst = (uint32_t)a.vs.n * 2;
-  const auto kr = make_rsrc(a.kn + b * a.kns.b + h * a.kns.h, (uint32_t)(a.N - 1) * kst + 256u);
-  const auto vr = make_rsrc(a.v + b * a.vs.b + h * a.vs.h, (uint32_t)(a.N - 1) * vst + 256u);
+  const uint32_t rows = (uint32_t)max(t_end, 1);
+  const auto kr = make_rsrc(a.kn + b * a.kns.b + h * a.kns.h, (rows - 1) * kst + 256u);
+  const auto vr = make_rsrc(a.v + b * a.vs.b + h * a.vs.h, (rows - 1) * vst + 256u);
   const auto rr = make_rsrc(a.rope, (uint32_t)a.N * kRopeBytes);
 
   // k_norm as B operand of P_k k_norm^T (token tw + l32, channels
@@ -268,27 +277,46 @@ __global__ __launch_bounds__(256, 2) void comp_state_kernel(StateArgs a) {
   }
 
   // this wave's rows of the chunk's partial C^T
-  float* out = a.partial + ((int64_t)bh * a.chunks + chunk) * kStateElems;
+  float* out = a.partial + ((int64_t)bh * a.nc * a.nsub + chunk) * kStateElems;
 #pragma unroll
   for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
     for (int r = 0; r < 16; ++r) out[((wave * 2 + nb) * 16 + r) * 64 + lane] = acc[nb][r];
 }
 
-// C^T[bh][d][r] = sum over chunks (in chunk order) of the partials; each
-// workgroup sums 256 of a head's elements.
+// C^T[bh][c][d][r] of causal chunk c = sum over the chunks c2 of its window
+// [c - window + 1, c] (all up to c for window 0), in ascending order, of
+// T_c2 = the sum of c2's sub-chunk partials in order.  Without a window there
+// is one chunk.  Each workgroup sums 256 of a head's elements, for every c.
 __global__ __launch_bounds__(256) void comp_reduce_kernel(const float* __restrict__ partial,
-                                                          int chunks, float* __restrict__ state) {
+                                                          int nc, int nsub, int window,
+                                                          float* __restrict__ state) {
   const int bh = blockIdx.x;
   const int e = blockIdx.y * 256 + threadIdx.x;
-  const float* src = partial + (int64_t)bh * chunks * kStateElems + e;
-  float s = 0.f;
-  for (int c = 0; c < chunks; ++c) s += src[(int64_t)c * kStateElems];
+  const float* src = partial + (int64_t)bh * nc * nsub * kStateElems + e;
   const int lane = e & 63, reg = (e >> 6) & 15, blk = e >> 10;  // blk = dt * 2 + nb
   const int dt = blk >> 1, nb = blk & 1;
   const int r = 32 * nb + (lane & 31);
   const int d = 32 * dt + 8 * (reg >> 2) + 4 * (lane >> 5) + (reg & 3);
-  state[(int64_t)bh * kStateElems + d * kRank + r] = s;
+  float* dst = state + (int64_t)bh * nc * kStateElems + d * kRank + r;
+  auto chunk_sum = [&](int c2) {
+    float t = 0.f;
+    for (int u = 0; u < nsub; ++u) t += src[((int64_t)c2 * nsub + u) * kStateElems];
+    return t;
+  };
+  if (window == 0) {  // running prefix: the same additions as the direct sums
+    float s = 0.f;
+    for (int c = 0; c < nc; ++c) {
+      s += chunk_sum(c);
+      dst[(int64_t)c * kStateElems] = s;
+    }
+  } else {
+    for (int c = 0; c < nc; ++c) {
+      float s = 0.f;
+      for (int c2 = max(0, c - window + 1); c2 <= c; ++c2) s += chunk_sum(c2);
+      dst[(int64_t)c * kStateElems] = s;
+    }
+  }
 }
 
 struct OutArgs {
@@ -302,6 +330,8 @@ struct OutArgs {
   uint16_t* o;
   Strides qns, gs, oss;
   int H, N;
+  int span;  // tokens per causal chunk (N without a window)
+  int ntg;   // workgroups per causal chunk, ceil(span / (kOutTiles * 128))
   float eps;
 };
 
@@ -350,8 +380,14 @@ __global__ __launch_bounds__(256, 2) void comp_out_kernel(OutArgs a) {
   __shared__ __attribute__((aligned(16))) float gam_s[kHeadDim];  // RMSNorm weight (1 if none)
   const int bh = blockIdx.x;
   const int b = bh / a.H, h = bh - b * a.H;
-  const int ntiles = (a.N + kSub - 1) / kSub;
-  const int tile0 = blockIdx.y * kOutTiles, tile_end = min(tile0 + kOutTiles, ntiles);
+  // tokens [t_beg, t_end) of causal chunk cc (one chunk without a window),
+  // all of them using that chunk's state, in tiles of 128
+  const int cc = blockIdx.y / a.ntg, grp = blockIdx.y - cc * a.ntg;
+  const int c_end = min((cc + 1) * a.span, a.N);
+  const int t_beg = cc * a.span + grp * kOutTiles * kSub;
+  const int t_end = min(t_beg + kOutTiles * kSub, c_end);
+  if (t_beg >= t_end) return;  // uniform: a short last chunk
+  const int ntile = (t_end - t_beg + kSub - 1) / kSub;
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
   const int g = lane >> 5, l32 = lane & 31;
 
@@ -360,12 +396,13 @@ __global__ __launch_bounds__(256, 2) void comp_out_kernel(OutArgs a) {
   bf16x8 qf[8];
   u32x2 osw[4][4];
   float gv;
-  load_tok(a, b, h, min(tile0 * kSub + 32 * wave + l32, a.N - 1), g, qf, osw, gv);
+  load_tok(a, b, h, min(t_beg + 32 * wave + l32, a.N - 1), g, qf, osw, gv);
 
-  // C^T of this head as bf16 hi + lo into LDS: thread t converts quads of
-  // 4 consecutive r (16-byte loads) and stores each as 8 bytes at its
-  // permuted position
-  const float* st = a.state + (int64_t)bh * kStateElems;
+  // C^T of this head and chunk as bf16 hi + lo into LDS: thread t converts
+  // quads of 4 consecutive r (16-byte loads) and stores each as 8 bytes at
+  // its permuted position
+  const int nc = (a.N + a.span - 1) / a.span;
+  const float* st = a.state + ((int64_t)bh * nc + cc) * kStateElems;
 #pragma unroll
   for (int m = 0; m < kStateElems / 4 / 256; ++m) {
     const int qd = t + 256 * m;              // quad index: d = qd / 16, r = 4 (qd % 16)
@@ -394,8 +431,8 @@ __global__ __launch_bounds__(256, 2) void comp_out_kernel(OutArgs a) {
   if (t < kHeadDim) gam_s[t] = a.gamma ? a.gamma[(int64_t)h * kHeadDim + t] : 1.f;
   __syncthreads();  // C^T, P_q and the RMSNorm weight are in LDS
 
-  for (int tile = tile0; tile < tile_end; ++tile) {
-    const int tok = tile * kSub + 32 * wave + l32;  // this lane's token
+  for (int tile = 0; tile < ntile; ++tile) {
+    const int tok = t_beg + tile * kSub + 32 * wave + l32;  // this lane's token
     // (cos, sin) of this lane's pairs: pairs (rr = 0, 1) and (2, 3) of each
     // (rb, j) are pairs m = 16 rb + 4 j + 2 g + {0, 1}, 16 contiguous bytes.
     // Issued before the next tile's loads, so waiting for them does not wait
@@ -413,7 +450,7 @@ __global__ __launch_bounds__(256, 2) void comp_out_kernel(OutArgs a) {
     bf16x8 qn[8];
     u32x2 on[4][4];
     float gn;
-    load_tok(a, b, h, min(tile + 1 < tile_end ? tok + kSub : tok, a.N - 1), g, qn, on, gn);
+    load_tok(a, b, h, min(tile + 1 < ntile ? tok + kSub : tok, a.N - 1), g, qn, on, gn);
 
     // projection P_q q_norm^T: lane holds token `tok`, rank indices
     // 32 rb + 8 j + 4 g + rr (P_q rows r = l32 + 32 rb as the A operand)
@@ -501,7 +538,7 @@ __global__ __launch_bounds__(256, 2) void comp_out_kernel(OutArgs a) {
     const float rstd = 1.f / sqrtf(ss_y * (1.f / kHeadDim) + a.eps);
     const float rms_o = sqrtf(ss_o * (1.f / kHeadDim));
     const float coef = gv * rms_o * rstd;
-    if (tok < a.N) {
+    if (tok < t_end) {
       uint16_t* orow = a.o + b * a.oss.b + h * a.oss.h + (int64_t)tok * a.oss.n;
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt)
@@ -537,9 +574,16 @@ __global__ __launch_bounds__(256, 2) void comp_out_kernel(OutArgs a) {
 
 }  // namespace
 
+// Tokens per causal chunk (the whole sequence without a window) and the
+// number of chunks, which is the number of states per head.
+static int comp_span(const Shape& s) {
+  return s.causal_chunk > 0 ? std::min(s.causal_chunk, s.N) : s.N;
+}
+int comp_state_chunks(const Shape& s) { return (s.N + comp_span(s) - 1) / comp_span(s); }
+
 size_t comp_state_workspace_bytes(const Shape& s) {
-  const int64_t chunks = (s.N + kChunk - 1) / kChunk;
-  return (size_t)s.B * s.H * chunks * kStateElems * sizeof(float);
+  const int64_t nsub = (comp_span(s) + kChunk - 1) / kChunk;
+  return (size_t)s.B * s.H * comp_state_chunks(s) * nsub * kStateElems * sizeof(float);
 }
 
 hipError_t launch_comp_state(const Shape& s, const CompStateIn& in, float* state, void* ws,
@@ -554,12 +598,14 @@ hipError_t launch_comp_state(const Shape& s, const CompStateIn& in, float* state
   a.vs = in.vs;
   a.H = s.H;
   a.N = s.N;
-  a.chunks = (s.N + kChunk - 1) / kChunk;
-  comp_state_kernel<<<dim3(s.B * s.H, a.chunks), 256, 0, stream>>>(a);
+  a.span = comp_span(s);
+  a.nc = comp_state_chunks(s);
+  a.nsub = (a.span + kChunk - 1) / kChunk;
+  comp_state_kernel<<<dim3(s.B * s.H, a.nc * a.nsub), 256, 0, stream>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  comp_reduce_kernel<<<dim3(s.B * s.H, kReduceSplit), 256, 0, stream>>>(a.partial, a.chunks,
-                                                                         state);
+  comp_reduce_kernel<<<dim3(s.B * s.H, kReduceSplit), 256, 0, stream>>>(
+      a.partial, a.nc, a.nsub, s.causal_chunk > 0 ? s.causal_window : 0, state);
   return hipGetLastError();
 }
 
@@ -579,8 +625,9 @@ hipError_t launch_comp_out(const Shape& s, const CompOutIn& in, hipStream_t stre
   a.H = s.H;
   a.N = s.N;
   a.eps = in.eps;
-  const int ntiles = (s.N + kSub - 1) / kSub;
-  comp_out_kernel<<<dim3(s.B * s.H, (ntiles + kOutTiles - 1) / kOutTiles), 256, 0, stream>>>(a);
+  a.span = comp_span(s);
+  a.ntg = (a.span + kOutTiles * kSub - 1) / (kOutTiles * kSub);
+  comp_out_kernel<<<dim3(s.B * s.H, comp_state_chunks(s) * a.ntg), 256, 0, stream>>>(a);
   return hipGetLastError();
 }
 

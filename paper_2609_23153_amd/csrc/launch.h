@@ -82,7 +82,7 @@ struct CompOutIn {
   const void* q_norm;  // bf16 via qns
   const void* pq;      // bf16 [H][64][128]
   const float* rope;
-  const float* state;  // fp32 [B][H][128][64] (C^T, d-major)
+  const float* state;  // fp32 [B][H][chunks][128][64] (C^T, d-major)
   const float* gamma;  // fp32 [H][128] or null
   const float* gate;   // fp32 via gs
   const void* o_s;     // bf16 via oss
@@ -90,6 +90,8 @@ struct CompOutIn {
   Strides qns, gs, oss;
   float eps;
 };
+// states per head: one per causal chunk, or 1 without a window
+int comp_state_chunks(const Shape& s);
 size_t comp_state_workspace_bytes(const Shape& s);
 hipError_t launch_comp_state(const Shape& s, const CompStateIn& in, float* state, void* ws,
                              hipStream_t stream);

@@ -238,12 +238,14 @@ def test_causal_window_fields_are_checked():
     assert sel(1024, -2) == -1                    # negative window
     assert sel(0, 3) == -1                        # window without chunks
     assert sel(1024, 2, mode=sa.SA_SELECT_HEAD_TOPK, budget=500) == -2   # whole-head mode
-    ds = desc()
-    ds.causal_chunk, ds.causal_window = 1024, 2
-    cneed = lib.sparse_attn_workspace_size(ctypes.byref(ds), sa.SA_OP_COMP_STATE, 1)
-    assert lib.sparse_attn_comp_state(ctypes.byref(ds), 64, P, st3, P, P, P, P, P, cneed,
-                                      None) == -2
-    g3 = (ctypes.c_int64 * 3)(2 * 4096, 4096, 1)
-    assert lib.sparse_attn_comp_out(ctypes.byref(ds), 64, P, st3, P, P, P, None, 1e-6, P, g3,
-                                    P, P, None) == -2
+    # the compensation state keeps one partial per (chunk, 1024-token
+    # sub-chunk) of the 4096 tokens: chunks of 1000 -> 5 x 1 partials, one
+    # chunk of 4096 -> 4, chunks of 1500 -> 3 x 2
+    d0 = desc()
+    base = lib.sparse_attn_workspace_size(ctypes.byref(d0), sa.SA_OP_COMP_STATE, 1)
+    for chunk, parts in ((1000, 5), (4096, 4), (1500, 6)):
+        ds = desc()
+        ds.causal_chunk, ds.causal_window = chunk, 0
+        assert lib.sparse_attn_workspace_size(ctypes.byref(ds), sa.SA_OP_COMP_STATE, 1) == \
+            base // 4 * parts
     assert ctypes.sizeof(sa.SparseAttnDesc) == 136   # the C struct with the two int32 fields

@@ -116,3 +116,71 @@ def test_comp_full_size_heads():
     state, o = run_gpu(qn, kn, v, o_s, pq, pk, gamma, gate, rope)
     for i in range(len(heads)):
         check_head(0, i, qn, kn, v, o_s, pq, pk, gamma, gate, rope, state, o, "14B-720P")
+
+
+# ---- causal window -----------------------------------------------------------
+def check_head_causal(b, h, qn, kn, v, o_s, pq, pk, gamma, gate, rope, state, o, causal, what,
+                      rows=None):
+    """State per chunk and gated output against the oracle's causal branch."""
+    rp = rope.numpy()
+    chunk, window = causal
+    ref_states = O.comp_state_causal(widen(kn[b, h]), widen(v[b, h]), widen(pk[h]), rp, chunk,
+                                     window)
+    assert state.shape[2] == ref_states.shape[0], (what, state.shape)
+    es = max(rel_l2(state[b, h, c].T, ref_states[c]) for c in range(ref_states.shape[0]))
+    g = None if gamma is None else gamma[h].double().numpy()
+    olr = O.comp_lowrank_causal(widen(qn[b, h]), widen(pq[h]), rp, ref_states, chunk, g, 1e-6)
+    ref = O.comp_combine(widen(o_s[b, h]), olr, gate[b, h].double().numpy())
+    got = o[b, h].to(torch.float64).numpy()
+    if rows is not None:
+        got, ref = got[rows], ref[rows]
+    eo = rel_l2(got, ref)
+    scaled = float((np.abs(got - ref) / np.maximum(1.0, np.abs(ref))).max())
+    say(f"  {what} b{b} h{h}: {ref_states.shape[0]} states, worst rel_l2={es:.3e}  out "
+        f"rel_l2={eo:.3e} max |err|/max(1,|ref|)={scaled:.3e}")
+    assert es <= 1e-2, (what, es)
+    assert eo <= 1e-2 and scaled <= 2e-2, (what, eo, scaled)
+
+
+def run_gpu_causal(qn, kn, v, o_s, pq, pk, gamma, gate, rope, causal):
+    d = lambda t: None if t is None else t.to(DEV)
+    qd, kd, vd, od, pqd, pkd, gd, gtd, rd = map(d, (qn, kn, v, o_s, pq, pk, gamma, gate, rope))
+    state = sa.sparse_attn_comp_state(kd, vd, pkd, rd, causal=causal)
+    o = sa.sparse_attn_comp_out(qd, pqd, rd, state, gtd, od, gamma=gd, causal=causal)
+    torch.cuda.synchronize()
+    return state.cpu().numpy(), o.cpu()
+
+
+@pytest.mark.parametrize("grid,causal", [((4, 16, 32), (1024, 0)), ((4, 16, 32), (1024, 2)),
+                                         ((4, 16, 32), (2048, 1)), ((5, 8, 25), (300, 0)),
+                                         ((3, 7, 11), (77, 2)), ((6, 20, 25), (1500, 0))])
+def test_comp_causal(grid, causal):
+    """Chunks of whole frames and chunk boundaries inside 128-token tiles and
+    1024-token sub-chunks (300, 77, 1500 tokens), windows 0, 1, 2."""
+    wl, qn, kn, v, o_s, pq, pk, gamma, gate, rope = inputs(grid, seed=sum(grid) + causal[0])
+    state, o = run_gpu_causal(qn, kn, v, o_s, pq, pk, gamma, gate, rope, causal)
+    for h in range(qn.shape[1]):
+        check_head_causal(0, h, qn, kn, v, o_s, pq, pk, gamma, gate, rope, state, o, causal,
+                          f"causal {grid} {causal}")
+
+
+def test_comp_causal_one_chunk_equals_unrestricted():
+    """A single chunk covering the sequence: state and output equal the
+    unrestricted calls bit for bit."""
+    wl, qn, kn, v, o_s, pq, pk, gamma, gate, rope = inputs((4, 16, 32), seed=9)
+    s0, o0 = run_gpu(qn, kn, v, o_s, pq, pk, gamma, gate, rope)
+    s1, o1 = run_gpu_causal(qn, kn, v, o_s, pq, pk, gamma, gate, rope, (qn.shape[2], 0))
+    assert np.array_equal(s0, s1[:, :, 0])
+    assert torch.equal(o0.view(torch.int16), o1.view(torch.int16))
+
+
+def test_comp_causal_full_size_heads():
+    """The 14B-720P shape generated in chunks of 3 latent frames (10,800
+    tokens, full history: 7 states per head): two heads whole."""
+    grid = (21, 45, 80)
+    wl, qn, kn, v, o_s, pq, pk, gamma, gate, rope = inputs(grid, heads=2, seed=31)
+    causal = (3 * 45 * 80, 0)
+    state, o = run_gpu_causal(qn, kn, v, o_s, pq, pk, gamma, gate, rope, causal)
+    for h in range(2):
+        check_head_causal(0, h, qn, kn, v, o_s, pq, pk, gamma, gate, rope, state, o, causal,
+                          "14B-720P causal")
