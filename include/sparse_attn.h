@@ -84,9 +84,11 @@ typedef struct {
    * key blocks (those holding an allowed key of some query of the block) and
    * keeps min(budget, candidates) of them (cnt says how many; the rest of the
    * row is -1); the forward calls mask every score outside a query's allowed
-   * keys, and a row left with none gets O = 0 and LSE = -inf.  The whole-head
-   * selection mode and the compensation calls return SA_ERR_UNSUPPORTED with
-   * a window.  Negative values, or a window without chunks: SA_ERR_INVALID_ARG. */
+   * keys, and a row left with none gets O = 0 and LSE = -inf; the backward
+   * takes the same window; the compensation calls keep one state per chunk
+   * (see sparse_attn_comp_state).  The whole-head selection mode returns
+   * SA_ERR_UNSUPPORTED with a window.  Negative values, or a window without
+   * chunks: SA_ERR_INVALID_ARG. */
   int32_t causal_chunk;
   int32_t causal_window;
 } sparse_attn_desc;
