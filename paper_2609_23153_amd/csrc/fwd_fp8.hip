@@ -36,6 +36,7 @@ constexpr int kTileBytes = kTile * kRowBytes;   // 8 KB per K or V tile
 constexpr int kPairBytes = 2 * kTileBytes;      // one pair of tiles
 constexpr float kLazy = 2.f;  // log2 headroom before the accumulator is rescaled
 constexpr float kPScale = 64.f;                  // 2^(8 - kLazy): P in (0, 256] before e4m3
+constexpr float kLog2PScale = 6.f;               // log2(kPScale)
 constexpr int kPScaleInvE8m0 = 127 - 6;          // E8M0 code of 2^-(8 - kLazy)
 constexpr int kOneE8m0 = 127;                    // E8M0 code of 1
 constexpr int kFp8One = 0x38383838;              // four e4m3 ones
@@ -361,6 +362,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
     // P^T as B operand: slot 16*rt + r <- s[rt][r]; values 2^(x - m) * 2^(8 - kLazy)
     // rounded to e4m3
     i32x8 pk;
+    const float mofs = kLog2PScale - msafe;  // the factor kPScale folded into the exponent
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
 #pragma unroll
@@ -368,7 +370,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
         float x[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u)
-          x[u] = __builtin_amdgcn_exp2f(fmaf(s[rt][r + u], p.scale_log2, -msafe)) * kPScale;
+          x[u] = __builtin_amdgcn_exp2f(fmaf(s[rt][r + u], p.scale_log2, mofs));
         int w = __builtin_amdgcn_cvt_pk_fp8_f32(x[0], x[1], 0, false);
         w = __builtin_amdgcn_cvt_pk_fp8_f32(x[2], x[3], w, true);
         pk[4 * rt + r / 4] = w;
