@@ -530,11 +530,16 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p) {
   barrier_keep_loads();
 
   const float c2 = p.tau * kLog2e;
-  f32x16 acck[2], accv[2];
+  // phase 2: wave (mat, hh) accumulates dV^T (mat 0) or dK^T / tau (mat 1)
+  // for channels 64 hh + 32 dt .. and keys 32 kb ..
+  const int mat = wave & 1;
+  f32x16 acc[2][2];
 #pragma unroll
   for (int dt = 0; dt < 2; ++dt)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acck[dt][r] = accv[dt][r] = 0.f;
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[dt][kb][r] = 0.f;
 
   // One query tile from (qt, ot) starting at st, which every wave sees
   // landed; stn starts the next one.  Once every wave is done reading
@@ -594,8 +599,10 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p) {
     }
     wait_lgkm0();
     barrier_keep_loads();  // P and dS of the whole tile in LDS
-    // phase 2: keys 32 kh.., channels 64 hh.. (MFMA output: lane holds key
-    // 32 kh + l32, channels 64 hh + 32 dt + 8(r>>2) + 4g + (r&3))
+    // phase 2: wave (mat, hh): dV^T += dO^T P (mat 0) or dK^T += Q^T dS (mat
+    // 1) for channels 64 hh .. and all 64 keys (MFMA output [dt][kb]: lane
+    // holds key 32 kb + l32, channels 64 hh + 32 dt + 8(r>>2) + 4g + (r&3));
+    // each step reads 2 A and 2 B fragments for 4 MFMAs
     {
       const int ln = fresh_lane();
       uint32_t to[2][2], po[2][2];
@@ -604,28 +611,28 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p) {
 #pragma unroll
         for (int x = 0; x < 2; ++x) {
           to[hf][x] = trans_off(ln, hf, 2 * hh + x);
-          po[hf][x] = ptr_off(ln, hf, x, kh);
+          po[hf][x] = ptr_off(ln, hf, x, 0);
         }
+      const uint8_t* at = mat ? qt : ot;        // A: Q^T or dO^T
+      const uint8_t* bt = mat ? sbuf : pbuf;    // B: dS or P
 #define PFRAG(buf, r16)                                                                     \
   tr_pair(buf + ((r16) >> 5) * 2 * kPBlock + ((r16)&16) * 64 + po[0][((r16) >> 4) & 1],     \
           buf + ((r16) >> 5) * 2 * kPBlock + ((r16)&16) * 64 + po[1][((r16) >> 4) & 1])
 #define TFRAG(t, r16, dt) tr_pair(t + (r16)*kRowBytes + to[0][dt], t + (r16)*kRowBytes + to[1][dt])
 #pragma unroll
       for (int r16 = 0; r16 < kTile; r16 += 16) {
-        const bf16x8 pf = PFRAG(pbuf, r16);
+        bf16x8 af[2], bf[2];
+#pragma unroll
+        for (int x = 0; x < 2; ++x) {
+          af[x] = TFRAG(at, r16, x);
+          bf[x] = PFRAG(bt + x * kPBlock, r16);  // key half x: block (x, row half)
+        }
 #pragma unroll
         for (int dt = 0; dt < 2; ++dt)
-          accv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(TFRAG(ot, r16, dt), pf, accv[dt], 0, 0,
-                                                             0);
-      }
-      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int r16 = 0; r16 < kTile; r16 += 16) {
-        const bf16x8 sf = PFRAG(sbuf, r16);
-#pragma unroll
-        for (int dt = 0; dt < 2; ++dt)
-          acck[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(TFRAG(qt, r16, dt), sf, acck[dt], 0, 0,
-                                                             0);
+          for (int kb = 0; kb < 2; ++kb)
+            acc[dt][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[dt], bf[kb], acc[dt][kb], 0,
+                                                                  0, 0);
       }
 #undef PFRAG
 #undef TFRAG
@@ -656,22 +663,23 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p) {
   }
   wait_vm0();
 
-  // store dK = tau * acck, dV = accv (lane: key, 4 channels at a time)
-  if (key < p.N) {
-    uint16_t* ok = p.dk + b * p.ks.b + h * p.ks.h + (int64_t)key * p.ks.n + 64 * hh;
-    uint16_t* ov = p.dv + b * p.vs.b + h * p.vs.h + (int64_t)key * p.vs.n + 64 * hh;
+  // store dV = acc (mat 0) or dK = tau * acc (mat 1): lane holds key
+  // 32 kb + l32, 4 channels at a time
+  const float sc = mat ? p.tau : 1.f;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    const int key2 = k0 + 32 * kb + l32;
+    if (key2 >= p.N) continue;
+    uint16_t* out = mat ? p.dk + b * p.ks.b + h * p.ks.h + (int64_t)key2 * p.ks.n + 64 * hh
+                        : p.dv + b * p.vs.b + h * p.vs.h + (int64_t)key2 * p.vs.n + 64 * hh;
 #pragma unroll
     for (int dt = 0; dt < 2; ++dt)
 #pragma unroll
       for (int jq = 0; jq < 4; ++jq) {
-        const int c = dt * 32 + 8 * jq + 4 * g;
-        u32x2 wk, wv;
-        wk[0] = cvt_bf16x2(p.tau * acck[dt][4 * jq], p.tau * acck[dt][4 * jq + 1]);
-        wk[1] = cvt_bf16x2(p.tau * acck[dt][4 * jq + 2], p.tau * acck[dt][4 * jq + 3]);
-        wv[0] = cvt_bf16x2(accv[dt][4 * jq], accv[dt][4 * jq + 1]);
-        wv[1] = cvt_bf16x2(accv[dt][4 * jq + 2], accv[dt][4 * jq + 3]);
-        *reinterpret_cast<u32x2*>(ok + c) = wk;
-        *reinterpret_cast<u32x2*>(ov + c) = wv;
+        u32x2 w;
+        w[0] = cvt_bf16x2(sc * acc[dt][kb][4 * jq], sc * acc[dt][kb][4 * jq + 1]);
+        w[1] = cvt_bf16x2(sc * acc[dt][kb][4 * jq + 2], sc * acc[dt][kb][4 * jq + 3]);
+        *reinterpret_cast<u32x2*>(out + dt * 32 + 8 * jq + 4 * g) = w;
       }
   }
 }
