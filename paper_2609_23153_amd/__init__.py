@@ -309,8 +309,10 @@ def sparse_attn_comp_state(k_norm, v, pk, rope, state=None, ws=None, causal=None
     B, H, N, d = k_norm.shape
     desc = make_desc(k_norm, k_norm, v, causal=causal)
     if state is None:
-        shape = (B, H, d, COMP_RANK) if causal is None else \
-            (B, H, -(-N // min(causal[0], N)), d, COMP_RANK)
+        if causal is None or int(causal[0]) <= 0:
+            shape = (B, H, d, COMP_RANK)
+        else:
+            shape = (B, H, -(-N // min(int(causal[0]), N)), d, COMP_RANK)
         state = torch.empty(shape, dtype=torch.float32, device=k_norm.device)
     for t, name, dt in ((pk, "pk", torch.bfloat16), (rope, "rope", torch.float32),
                         (state, "state", torch.float32)):
