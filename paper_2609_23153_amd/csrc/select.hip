@@ -223,18 +223,73 @@ __device__ __forceinline__ uint32_t kth_largest32(const uint32_t (&v)[KPL], cons
   return prefix;
 }
 
+// The k largest of the wave's member keys (hi, lo words; ties to the lower
+// index jj), written to out in ascending jj order.  Members must sit in
+// ascending jj order over (slot t, lane).  Requires 1 <= k <= count(member).
+template <int KPL>
+__device__ __forceinline__ void select_emit(const uint32_t (&hi)[KPL], const uint32_t (&lo)[KPL],
+                                            const bool (&member)[KPL], const int (&jj)[KPL],
+                                            int k, int32_t* out) {
+  bool exact;
+  const uint32_t thi = kth_largest32<KPL>(hi, member, k, &exact);
+  // selection: hi > thi, or hi == thi and (lo > tlo, or lo == tlo and among
+  // the first need_eq such keys in index order)
+  uint32_t tlo = 0;
+  int need_eq = 0;
+  if (!exact) {
+    int gt = 0;
+#pragma unroll
+    for (int t = 0; t < KPL; ++t) gt += __popcll(__ballot(member[t] && hi[t] > thi));
+    bool grp[KPL];
+#pragma unroll
+    for (int t = 0; t < KPL; ++t) grp[t] = member[t] && hi[t] == thi;
+    bool ex2;
+    tlo = kth_largest32<KPL>(lo, grp, k - gt, &ex2);
+    int gt2 = 0;
+#pragma unroll
+    for (int t = 0; t < KPL; ++t) gt2 += __popcll(__ballot(grp[t] && lo[t] > tlo));
+    need_eq = k - gt - gt2;
+  }
+  const uint64_t below = lanes_below_mask();
+  int taken = 0, eq_seen = 0;
+#pragma unroll
+  for (int t = 0; t < KPL; ++t) {
+    bool sel;
+    if (exact) {
+      sel = member[t] && hi[t] >= thi;
+    } else {
+      const bool eq = member[t] && hi[t] == thi && lo[t] == tlo;
+      const uint64_t eq_mask = __ballot(eq);
+      const int eq_rank = eq_seen + __popcll(eq_mask & below);
+      sel = (member[t] && (hi[t] > thi || (hi[t] == thi && lo[t] > tlo))) ||
+            (eq && eq_rank < need_eq);
+      eq_seen += __popcll(eq_mask);
+    }
+    const uint64_t sel_mask = __ballot(sel);
+    if (sel) out[taken + __popcll(sel_mask & below)] = jj[t];
+    taken += __popcll(sel_mask);
+  }
+}
+
 // One wavefront per query block: the k largest of the row's order keys
 // (64-bit), ties to the lower block index, emitted in ascending index order.
-// The k-th largest key is found on its high 32 bits first; only the keys that
-// tie with it there take part in the search over the low 32 bits.
+// Fast path: the k-th largest high word among the 64 lanes' maxima, P, bounds
+// the row's k-th largest key from below (at least k keys have high word
+// >= P), so only keys with high word >= P can be kept.  When at most 64 keys
+// pass, they are compacted in index order, one per lane, and the exact
+// selection runs on them; otherwise it runs on the whole row.  Either way the
+// k-th largest key is found on its high 32 bits first; only the keys that tie
+// with it there take part in the search over the low 32 bits.
 template <int KPL>
 __global__ __launch_bounds__(256) void topk_row_kernel(const double* __restrict__ scores,
                                                        int nb, int rows, int k_all, int kmax,
                                                        bool k_per_row, Shape cs,
                                                        int32_t* __restrict__ idx,
                                                        int32_t* __restrict__ cnt) {
+  __shared__ uint32_t cand[4][3][kWave];  // per wave: candidate hi, lo, index
   const int lane = threadIdx.x & (kWave - 1);
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int wv = threadIdx.x >> 6;
+  const int row = blockIdx.x * 4 + wv;
   if (row >= rows) return;  // uniform per wave
   // Candidate key blocks [jlo, jhi): under a causal window those holding an
   // allowed key of some query of the block (the allowed ranges never move
@@ -253,55 +308,57 @@ __global__ __launch_bounds__(256) void topk_row_kernel(const double* __restrict_
   const double* s = scores + (int64_t)row * nb;
   uint32_t hi[KPL], lo[KPL];
   bool valid[KPL];
+  int jj[KPL];
+  uint32_t mhi = 0;  // high word of this lane's largest key (0: none)
 #pragma unroll
   for (int t = 0; t < KPL; ++t) {
     const int j = lane + kWave * t;
+    jj[t] = j;
     valid[t] = j >= jlo && j < jhi;
     const uint64_t key = valid[t] ? order_key(s[j]) : 0ull;
     hi[t] = (uint32_t)(key >> 32);
     lo[t] = (uint32_t)key;
+    mhi = max(mhi, hi[t]);
   }
-  bool exact;
-  const uint32_t thi = kth_largest32<KPL>(hi, valid, k, &exact);
-  // selection: hi > thi, or hi == thi and (lo > tlo, or lo == tlo and among
-  // the first need_eq such keys in index order)
-  uint32_t tlo = 0;
-  int need_eq = 0;
-  if (!exact) {
-    int gt = 0;
-#pragma unroll
-    for (int t = 0; t < KPL; ++t) gt += __popcll(__ballot(valid[t] && hi[t] > thi));
-    bool grp[KPL];
-#pragma unroll
-    for (int t = 0; t < KPL; ++t) grp[t] = valid[t] && hi[t] == thi;
-    bool ex2;
-    tlo = kth_largest32<KPL>(lo, grp, k - gt, &ex2);
-    int gt2 = 0;
-#pragma unroll
-    for (int t = 0; t < KPL; ++t) gt2 += __popcll(__ballot(grp[t] && lo[t] > tlo));
-    need_eq = k - gt - gt2;
-  }
-
-  const uint64_t below = lanes_below_mask();
   int32_t* out = idx + (int64_t)row * kmax;
-  int taken = 0, eq_seen = 0;
+
+  bool fast = __popcll(__ballot(mhi != 0u)) >= k;
+  uint32_t P = 0;
+  int c = 0;
+  if (fast) {  // wave-uniform
+    const uint32_t mv[1] = {mhi};
+    const bool mm[1] = {mhi != 0u};
+    bool ex;
+    P = kth_largest32<1>(mv, mm, k, &ex);
 #pragma unroll
-  for (int t = 0; t < KPL; ++t) {
-    const int j = lane + kWave * t;
-    bool sel;
-    if (exact) {
-      sel = valid[t] && hi[t] >= thi;
-    } else {
-      const bool eq = valid[t] && hi[t] == thi && lo[t] == tlo;
-      const uint64_t eq_mask = __ballot(eq);
-      const int eq_rank = eq_seen + __popcll(eq_mask & below);
-      sel = (valid[t] && (hi[t] > thi || (hi[t] == thi && lo[t] > tlo))) ||
-            (eq && eq_rank < need_eq);
-      eq_seen += __popcll(eq_mask);
+    for (int t = 0; t < KPL; ++t) c += __popcll(__ballot(valid[t] && hi[t] >= P));
+    fast = c <= kWave;
+  }
+  if (fast) {
+    // compact the candidates in ascending index order, one per lane
+    const uint64_t below = lanes_below_mask();
+    int base = 0;
+#pragma unroll
+    for (int t = 0; t < KPL; ++t) {
+      const bool ok = valid[t] && hi[t] >= P;
+      const uint64_t m = __ballot(ok);
+      if (ok) {
+        const int pos = base + __popcll(m & below);
+        cand[wv][0][pos] = hi[t];
+        cand[wv][1][pos] = lo[t];
+        cand[wv][2][pos] = (uint32_t)jj[t];
+      }
+      base += __popcll(m);
     }
-    const uint64_t sel_mask = __ballot(sel);
-    if (sel) out[taken + __popcll(sel_mask & below)] = j;
-    taken += __popcll(sel_mask);
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's writes landed
+    __builtin_amdgcn_wave_barrier();
+    const uint32_t ch[1] = {lane < c ? cand[wv][0][lane] : 0u};
+    const uint32_t cl[1] = {lane < c ? cand[wv][1][lane] : 0u};
+    const int cj[1] = {lane < c ? (int)cand[wv][2][lane] : 0};
+    const bool cv[1] = {lane < c};
+    select_emit<1>(ch, cl, cv, cj, k, out);
+  } else {
+    select_emit<KPL>(hi, lo, valid, jj, k, out);
   }
   for (int p = k + lane; p < kmax; p += kWave) out[p] = -1;
   if (lane == 0) cnt[row] = k;
