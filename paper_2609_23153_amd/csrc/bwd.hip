@@ -174,10 +174,10 @@ __device__ __forceinline__ void wait_lgkm0() {
 __device__ __forceinline__ int list_tile(list_ptr list, int n, int total, int spb, int block,
                                          int nb, int N, int* next) {
   for (; n < total; ++n) {
-    const int e = n / spb;
+    const int e = n >> (spb - 1);  // spb (sub-tiles per block) is 1 or 2
     const int j = list[e];
     if (j < 0 || j >= nb) continue;
-    const int st = j * block + (n - e * spb) * kTile;
+    const int st = j * block + (n - (e << (spb - 1))) * kTile;
     if (st < N) {
       *next = n + 1;
       return st;

@@ -72,19 +72,19 @@ struct Params {
 // list entry is out of range or the sub-tile lies past the sequence end.
 typedef const __attribute__((address_space(4))) int32_t* list_ptr;
 
-__device__ __forceinline__ int tile_start(list_ptr list, int n, int spb, int block, int nb,
+__device__ __forceinline__ int tile_start(list_ptr list, int n, int sh, int block, int nb,
                                           int N) {
-  const int e = n / spb;
+  const int e = n >> sh;
   const int j = list[e];
   if (j < 0 || j >= nb) return -1;
-  const int st = j * block + (n - e * spb) * kTile;
+  const int st = j * block + (n - (e << sh)) * kTile;
   return st < N ? st : -1;
 }
 
-__device__ __forceinline__ int next_tile(list_ptr list, int n, int total, int spb, int block,
+__device__ __forceinline__ int next_tile(list_ptr list, int n, int total, int sh, int block,
                                          int nb, int N, int* start) {
   for (; n < total; ++n) {
-    const int st = tile_start(list, n, spb, block, nb, N);
+    const int st = tile_start(list, n, sh, block, nb, N);
     if (st >= 0) {
       *start = st;
       return n;
@@ -170,6 +170,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
   const int q0 = qt * kTile;
   const int iblk = q0 / p.block;
   const int spb = p.block / kTile;
+  const int sh = spb == 2 ? 1 : 0;  // log2(spb): blocks are 64 or 128 tokens
   const int c = min(max(p.cnt[(int64_t)bh * p.nb + iblk], 0), p.kmax);
   const int total = c * spb;
   // The list is read-only here: reading it through the constant address space
@@ -198,9 +199,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
   // two valid tiles (total / N when there are none).  The list entry after
   // n2 is read one step ahead.
   int s0 = p.N, s1 = p.N, s2 = p.N;
-  int n = next_tile(list, 0, total, spb, p.block, p.nb, p.N, &s0);
-  int n1 = next_tile(list, n + 1, total, spb, p.block, p.nb, p.N, &s1);
-  int n2 = next_tile(list, n1 + 1, total, spb, p.block, p.nb, p.N, &s2);
+  int n = next_tile(list, 0, total, sh, p.block, p.nb, p.N, &s0);
+  int n1 = next_tile(list, n + 1, total, sh, p.block, p.nb, p.N, &s1);
+  int n2 = next_tile(list, n1 + 1, total, sh, p.block, p.nb, p.N, &s2);
 
   // Prologue.  The Q tile is staged through vb2 (same swizzle as K) while
   // K(0), V(0), V(1), K(1) are issued; step 0 refills vb2 with V(2) once every
@@ -278,7 +279,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
       kf[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(kc + (kxs ^ (uint32_t)(ks << 5))));
     // list entry of the tile after n2 (a scalar load, waited below)
     const int ahead = n2 + 1;
-    const int pre = list[min(ahead / spb, p.kmax - 1)];
+    const int pre = list[min(ahead >> sh, p.kmax - 1)];
     wait_lgkm0();
     barrier_keep_loads();  // every wave holds its K fragments: kc is free
     dma_tile(kc, kr, dofs.k, (uint32_t)s2 * kst);
@@ -361,12 +362,12 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(Params p) {
     n2 = total;
     if (ahead < total) {
       const int j = __builtin_amdgcn_readfirstlane(pre);
-      const int st = j * p.block + (ahead % spb) * kTile;
+      const int st = j * p.block + (ahead & (spb - 1)) * kTile;
       if (j >= 0 && j < p.nb && st < p.N) {
         n2 = ahead;
         s2 = st;
       } else {
-        n2 = next_tile(list, ahead + 1, total, spb, p.block, p.nb, p.N, &s2);
+        n2 = next_tile(list, ahead + 1, total, sh, p.block, p.nb, p.N, &s2);
       }
     }
     // keep the whole tile's work ahead of the wait

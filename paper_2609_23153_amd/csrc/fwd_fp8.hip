@@ -73,10 +73,10 @@ struct Params {
 
 __device__ __forceinline__ int tile_start(list_ptr list, int n, int spb, int block, int nb,
                                           int N) {
-  const int e = n / spb;
+  const int e = n >> (spb - 1);  // spb (sub-tiles per block) is 1 or 2
   const int j = list[e];
   if (j < 0 || j >= nb) return -1;
-  const int st = j * block + (n - e * spb) * kTile;
+  const int st = j * block + (n - (e << (spb - 1))) * kTile;
   return st < N ? st : -1;
 }
 
@@ -176,7 +176,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
   // (na*, nb*), start rows (ta*, tb*; N when missing: such tiles read zeros
   // and all their keys are masked) and key blocks (ja*, jb*).  The list
   // entries after P2 and the scales of P1 are read one step ahead.
-  auto block_of = [&](int n) { return n < total ? list[n / spb] : 0; };
+  auto block_of = [&](int n) { return n < total ? list[n >> (spb - 1)] : 0; };
   int ta0 = p.N, tb0 = p.N, ta1 = p.N, tb1 = p.N, ta2 = p.N, tb2 = p.N;
   int na0 = next_tile(list, 0, total, spb, p.block, p.nb, p.N, &ta0);
   int nb0 = next_tile(list, na0 + 1, total, spb, p.block, p.nb, p.N, &tb0);
@@ -257,7 +257,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
     *jout = 0;
     if (ahead >= total) return total;
     const int j = __builtin_amdgcn_readfirstlane(pre);
-    const int s0 = j * p.block + (ahead % spb) * kTile;
+    const int s0 = j * p.block + (ahead & (spb - 1)) * kTile;
     if (j >= 0 && j < p.nb && s0 < p.N) {
       *st = s0;
       *jout = j;
@@ -293,8 +293,8 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
     }
     // one step ahead: scales of P1, list entries after P2
     const float fka = skh[ja1], fva = svh[ja1], fkb = skh[jb1], fvb = svh[jb1];
-    const int pre1 = list[min((nb2 + 1) / spb, p.kmax - 1)];
-    const int pre2 = list[min((nb2 + 2) / spb, p.kmax - 1)];
+    const int pre1 = list[min((nb2 + 1) >> (spb - 1), p.kmax - 1)];
+    const int pre2 = list[min((nb2 + 2) >> (spb - 1), p.kmax - 1)];
     wait_lgkm0();
     barrier_keep_loads();  // every wave holds its K fragments: kc is free
     dma_pair(kc, kr, koff, ta2, tb2);
