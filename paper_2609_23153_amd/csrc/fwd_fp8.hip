@@ -71,10 +71,19 @@ struct Params {
   Shape cs;  // causal window (causal_chunk 0: none)
 };
 
+// Scalar load of element `i` (non-negative) of a uniform array: the byte
+// offset stays a 32-bit SGPR operand of s_load (one shift) instead of a
+// 64-bit address computed per load.
+template <typename T>
+__device__ __forceinline__ T sld(const __attribute__((address_space(4))) T* base, uint32_t i) {
+  return *reinterpret_cast<const __attribute__((address_space(4))) T*>(
+      reinterpret_cast<const __attribute__((address_space(4))) char*>(base) + i * (uint32_t)sizeof(T));
+}
+
 __device__ __forceinline__ int tile_start(list_ptr list, int n, int spb, int block, int nb,
                                           int N) {
   const int e = n >> (spb - 1);  // spb (sub-tiles per block) is 1 or 2
-  const int j = list[e];
+  const int j = sld(list, (uint32_t)e);
   if (j < 0 || j >= nb) return -1;
   const int st = j * block + (n - (e << (spb - 1))) * kTile;
   return st < N ? st : -1;
@@ -176,7 +185,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
   // (na*, nb*), start rows (ta*, tb*; N when missing: such tiles read zeros
   // and all their keys are masked) and key blocks (ja*, jb*).  The list
   // entries after P2 and the scales of P1 are read one step ahead.
-  auto block_of = [&](int n) { return n < total ? list[n >> (spb - 1)] : 0; };
+  auto block_of = [&](int n) { return n < total ? sld(list, (uint32_t)(n >> (spb - 1))) : 0; };
   int ta0 = p.N, tb0 = p.N, ta1 = p.N, tb1 = p.N, ta2 = p.N, tb2 = p.N;
   int na0 = next_tile(list, 0, total, spb, p.block, p.nb, p.N, &ta0);
   int nb0 = next_tile(list, na0 + 1, total, spb, p.block, p.nb, p.N, &tb0);
@@ -188,7 +197,8 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
   int ja2 = block_of(na2), jb2 = block_of(nb2);
   // scale codes of the current pair: (K, V) for tiles A and B
   const int ja0 = block_of(na0), jb0 = block_of(nb0);
-  int sk_a = e8m0(skh[ja0]), sv_a = e8m0(svh[ja0]), sk_b = e8m0(skh[jb0]), sv_b = e8m0(svh[jb0]);
+  int sk_a = e8m0(sld(skh, ja0)), sv_a = e8m0(sld(svh, ja0)), sk_b = e8m0(sld(skh, jb0)),
+      sv_b = e8m0(sld(svh, jb0));
 
   // Prologue: the Q tile is staged through vp2 (K swizzle) while the K and V
   // pairs P0 and P1 are issued; step 0 refills vp2 with V(P2) once every wave
@@ -292,9 +302,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
       }
     }
     // one step ahead: scales of P1, list entries after P2
-    const float fka = skh[ja1], fva = svh[ja1], fkb = skh[jb1], fvb = svh[jb1];
-    const int pre1 = list[min((nb2 + 1) >> (spb - 1), p.kmax - 1)];
-    const int pre2 = list[min((nb2 + 2) >> (spb - 1), p.kmax - 1)];
+    const float fka = sld(skh, ja1), fva = sld(svh, ja1), fkb = sld(skh, jb1), fvb = sld(svh, jb1);
+    const int pre1 = sld(list, (uint32_t)min((nb2 + 1) >> (spb - 1), p.kmax - 1));
+    const int pre2 = sld(list, (uint32_t)min((nb2 + 2) >> (spb - 1), p.kmax - 1));
     wait_lgkm0();
     barrier_keep_loads();  // every wave holds its K fragments: kc is free
     dma_pair(kc, kr, koff, ta2, tb2);
