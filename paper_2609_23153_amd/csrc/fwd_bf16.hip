@@ -10,11 +10,12 @@
 //    staging registers, no VALU), rows past the sequence end reading zero
 //    through the buffer range check.  Both are stored row-major with a
 //    16-byte-chunk XOR swizzle chosen on the global side.
-//  * Each step first reads its whole K and V fragments from LDS into
-//    registers; after one barrier both buffers are free and immediately
-//    receive K(n+3) and V(n+2).  A K tile thus has three steps and a V tile
-//    two to arrive, from 80 KB of LDS per workgroup (K triple-, V double-
-//    buffered): enough bytes in flight to cover L2 latency under load.
+//  * K is double- and V triple-buffered (80 KB of LDS per workgroup).  Step n
+//    first refills the V buffer step n-1 read with V(n+2), then reads its K
+//    fragments into registers; after one barrier the K buffer is free and
+//    receives K(n+2), and the V^T fragments of step n are read while the S
+//    products run.  A K tile has about a step and a half, a V tile two, to
+//    arrive: enough bytes in flight to cover L2 latency under load.
 //  * Wave w owns query rows 32*(w&1)..+31 and keys 32*(w>>1)..+31 of a tile:
 //      S^T (32 keys x 32 queries) = K_half . Q_half^T   8 x v_mfma_f32_32x32x16_bf16
 //      O^T (128 x 32)          += V_half^T . P^T       8 x v_mfma_f32_32x32x16_bf16

@@ -306,16 +306,17 @@ __global__ __launch_bounds__(256) void topk_row_kernel(const double* __restrict_
   // never more than the candidates
   const int k = min(k_per_row ? __builtin_amdgcn_readfirstlane(cnt[row]) : k_all, jhi - jlo);
   const double* s = scores + (int64_t)row * nb;
+  // Keys outside [jlo, jhi) are 0.  Every threshold below is >= 1 (a high
+  // word of some lane's nonzero maximum), so they never pass a ">= P" test
+  // and the fast path needs no separate membership flags.
   uint32_t hi[KPL], lo[KPL];
-  bool valid[KPL];
   int jj[KPL];
   uint32_t mhi = 0;  // high word of this lane's largest key (0: none)
 #pragma unroll
   for (int t = 0; t < KPL; ++t) {
     const int j = lane + kWave * t;
     jj[t] = j;
-    valid[t] = j >= jlo && j < jhi;
-    const uint64_t key = valid[t] ? order_key(s[j]) : 0ull;
+    const uint64_t key = (j >= jlo && j < jhi) ? order_key(s[j]) : 0ull;
     hi[t] = (uint32_t)(key >> 32);
     lo[t] = (uint32_t)key;
     mhi = max(mhi, hi[t]);
@@ -331,7 +332,7 @@ __global__ __launch_bounds__(256) void topk_row_kernel(const double* __restrict_
     bool ex;
     P = kth_largest32<1>(mv, mm, k, &ex);
 #pragma unroll
-    for (int t = 0; t < KPL; ++t) c += __popcll(__ballot(valid[t] && hi[t] >= P));
+    for (int t = 0; t < KPL; ++t) c += __popcll(__ballot(hi[t] >= P));
     fast = c <= kWave;
   }
   if (fast) {
@@ -340,7 +341,7 @@ __global__ __launch_bounds__(256) void topk_row_kernel(const double* __restrict_
     int base = 0;
 #pragma unroll
     for (int t = 0; t < KPL; ++t) {
-      const bool ok = valid[t] && hi[t] >= P;
+      const bool ok = hi[t] >= P;
       const uint64_t m = __ballot(ok);
       if (ok) {
         const int pos = base + __popcll(m & below);
@@ -358,6 +359,9 @@ __global__ __launch_bounds__(256) void topk_row_kernel(const double* __restrict_
     const bool cv[1] = {lane < c};
     select_emit<1>(ch, cl, cv, cj, k, out);
   } else {
+    bool valid[KPL];
+#pragma unroll
+    for (int t = 0; t < KPL; ++t) valid[t] = jj[t] >= jlo && jj[t] < jhi;
     select_emit<KPL>(hi, lo, valid, jj, k, out);
   }
   for (int p = k + lane; p < kmax; p += kWave) out[p] = -1;
