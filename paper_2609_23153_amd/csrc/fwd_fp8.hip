@@ -172,7 +172,12 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
   const int wv = __builtin_amdgcn_readfirstlane(wave);
   auto dma_pair = [&](uint8_t* dst, __amdgpu_buffer_rsrc_t r, const uint32_t (&off)[2], int a0,
                       int b0) {
-    const uint32_t base = lds_addr(dst) + (uint32_t)(16 * wv) * kRowBytes;
+    // the wave's row offset passes through an opaque move, so the compiler
+    // adds the constant buffer offsets per copy instead of holding every
+    // (buffer, copy) address live across the loop
+    uint32_t wrow;
+    asm volatile("s_mov_b32 %0, %1" : "=s"(wrow) : "s"((uint32_t)(16 * wv) * kRowBytes));
+    const uint32_t base = lds_addr(dst) + wrow;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -181,17 +186,18 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
               (uint32_t)(t ? b0 : a0) * kRowBytes);
   };
 
-  // Pair cursor: pairs P0 (being computed), P1 and P2 as tile indices
-  // (na*, nb*), start rows (ta*, tb*; N when missing: such tiles read zeros
-  // and all their keys are masked) and key blocks (ja*, jb*).  The list
-  // entries after P2 and the scales of P1 are read one step ahead.
+  // Pair cursor: pairs P0 (being computed), P1 and P2 as start rows (ta*,
+  // tb*; N when missing: such tiles read zeros and all their keys are
+  // masked, and the loop ends when P0 has no first tile) and key blocks (ja*,
+  // jb*); nb2 is the list position of the last tile taken.  The list entries
+  // after P2 and the scales of P1 are read one step ahead.
   auto block_of = [&](int n) { return n < total ? sld(list, (uint32_t)(n >> (spb - 1))) : 0; };
   int ta0 = p.N, tb0 = p.N, ta1 = p.N, tb1 = p.N, ta2 = p.N, tb2 = p.N;
-  int na0 = next_tile(list, 0, total, spb, p.block, p.nb, p.N, &ta0);
-  int nb0 = next_tile(list, na0 + 1, total, spb, p.block, p.nb, p.N, &tb0);
-  int na1 = next_tile(list, nb0 + 1, total, spb, p.block, p.nb, p.N, &ta1);
-  int nb1 = next_tile(list, na1 + 1, total, spb, p.block, p.nb, p.N, &tb1);
-  int na2 = next_tile(list, nb1 + 1, total, spb, p.block, p.nb, p.N, &ta2);
+  const int na0 = next_tile(list, 0, total, spb, p.block, p.nb, p.N, &ta0);
+  const int nb0 = next_tile(list, na0 + 1, total, spb, p.block, p.nb, p.N, &tb0);
+  const int na1 = next_tile(list, nb0 + 1, total, spb, p.block, p.nb, p.N, &ta1);
+  const int nb1 = next_tile(list, na1 + 1, total, spb, p.block, p.nb, p.N, &tb1);
+  const int na2 = next_tile(list, nb1 + 1, total, spb, p.block, p.nb, p.N, &ta2);
   int nb2 = next_tile(list, na2 + 1, total, spb, p.block, p.nb, p.N, &tb2);
   int ja1 = block_of(na1), jb1 = block_of(nb1);
   int ja2 = block_of(na2), jb2 = block_of(nb2);
@@ -396,12 +402,8 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
                                                            kPScaleInvE8m0);
 
     // advance the cursor
-    na0 = na1;
-    nb0 = nb1;
     ta0 = ta1;
     tb0 = tb1;
-    na1 = na2;
-    nb1 = nb2;
     ta1 = ta2;
     tb1 = tb2;
     ja1 = ja2;
@@ -411,11 +413,11 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
     sk_b = e8m0(fkb);
     sv_b = e8m0(fvb);
     const int prev = nb2;
-    na2 = advance(prev + 1, pre1, &ta2, &ja2);
-    if (na2 == prev + 1) {
-      nb2 = advance(na2 + 1, pre2, &tb2, &jb2);
+    const int n2 = advance(prev + 1, pre1, &ta2, &ja2);
+    if (n2 == prev + 1) {
+      nb2 = advance(n2 + 1, pre2, &tb2, &jb2);
     } else {
-      nb2 = next_tile(list, na2 + 1, total, spb, p.block, p.nb, p.N, &tb2);
+      nb2 = next_tile(list, n2 + 1, total, spb, p.block, p.nb, p.N, &tb2);
       jb2 = block_of(nb2);
     }
     // keep the whole pair's work ahead of the wait
@@ -424,17 +426,17 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
     barrier_keep_loads();  // also: every wave is done reading vc
   };
   // step n reads K pair buffer n%2 and V pair buffer n%3, refills V (n+2)%3
-  while (na0 < total) {
+  while (ta0 < p.N) {
     step(kp0, vp0, vp2);
-    if (na0 >= total) break;
+    if (ta0 >= p.N) break;
     step(kp1, vp1, vp0);
-    if (na0 >= total) break;
+    if (ta0 >= p.N) break;
     step(kp0, vp2, vp1);
-    if (na0 >= total) break;
+    if (ta0 >= p.N) break;
     step(kp1, vp0, vp2);
-    if (na0 >= total) break;
+    if (ta0 >= p.N) break;
     step(kp0, vp1, vp0);
-    if (na0 >= total) break;
+    if (ta0 >= p.N) break;
     step(kp1, vp2, vp1);
   }
   wait_vm0();
