@@ -45,6 +45,22 @@ constexpr int kCtStride = 72;           // bf16 per C^T row in LDS (64 + 8 paddi
 typedef __attribute__((__vector_size__(4 * sizeof(short)))) short i16x4;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+// Two fp32 values as packed bf16, rounded to nearest even by the hardware
+// conversion (v_cvt_pk_bf16_f32): one instruction per pair.
+typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2_t;
+__device__ __forceinline__ uint32_t cvt_pk_bf16(float lo, float hi) {
+  const bf16x2_t t = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, t);
+}
+
+// x0, x1 split as packed bf16 hi and lo pairs {hi, lo}: hi = bf16(x),
+// lo = bf16(x - hi) (the hi values unpack to fp32 exactly by a shift and a
+// mask).
+__device__ __forceinline__ u32x2 split_pair(float x0, float x1) {
+  const uint32_t hw = cvt_pk_bf16(x0, x1);
+  return u32x2{hw, cvt_pk_bf16(x0 - bf16_lo(hw), x1 - bf16_hi(hw))};
+}
+
 // silu(x) = x sigmoid(x), the reciprocal by v_rcp_f32 (1 ulp) rather than
 // a full-precision division
 __device__ __forceinline__ float silu(float x) {
@@ -211,13 +227,9 @@ __global__ __launch_bounds__(256, 2) void comp_state_kernel(StateArgs a) {
         u32x2 wh, wl;
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
-          const __bf16 h0 = (__bf16)rv[2 * u], h1 = (__bf16)rv[2 * u + 1];
-          const __bf16 l0 = (__bf16)(rv[2 * u] - (float)h0);
-          const __bf16 l1 = (__bf16)(rv[2 * u + 1] - (float)h1);
-          wh[u] = (uint32_t)__builtin_bit_cast(uint16_t, h0) |
-                  ((uint32_t)__builtin_bit_cast(uint16_t, h1) << 16);
-          wl[u] = (uint32_t)__builtin_bit_cast(uint16_t, l0) |
-                  ((uint32_t)__builtin_bit_cast(uint16_t, l1) << 16);
+          const u32x2 hl = split_pair(rv[2 * u], rv[2 * u + 1]);
+          wh[u] = hl[0];
+          wl[u] = hl[1];
         }
         // r = 32 nb + 8 j + 4 g .. +3: bytes 64 nb + 16 j + 8 g of the row
         const int c = 4 * nb + j;
@@ -469,7 +481,7 @@ __global__ __launch_bounds__(256, 2) void comp_out_kernel(OutArgs a) {
       }
     }
     // silu and rotation; q~^T as B operand split hi + lo, k-step s: indices 16 s + 4 g + rr, 16 s + 8 + 4 g + rr
-    bf16x8 qt[4], ql[4];
+    u32x4 qtw[4], qlw[4];  // packed bf16 pairs
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
@@ -485,10 +497,10 @@ __global__ __launch_bounds__(256, 2) void comp_out_kernel(OutArgs a) {
         const int s2 = 2 * rb + (j >> 1), half = 4 * (j & 1);
         const float rv[4] = {r0, r1, r2, r3};
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const __bf16 hi = (__bf16)rv[u];
-          qt[s2][half + u] = hi;
-          ql[s2][half + u] = (__bf16)(rv[u] - (float)hi);
+        for (int u = 0; u < 2; ++u) {
+          const u32x2 hl = split_pair(rv[2 * u], rv[2 * u + 1]);
+          qtw[s2][half / 2 + u] = hl[0];
+          qlw[s2][half / 2 + u] = hl[1];
         }
       }
 
@@ -504,9 +516,9 @@ __global__ __launch_bounds__(256, 2) void comp_out_kernel(OutArgs a) {
       for (int s2 = 0; s2 < 4; ++s2) {
         const bf16x8 cf = as_bf16x8(*reinterpret_cast<const u32x4*>(crow + 16 * s2 + 8 * fg));
         const bf16x8 cl = as_bf16x8(*reinterpret_cast<const u32x4*>(clrow + 16 * s2 + 8 * fg));
-        y[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cl, qt[s2], y[dt], 0, 0, 0);
-        y[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cf, ql[s2], y[dt], 0, 0, 0);
-        y[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cf, qt[s2], y[dt], 0, 0, 0);
+        y[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cl, as_bf16x8(qtw[s2]), y[dt], 0, 0, 0);
+        y[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cf, as_bf16x8(qlw[s2]), y[dt], 0, 0, 0);
+        y[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cf, as_bf16x8(qtw[s2]), y[dt], 0, 0, 0);
       }
     }
 
@@ -520,7 +532,9 @@ __global__ __launch_bounds__(256, 2) void comp_out_kernel(OutArgs a) {
         osw[dt][2 * jp] = u32x2{w[0], w[1]};
         osw[dt][2 * jp + 1] = u32x2{w[2], w[3]};
       }
-    float ss_y = 0.f, ss_o = 0.f;
+    // sums of squares in four independent partials each (short dependency
+    // chains)
+    float py[4] = {0.f, 0.f, 0.f, 0.f}, po[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -529,10 +543,12 @@ __global__ __launch_bounds__(256, 2) void comp_out_kernel(OutArgs a) {
         const float o4[4] = {bf16_lo(w[0]), bf16_hi(w[0]), bf16_lo(w[1]), bf16_hi(w[1])};
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          ss_y = fmaf(y[dt][4 * j + u], y[dt][4 * j + u], ss_y);
-          ss_o = fmaf(o4[u], o4[u], ss_o);
+          py[u] = fmaf(y[dt][4 * j + u], y[dt][4 * j + u], py[u]);
+          po[u] = fmaf(o4[u], o4[u], po[u]);
         }
       }
+    float ss_y = (py[0] + py[1]) + (py[2] + py[3]);
+    float ss_o = (po[0] + po[1]) + (po[2] + po[3]);
     ss_y += __shfl_xor(ss_y, 32, kWave);
     ss_o += __shfl_xor(ss_o, 32, kWave);
     const float rstd = 1.f / sqrtf(ss_y * (1.f / kHeadDim) + a.eps);
@@ -555,8 +571,8 @@ __global__ __launch_bounds__(256, 2) void comp_out_kernel(OutArgs a) {
             float x[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) x[u] = fmaf(coef * y[dt][4 * j + u], gm[u], o4[u]);
-            wo[2 * jj] = pack_bf16x2(x[0], x[1]);
-            wo[2 * jj + 1] = pack_bf16x2(x[2], x[3]);
+            wo[2 * jj] = cvt_pk_bf16(x[0], x[1]);
+            wo[2 * jj + 1] = cvt_pk_bf16(x[2], x[3]);
           }
           // back to 8 contiguous channels per lane: 32 dt + 16 jp + 8 g ..
           st16(orow + 32 * dt + 16 * jp + 8 * g, swap_quads(wo));

@@ -31,6 +31,14 @@
 namespace sa {
 namespace {
 
+// Two fp32 values as packed bf16, rounded to nearest even by the hardware
+// conversion (v_cvt_pk_bf16_f32): one instruction per pair.
+__device__ __forceinline__ uint32_t cvt_pk_bf16(float lo, float hi) {
+  typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2_t;
+  const bf16x2_t t = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, t);
+}
+
 // ---- per-row quantisation --------------------------------------------------
 
 constexpr int kRowsPerGroup = 4;  // one row per wave
@@ -466,8 +474,8 @@ __global__ __launch_bounds__(256) void linear_w8a8_kernel(LinArgs a) {
 #pragma unroll
             for (int u = 0; u < 4; ++u) v[u] = fmaf(acc[i][jj][4 * q + u] * sxv, swv[u], bv[u]);
             u32x2 o;
-            o[0] = pack_bf16x2(v[0], v[1]);
-            o[1] = pack_bf16x2(v[2], v[3]);
+            o[0] = cvt_pk_bf16(v[0], v[1]);
+            o[1] = cvt_pk_bf16(v[2], v[3]);
             const int c = 4 * i2 + q;  // chunk of 8 channels within the 64
             *reinterpret_cast<u32x2*>(stg + l32e * 128 + ((c ^ (l32e & 7)) << 4) + 8 * ge) = o;
           }
