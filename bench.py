@@ -101,7 +101,8 @@ def selected_flops(cnt, idx, N, block, d):
     sizes[-1] = N - (nb - 1) * block
     kmax = idx.shape[-1]
     valid = np.arange(kmax)[None, None, None, :] < cnt[..., None]
-    nj = np.where(valid & (idx >= 0), sizes[np.clip(idx, 0, nb - 1)], 0).sum(-1)  # [B,H,nb]
+    ok = valid & (idx >= 0) & (idx < nb)  # entries the kernels skip add nothing
+    nj = np.where(ok, sizes[np.clip(idx, 0, nb - 1)], 0).sum(-1)  # [B,H,nb]
     return int(4 * d * (nj * sizes[None, None, :]).sum())
 
 
