@@ -5,15 +5,15 @@ The order is a permutation of the tiles t = (b*H + h) * ceil(L/64) + row/64:
 first a stable sort by cost class descending, where a tile's cost is the
 number of 64-key tiles its query block attends (list length times block/64)
 and its class is 0 for no work, else bit_length(cost) capped at 15; then launch
-slot s takes sorted position p(s), which hands each of the 8 XCDs runs of 64
-consecutive positions: with G tiles and groups of 8*64 slots, for s inside the
-whole groups p(s) = (s//8 // 64) * 512 + (s % 8) * 64 + (s//8) % 64, and
-p(s) = s for the slots of the last partial group.
+slot s takes sorted position p(s), which hands each of the 8 XCDs runs of 256
+consecutive positions: with G tiles and groups of 8*256 slots, for s inside
+the whole groups p(s) = (s//8 // 256) * 2048 + (s % 8) * 256 + (s//8) % 256,
+and p(s) = s for the slots of the last partial group.
 """
 import numpy as np
 
 XCDS = 8
-RUN = 64
+RUN = 256
 
 
 def cost_class(tiles: int) -> int:

@@ -22,7 +22,7 @@ namespace {
 
 constexpr int kClasses = 16;
 constexpr int kXcds = 8;
-constexpr int kRun = 64;           // consecutive list positions handed to one XCD
+constexpr int kRun = 256;          // consecutive list positions handed to one XCD
 constexpr int kChunk = 1024;       // tiles per counting / scatter workgroup
 constexpr int kSortThreads = 256;  // 4 waves x 4 rounds of 64 tiles
 constexpr int kScanThreads = 1024;

@@ -392,8 +392,10 @@ def test_launch_order_definition_small_cases():
     # block 128: one list per two 64-row tiles, cost doubled; cnt clamped to kmax
     cnt = np.array([[[5, 1]]])
     assert launch_order(cnt, 2, 256, 128).tolist() == [0, 1, 2, 3]
-    # XCD interleave over one full group of 512 uniform tiles
-    cnt = np.full((1, 1, 512), 1)
-    o = launch_order(cnt, 1, 512 * 64, 64)
-    assert sorted(o.tolist()) == list(range(512))
-    assert o[:9].tolist() == [0, 64, 128, 192, 256, 320, 384, 448, 1]
+    # XCD interleave over one full group of 8 x 256 uniform tiles: slot s
+    # goes to XCD s % 8, which walks its own run of 256 consecutive tiles
+    cnt = np.full((1, 1, 2048), 1)
+    o = launch_order(cnt, 1, 2048 * 64, 64)
+    assert sorted(o.tolist()) == list(range(2048))
+    assert o[:9].tolist() == [0, 256, 512, 768, 1024, 1280, 1536, 1792, 1]
+    assert o[8 * 255 + 7] == 7 * 256 + 255
