@@ -49,6 +49,16 @@ __device__ __forceinline__ uint32_t cvt_bf16x2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, t);
 }
 
+// Work item of workgroup `slot` among G: each XCD (slot % 8) walks runs of
+// 64 consecutive items, so tiles whose operands overlap share that XCD's L2;
+// the slots of the last partial group keep their own item.
+__device__ __forceinline__ int xcd_item(int slot, int G) {
+  constexpr int kRunB = 64, kGroup = 8 * kRunB;
+  if (slot >= (G / kGroup) * kGroup) return slot;
+  const int r = slot >> 3;
+  return (r / kRunB) * kGroup + (slot & 7) * kRunB + r % kRunB;
+}
+
 // 16-byte chunk c of tile row r sits at slot c ^ (r & 15).
 __device__ __forceinline__ int swz(int row, int c) { return c ^ (row & 15); }
 
@@ -246,8 +256,9 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
   __shared__ __attribute__((aligned(1024))) uint8_t vb0[kTileBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t vb1[kTileBytes];
 
-  const int bh = blockIdx.x / p.ntiles;
-  const int qt = blockIdx.x - bh * p.ntiles;
+  const int item = xcd_item((int)blockIdx.x, (int)gridDim.x);
+  const int bh = item / p.ntiles;
+  const int qt = item - bh * p.ntiles;
   const int b = bh / p.H, h = bh - b * p.H;
   const int q0 = qt * kTile;
   const int iblk = q0 / p.block;
@@ -456,8 +467,9 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p) {
   __shared__ __attribute__((aligned(1024))) uint8_t pbuf[4 * kPBlock];
   __shared__ __attribute__((aligned(1024))) uint8_t sbuf[4 * kPBlock];
 
-  const int bh = blockIdx.x / p.ntiles;
-  const int kt0 = blockIdx.x - bh * p.ntiles;
+  const int item = xcd_item((int)blockIdx.x, (int)gridDim.x);
+  const int bh = item / p.ntiles;
+  const int kt0 = item - bh * p.ntiles;
   const int b = bh / p.H, h = bh - b * p.H;
   const int k0 = kt0 * kTile;
   const int jblk = k0 / p.block;
