@@ -37,7 +37,7 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
 
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "fwd_bf16_wan14b_720p_hbm_traffic.txt")
-FWD_BF16_SOURCES = ("fwd_bf16.hip", "common.h", "launch.h")
+FWD_BF16_SOURCES = ("fwd_bf16.hip", "common.h", "launch.h", "sched.hip")  # sched.hip: the launch order
 
 
 def measured_traffic(workload):
