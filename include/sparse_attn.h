@@ -143,10 +143,16 @@ int64_t sparse_attn_num_tiles(const sparse_attn_desc* desc);
  * Work scheduling for the fused forward (ragged per-query-block work, the
  * selection lists of §2 Eq. comp-sparse being of unequal length in general).
  * Writes the launch order of the B*H*ceil(L/64) query tiles (tile t = (b*H +
- * h) * ceil(L/64) + row/64): tiles sorted by cost class floor(log2(key tiles))
- * descending (longest first; stable, so equal-cost tiles keep raster order),
- * then interleaved so that each XCD of the device receives runs of
- * consecutive tiles.  Every tile appears exactly once.
+ * h) * ceil(L/64) + row/64), a permutation of them.  The tiles are sorted by
+ * cost class descending (longest first; stable, so equal classes keep raster
+ * order), the class of a tile being 0 when its query block attends no key
+ * tile and min(bit_length(key tiles), 15) otherwise, key tiles = 64-key tiles
+ * = list length * block / 64.  Launch slot s then takes sorted position p(s),
+ * which hands each XCD (slot mod 8) runs of 256 consecutive positions: in
+ * groups of 2048 slots, p(s) = 2048 * (s / 2048) + 256 * (s mod 8) +
+ * (s mod 2048) / 8, and the slots of a last partial group keep p(s) = s.
+ * Only performance depends on the order: the forward's results are the same
+ * bits with any order (or none).
  *  cnt     int32 [B][H][nqb] list lengths (clamped to [0, kmax])
  *  order   int32 [sparse_attn_num_tiles(desc)] out
  *  ws      ws_bytes >= sparse_attn_workspace_size(SA_OP_SCHEDULE)
@@ -266,7 +272,9 @@ int sparse_attn_comp_out(const sparse_attn_desc* desc, int32_t rank, const void*
  *  dq, dk, dv        bf16 out, laid out like q, k, v (desc strides)
  *  ws                ws_bytes >= sparse_attn_workspace_size(SA_OP_BWD)
  * Errors: SA_ERR_INVALID_ARG for null or misaligned pointers and bad
- * strides or lists; SA_ERR_WORKSPACE. */
+ * strides or lists; SA_ERR_UNSUPPORTED when a head of q, k, v or o spans
+ * 4 GiB or more ((seqlen + 64) * token stride * 2 bytes, the kernels' 32-bit
+ * row offsets); SA_ERR_WORKSPACE. */
 int sparse_attn_bwd(const sparse_attn_desc* desc, const void* q, const void* k, const void* v,
                     const void* o, const void* d_o, const float* lse, const int32_t* idx,
                     const int32_t* cnt, int32_t kmax, void* dq, void* dk, void* dv, void* ws,

@@ -23,7 +23,11 @@ __all__ = [
     "sparse_attn_quant_rows_fp8", "sparse_attn_linear_w8a8", "sparse_attn_bwd", "SA_OP_BWD",
 ]
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsparseattn.so")
+# SPARSE_ATTN_LIB names another build of the same library (the CPU sanitizer
+# build of the host layer that the argument-check tests run under); by
+# default the in-tree gfx950 build is loaded.
+LIB_PATH = os.environ.get("SPARSE_ATTN_LIB") or os.path.join(
+    os.path.dirname(os.path.abspath(__file__)), "libsparseattn.so")
 
 SA_SELECT_ROW_TOPK = 0
 SA_SELECT_HEAD_TOPK = 1

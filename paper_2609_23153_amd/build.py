@@ -55,5 +55,47 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
     return LIB
 
 
+SANITIZED_LIB = os.path.join(OUT_DIR, "asan", "libsparseattn_host_asan.so")
+
+
+def asan_runtime() -> str:
+    """The compiler's shared AddressSanitizer runtime (preloaded into the
+    Python process that loads the sanitized library)."""
+    res = _run([HIPCC, "-print-file-name=libclang_rt.asan-x86_64.so"]).strip().splitlines()
+    path = res[-1].strip() if res else ""
+    if not os.path.exists(path):
+        import glob
+        hits = glob.glob("/opt/rocm/llvm/lib/clang/*/lib/linux/libclang_rt.asan-x86_64.so")
+        path = hits[0] if hits else ""
+    if not path:
+        raise RuntimeError("no shared AddressSanitizer runtime found")
+    return path
+
+
+def build_host_sanitized(jobs: int = 8) -> str:
+    """Build of every source with AddressSanitizer and
+    UndefinedBehaviorSanitizer on the host code only (the gfx950 device code
+    is built as usual, without them): the CPU build under which the
+    argument-check tests of the C ABI run."""
+    out = os.path.dirname(SANITIZED_LIB)
+    os.makedirs(out, exist_ok=True)
+    san = ["-Xarch_host", "-fsanitize=address,undefined",
+           "-Xarch_host", "-fno-sanitize-recover=undefined",
+           "-Xarch_host", "-fno-omit-frame-pointer", "-shared-libsan"]
+    flags = [f for f in FLAGS if f != "-O3"] + ["-O1", "-g"]
+
+    def compile_one(src):
+        obj = os.path.join(out, src.replace(".hip", ".o"))
+        _run([HIPCC, *flags, *san, "-c", os.path.join(CSRC, src), "-o", obj])
+        return obj
+
+    with ThreadPoolExecutor(max_workers=jobs) as ex:
+        objs = list(ex.map(compile_one, SOURCES))
+    tmp = SANITIZED_LIB + ".tmp"
+    _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *san, *objs, "-o", tmp])
+    os.replace(tmp, SANITIZED_LIB)
+    return SANITIZED_LIB
+
+
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))

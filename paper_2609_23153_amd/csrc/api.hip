@@ -285,6 +285,11 @@ int sparse_attn_bwd(const sparse_attn_desc* desc, const void* q, const void* k, 
       !strides_ok(desc->v_stride) || !strides_ok(desc->o_stride))
     return SA_ERR_INVALID_ARG;
   if ((st = check_lists(s, idx, cnt, kmax)) != SA_OK) return st;
+  // the backward kernels address q, k, v, o and d_o rows of one head with
+  // 32-bit byte offsets, as the forward does
+  if (!offsets_fit(s, desc->q_stride, 2) || !offsets_fit(s, desc->k_stride, 2) ||
+      !offsets_fit(s, desc->v_stride, 2) || !offsets_fit(s, desc->o_stride, 2))
+    return SA_ERR_UNSUPPORTED;
   if (ws_bytes < sa::bwd_workspace_bytes(s)) return SA_ERR_WORKSPACE;
   sa::BwdIn in{};
   in.q = q;

@@ -61,3 +61,48 @@ def check_out(o_gpu, lse_gpu, o_ref, lse_ref, rows=None, rel=BF16_REL_L2, mabs=B
         assert np.array_equal(np.isneginf(lse), np.isneginf(lse_ref)), what
         if fin.any():
             assert np.abs(lse[fin] - lse_ref[fin]).max() <= LSE_ABS, what
+
+
+# ---- the library's launch order (its own definition, stated in the header of
+# sparse_attn_schedule; the paper fixes no order: only performance depends on
+# it) -------------------------------------------------------------------------
+XCD_RUN, XCDS = 256, 8
+
+
+def sorted_position(s, G):
+    """Sorted position taken by launch slot s of G (runs of 256 per XCD)."""
+    group = XCDS * XCD_RUN
+    if s >= (G // group) * group:
+        return s
+    return group * (s // group) + XCD_RUN * (s % XCDS) + (s % group) // XCDS
+
+
+def tile_classes(cnt, kmax, seqlen, block):
+    """Cost class of every query tile t = (b*H + h) * ceil(L/64) + row/64."""
+    cnt = np.asarray(cnt)
+    B, H, nb = cnt.shape
+    ntiles = -(-seqlen // 64)
+    t = np.arange(B * H * ntiles)
+    bh, qt = t // ntiles, t % ntiles
+    c = np.clip(cnt.reshape(-1)[bh * nb + (qt * 64) // block], 0, kmax)
+    tiles = c * (block // 64)
+    bits = np.zeros_like(tiles)
+    nz = tiles > 0
+    bits[nz] = np.floor(np.log2(tiles[nz])).astype(np.int64) + 1
+    return np.minimum(bits, 15)
+
+
+def check_launch_order(order, cnt, kmax, seqlen, block, what=""):
+    """Properties of a launch order: a permutation of every query tile; read
+    back in sorted position (the XCD interleave undone), cost classes do not
+    increase, and tiles of one class keep raster order."""
+    order = np.asarray(order, dtype=np.int64)
+    G = order.size
+    assert np.array_equal(np.sort(order), np.arange(G)), (what, "not a permutation")
+    pos = np.array([sorted_position(s, G) for s in range(G)], dtype=np.int64)
+    seq = np.empty(G, dtype=np.int64)
+    seq[pos] = order
+    cls = tile_classes(cnt, kmax, seqlen, block)[seq]
+    assert np.all(np.diff(cls) <= 0), (what, "classes increase along sorted positions")
+    same = np.diff(cls) == 0
+    assert np.all(np.diff(seq)[same] > 0), (what, "equal classes out of raster order")

@@ -249,3 +249,46 @@ def test_causal_window_fields_are_checked():
         assert lib.sparse_attn_workspace_size(ctypes.byref(ds), sa.SA_OP_COMP_STATE, 1) == \
             base // 4 * parts
     assert ctypes.sizeof(sa.SparseAttnDesc) == 136   # the C struct with the two int32 fields
+
+
+def test_bwd_rejects_bad_arguments():
+    lib = sa.library()
+    ds = desc()
+    need = lib.sparse_attn_workspace_size(ctypes.byref(ds), sa.SA_OP_BWD, 7)
+    assert need > 0
+
+    def call(d=ds, **kw):
+        names = ("q", "k", "v", "o", "do", "lse", "idx", "cnt", "kmax", "dq", "dk", "dv", "ws",
+                 "wsb")
+        args = dict(zip(names, (P, P, P, P, P, P, P, P, 7, P, P, P, P, need)))
+        args.update(kw)
+        return lib.sparse_attn_bwd(ctypes.byref(d), *[args[n] for n in names], None)
+
+    assert call(q=None) == -1                     # null input
+    assert call(do=None) == -1                    # null upstream gradient
+    assert call(lse=None) == -1                   # null LSE
+    assert call(dv=None) == -1                    # null output
+    assert call(ws=None) == -1                    # null workspace
+    assert call(idx=None) == -1                   # null list
+    assert call(kmax=0) == -1                     # kmax 0
+    assert call(dk=MIS) == -1                     # misaligned output
+    assert call(o=MIS) == -1                      # misaligned forward output
+    assert call(wsb=need - 1) == -3               # workspace too small
+    bad = desc()
+    bad.o_stride[2] = 132                         # token stride not a multiple of 8
+    assert call(d=bad) == -1
+    bad = desc(d=64)
+    assert call(d=bad) == -2                      # head_dim
+    # a token-major layout whose head spans >= 4 GiB: (N + 64) * stride * 2
+    # bytes past the 32-bit row offsets of the kernels
+    for f in ("q_stride", "k_stride", "v_stride", "o_stride"):
+        big = desc(N=75600)
+        getattr(big, f)[2] = 28416                # (75600 + 64) * 28416 * 2 >= 2^32
+        wsb = lib.sparse_attn_workspace_size(ctypes.byref(big), sa.SA_OP_BWD, 7)
+        assert call(d=big, wsb=wsb) == -2, f
+        getattr(big, f)[2] = 28368                # just inside: passes the range check
+        assert (75600 + 64) * 28368 * 2 + 256 < 1 << 32
+    # the forward rejects the same layouts
+    big = desc(N=75600)
+    big.k_stride[2] = 28416
+    assert lib.sparse_attn_fwd(ctypes.byref(big), P, P, P, P, P, 7, None, P, None, None) == -2

@@ -184,3 +184,53 @@ def test_bwd_causal_full_chunk_equals_unrestricted():
     torch.cuda.synchronize()
     for x, y in zip(a, b):
         assert torch.equal(x.view(torch.int16), y.view(torch.int16))
+
+
+@pytest.mark.parametrize("N", [1064, 4160])
+def test_bwd_block128_tail_sub_tile_past_end(N):
+    """Block 128 with N mod 128 in (0, 64]: the last block's second 64-row
+    sub-tile lies past N for the dQ query tiles and the dK/dV key tiles;
+    lists often include the tail block."""
+    from test_gpu_parity import tail_lists
+    g = torch.Generator().manual_seed(N + 9)
+    q, k, v = (torch.randn(1, 2, N, 128, generator=g).to(torch.bfloat16) for _ in range(3))
+    nb = O.block_count(N, 128)
+    idx, cnt = tail_lists(nb, min(nb, 7), seed=N + 4)
+    do, dq, dk, dv = run_bwd(q, k, v, idx, cnt, 128, 8)
+    check_grads(q, k, v, do, idx, cnt, 128, dq, dk, dv, f"b128 tail N={N}")
+
+
+@pytest.mark.parametrize("N,block,causal", [(1064, 128, (300, 1)), (4160, 128, (1000, 0))])
+def test_bwd_block128_tail_causal(N, block, causal):
+    from test_gpu_parity import tail_lists
+    g = torch.Generator().manual_seed(N + 11)
+    q, k, v = (torch.randn(1, 2, N, 128, generator=g).to(torch.bfloat16) for _ in range(3))
+    kk = O.keep_count(3000, O.block_count(N, block))
+    idx, cnt = sa.sparse_attn_select(q.to(DEV), k.to(DEV), kk, block=block, causal=causal)
+    idx, cnt = idx.cpu(), cnt.cpu()
+    do, dq, dk, dv = run_bwd(q, k, v, idx, cnt, block, 9, causal=causal)
+    check_grads(q, k, v, do, idx, cnt, block, dq, dk, dv, f"b128 tail causal N={N} {causal}",
+                causal=causal)
+
+
+def test_bwd_strided_token_major_layout():
+    """[B, N, H, d] storage viewed as [B, H, N, d] for every input and
+    gradient (strides (N*H*d, d, H*d))."""
+    from test_gpu_parity import tail_lists
+    g = torch.Generator().manual_seed(13)
+    N, H = 1500, 3
+    base = [torch.randn(1, N, H, 128, generator=g).to(torch.bfloat16) for _ in range(4)]
+    q, k, v, do = (t.permute(0, 2, 1, 3) for t in base)
+    nb = O.block_count(N, 64)
+    idx, cnt = tail_lists(nb, 6, seed=14, H=H)
+    qd, kd, vd, dod = (t.to(DEV).permute(0, 2, 1, 3) for t in base)
+    idxd, cntd = idx.to(DEV), cnt.to(DEV)
+    o = torch.empty(1, N, H, 128, dtype=torch.bfloat16, device=DEV).permute(0, 2, 1, 3)
+    o, lse = sa.sparse_attn_fwd(qd, kd, vd, idxd, cntd, o=o)
+    grads = [torch.empty(1, N, H, 128, dtype=torch.bfloat16, device=DEV).permute(0, 2, 1, 3)
+             for _ in range(3)]
+    dq, dk, dv = sa.sparse_attn_bwd(qd, kd, vd, o, dod, lse, idxd, cntd, dq=grads[0],
+                                    dk=grads[1], dv=grads[2])
+    torch.cuda.synchronize()
+    assert dq.stride() == qd.stride()
+    check_grads(q, k, v, do, idx, cnt, 64, dq.cpu(), dk.cpu(), dv.cpu(), "strided [B,N,H,d]")

@@ -151,3 +151,14 @@ def test_causal_full_chunk_equals_unrestricted():
     torch.cuda.synchronize()
     assert torch.equal(i0, i1) and torch.equal(c0, c1)
     assert torch.equal(o0.view(torch.int16), o1.view(torch.int16)) and torch.equal(l0, l1)
+
+
+@pytest.mark.parametrize("N,causal", [(1064, (300, 1)), (4160, (1000, 0)), (8200, (2000, 2))])
+def test_causal_block128_tail_sub_tile_past_end(N, causal):
+    """Block 128 with N mod 128 in (0, 64] under a window: the last block's
+    second 64-token sub-tile lies past N, and chunk boundaries fall inside
+    blocks."""
+    g = torch.Generator().manual_seed(N + 17)
+    q, k, v = (torch.randn(1, 2, N, 128, generator=g).to(torch.bfloat16) for _ in range(3))
+    idx, cnt = select_causal_check(q, k, 128, 3000, causal, f"b128 tail N={N} {causal}")
+    fwd_causal_check(q, k, v, idx, cnt, 128, causal, f"b128 tail fwd N={N} {causal}")

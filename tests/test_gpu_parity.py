@@ -8,8 +8,7 @@ import torch
 import oracle as O
 import paper_2609_23153_amd as sa
 import workloads as W
-from gpu_helpers import check_out, oracle_attend, oracle_select, say, widen
-from oracle.schedule import launch_order
+from gpu_helpers import check_launch_order, check_out, oracle_attend, oracle_select, say, widen
 
 pytestmark = pytest.mark.gpu
 
@@ -124,8 +123,8 @@ def fwd_and_check(q, k, v, idx, cnt, block, what, qblocks=None, heads=None, sche
     if schedule:
         order = sa.sparse_attn_schedule(cnt, q.shape[2], idx.shape[-1], block=block)
         torch.cuda.synchronize()
-        ref = launch_order(cnt.cpu().numpy(), idx.shape[-1], q.shape[2], block)
-        assert np.array_equal(order.cpu().numpy(), ref), what
+        check_launch_order(order.cpu().numpy(), cnt.cpu().numpy(), idx.shape[-1], q.shape[2],
+                           block, what)
     o, lse = sa.sparse_attn_fwd(qd, kd, vd, idx, cnt, block=block, order=order)
     torch.cuda.synchronize()
     o, lse = o.cpu(), lse.cpu()
@@ -151,22 +150,27 @@ def test_fwd_tiny(schedule):
     fwd_and_check(q, k, v, idx, cnt, wl.block, "tiny fwd", schedule=schedule)
 
 
-def test_schedule_large_ragged_matches_definition():
+def test_schedule_large_ragged_properties():
     # 3 x 40 heads x 1182 blocks of ragged lengths: several XCD groups and a
-    # partial tail group
+    # partial tail group; the order is a permutation whose sorted positions
+    # carry non-increasing cost classes, raster order within a class
     rng = np.random.default_rng(21)
     cnt = rng.integers(0, 300, size=(3, 40, 1182)).astype(np.int32)
     cnt[0, 0, :50] = 0
     cntd = torch.from_numpy(cnt).to(DEV)
     order = sa.sparse_attn_schedule(cntd, 75600, 250, block=64)
     torch.cuda.synchronize()
-    ref = launch_order(cnt, 250, 75600, 64)
-    assert np.array_equal(order.cpu().numpy(), ref)
+    check_launch_order(order.cpu().numpy(), cnt, 250, 75600, 64, "ragged b64")
     order = sa.sparse_attn_schedule(cntd[:, :, :591].contiguous(), 75600, 250, block=128)
     with pytest.raises(ValueError):
         sa.sparse_attn_schedule(cntd[:, :, :591], 75600, 250, block=128)
     torch.cuda.synchronize()
-    assert np.array_equal(order.cpu().numpy(), launch_order(cnt[:, :, :591], 250, 75600, 128))
+    check_launch_order(order.cpu().numpy(), cnt[:, :, :591], 250, 75600, 128, "ragged b128")
+    # uniform lists: one class, so the order is the XCD interleave of raster order
+    cnt1 = np.full((1, 40, 1182), 36, dtype=np.int32)
+    order = sa.sparse_attn_schedule(torch.from_numpy(cnt1).to(DEV), 75600, 36, block=64)
+    torch.cuda.synchronize()
+    check_launch_order(order.cpu().numpy(), cnt1, 36, 75600, 64, "uniform")
 
 
 def test_fwd_wan13b_sampled_heads():
@@ -261,3 +265,60 @@ def test_wan14b_full_size_sampled():
                   what=f"wan14b h{h}")
     # property at any size: every output row is finite and LSE finite
     assert torch.isfinite(o).all() and torch.isfinite(lse).all()
+    # raster order (no schedule) gives the same bits
+    o0, l0 = sa.sparse_attn_fwd(qd, kd, vd, idx, cnt)
+    torch.cuda.synchronize()
+    assert torch.equal(o0.cpu().view(torch.int16), o.cpu().view(torch.int16))
+    assert torch.equal(l0.cpu().view(torch.int32), lse.cpu().view(torch.int32))
+    check_launch_order(order.cpu().numpy(), cnt_c, kk, wl.seqlen, wl.block, "wan14b")
+
+
+# ---------------------------------------------------- block-128 tail blocks
+def tail_lists(nb, kmax, seed, B=1, H=2):
+    """Random ragged lists (about 10% empty) in which a third of the rows
+    list the last key block, so the tail block is walked often."""
+    idx = np.full((B, H, nb, kmax), -1, dtype=np.int32)
+    cnt = np.zeros((B, H, nb), dtype=np.int32)
+    for b in range(B):
+        for h in range(H):
+            ii, cc = W.random_block_lists(nb, nb, kmax, seed=seed + 10 * b + h, p_empty=0.1)
+            for i in range(0, nb, 3):
+                if cc[i] > 0 and nb - 1 not in ii[i, :cc[i]]:
+                    ii[i, cc[i] - 1] = nb - 1
+                    ii[i, :cc[i]] = np.sort(ii[i, :cc[i]])
+            idx[b, h], cnt[b, h] = ii, cc
+    return torch.from_numpy(idx), torch.from_numpy(cnt)
+
+
+@pytest.mark.parametrize("N", [1064, 4160, 8200])
+def test_fwd_block128_tail_sub_tile_past_end(N):
+    """Block 128 with N mod 128 in (0, 64]: the last block's second 64-row
+    sub-tile lies wholly past N (as query tile and as key tile), so the tile
+    cursors skip it; tails of 40, 64 and 8 tokens."""
+    assert 0 < N % 128 <= 64
+    g = torch.Generator().manual_seed(N)
+    q, k, v = (torch.randn(1, 2, N, 128, generator=g).to(torch.bfloat16) for _ in range(3))
+    nb = O.block_count(N, 128)
+    idx, cnt = tail_lists(nb, min(nb, 7), seed=N)
+    idx, cnt = idx.to(DEV), cnt.to(DEV)
+    for sched in (True, False):
+        fwd_and_check(q, k, v, idx, cnt, 128, f"b128 tail N={N} sched={sched}", schedule=sched)
+
+
+@pytest.mark.parametrize("N,block", [(1000, 64), (4160, 128), (3000, 64)])
+def test_fwd_order_does_not_change_results(N, block):
+    """The launch order only moves work between CUs: outputs and LSE with the
+    scheduled order and with raster order (order = NULL) are the same bits,
+    on ragged lists with empty rows and a tail block."""
+    g = torch.Generator().manual_seed(N + 3 * block)
+    q, k, v = (torch.randn(2, 3, N, 128, generator=g).to(torch.bfloat16).to(DEV)
+               for _ in range(3))
+    nb = O.block_count(N, block)
+    idx, cnt = tail_lists(nb, min(nb, 9), seed=N + 1, B=2, H=3)
+    idx, cnt = idx.to(DEV), cnt.to(DEV)
+    order = sa.sparse_attn_schedule(cnt, N, idx.shape[-1], block=block)
+    o1, l1 = sa.sparse_attn_fwd(q, k, v, idx, cnt, block=block, order=order)
+    o0, l0 = sa.sparse_attn_fwd(q, k, v, idx, cnt, block=block)
+    torch.cuda.synchronize()
+    assert torch.equal(o1.view(torch.int16), o0.view(torch.int16))
+    assert torch.equal(l1.view(torch.int32), l0.view(torch.int32))

@@ -10,8 +10,7 @@ import torch
 import oracle as O
 import paper_2609_23153_amd as sa
 import workloads as W
-from gpu_helpers import check_out, oracle_attend, say, widen
-from oracle.schedule import launch_order
+from gpu_helpers import check_launch_order, check_out, oracle_attend, say, widen
 
 pytestmark = pytest.mark.gpu
 
@@ -121,11 +120,14 @@ def test_fwd_on_head_lists():
                                          f"fwd lists b={block}")
         order = sa.sparse_attn_schedule(cnt, N, idx.shape[-1], block=block)
         torch.cuda.synchronize()
-        ref = launch_order(cnt.cpu().numpy(), idx.shape[-1], N, block)
-        assert np.array_equal(order.cpu().numpy(), ref)
+        check_launch_order(order.cpu().numpy(), cnt.cpu().numpy(), idx.shape[-1], N, block,
+                           f"head lists b={block}")
         o, lse = sa.sparse_attn_fwd(q.to(DEV), k.to(DEV), v.to(DEV), idx, cnt, block=block,
                                     order=order)
+        o0, l0 = sa.sparse_attn_fwd(q.to(DEV), k.to(DEV), v.to(DEV), idx, cnt, block=block)
         torch.cuda.synchronize()
+        # the launch order changes nothing in the results
+        assert torch.equal(o.view(torch.int16), o0.view(torch.int16)) and torch.equal(lse, l0)
         idx_c, cnt_c = idx.cpu().numpy(), cnt.cpu().numpy()
         for h in range(wl.heads):
             ro, rl = oracle_attend(q[0, h], k[0, h], v[0, h], idx_c[0, h], cnt_c[0, h], block, TAU)

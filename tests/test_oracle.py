@@ -380,22 +380,15 @@ def test_widen_bf16_matches_library():
                                   x.to(torch.float64).numpy())
 
 
-def test_launch_order_definition_small_cases():
-    from oracle.schedule import launch_order
-    # uniform lists and fewer tiles than one XCD group: identity order
-    cnt = np.full((1, 2, 10), 3)
-    assert launch_order(cnt, 3, 640, 64).tolist() == list(range(20))
-    # ragged: costlier tiles first, raster order within a class
-    cnt = np.array([[[1, 4, 0, 2]]])
-    # classes: cost 1 -> 1, 4 -> 3, 0 -> 0, 2 -> 2
-    assert launch_order(cnt, 9, 256, 64).tolist() == [1, 3, 0, 2]
-    # block 128: one list per two 64-row tiles, cost doubled; cnt clamped to kmax
-    cnt = np.array([[[5, 1]]])
-    assert launch_order(cnt, 2, 256, 128).tolist() == [0, 1, 2, 3]
-    # XCD interleave over one full group of 8 x 256 uniform tiles: slot s
-    # goes to XCD s % 8, which walks its own run of 256 consecutive tiles
-    cnt = np.full((1, 1, 2048), 1)
-    o = launch_order(cnt, 1, 2048 * 64, 64)
-    assert sorted(o.tolist()) == list(range(2048))
-    assert o[:9].tolist() == [0, 256, 512, 768, 1024, 1280, 1536, 1792, 1]
-    assert o[8 * 255 + 7] == 7 * 256 + 255
+def test_selection_margin_hand_cases():
+    """The diagnostic relative gap between the k-th and (k+1)-th largest
+    score of each row, worked by hand: row [3, 1, 2, 0.5] at k = 2 has gap
+    2 - 1 over 2 = 0.5; row [5, 4.5, 4, 0] has 0.5 / 4.5; the minimum is
+    the second.  Exact ties give 0, negative scores divide by |s_k|, and
+    keeping every block leaves no gap (inf)."""
+    s = np.array([[3.0, 1.0, 2.0, 0.5], [5.0, 4.5, 4.0, 0.0]])
+    assert O.selection_margin(s, 2) == pytest.approx(0.5 / 4.5, rel=1e-15)
+    assert O.selection_margin(s, 1) == pytest.approx(0.1, rel=1e-15)     # (5 - 4.5) / 5
+    assert O.selection_margin(np.array([[2.0, 1.0, 2.0]]), 1) == 0.0
+    assert O.selection_margin(np.array([[-1.0, -3.0, -2.0]]), 1) == 1.0
+    assert O.selection_margin(s, 4) == float("inf")
