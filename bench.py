@@ -68,8 +68,17 @@ def parse_args():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="wan14b_720p")
     ap.add_argument("--cpu-baseline", choices=["on", "off"], default="on")
-    ap.add_argument("--cpu-heads", type=int, default=2,
-                    help="heads of the workload the oracle runs for the CPU baseline")
+    ap.add_argument("--cpu-heads", type=int, default=16,
+                    help="heads of the workload the oracle runs for the CPU baseline (spread "
+                         "evenly over the layer; the time is scaled to all heads)")
+    ap.add_argument("--wan13b", choices=["on", "off"], default="on",
+                    help="also time select + schedule + fwd on the Wan2.1-1.3B 480P layer")
+    ap.add_argument("--normal", choices=["on", "off"], default="on",
+                    help="also time select + schedule + fwd at the 14B-720P shape on i.i.d. "
+                         "normal inputs (lists without locality)")
+    ap.add_argument("--cold", choices=["on", "off"], default="on",
+                    help="also time every call with the caches flushed before it (a 512 MB "
+                         "scratch overwrite)")
     ap.add_argument("--fp8", choices=["on", "off"], default="on",
                     help="also time the fp8 path on the outlier workload of the same shape")
     ap.add_argument("--comp", choices=["on", "off"], default="on",
@@ -84,7 +93,7 @@ def parse_args():
     ap.add_argument("--bwd", choices=["on", "off"], default="on",
                     help="also time the backward of the sparse branch (dQ, dK, dV) on the "
                          "bf16 layer's inputs, output and LSE with a synthetic upstream dO")
-    ap.add_argument("--sweep", choices=["on", "off"], default="off",
+    ap.add_argument("--sweep", choices=["on", "off"], default="on",
                     help="also time select + schedule + fwd over the sparsity sweep (blocks 64 "
                          "and 128 x keep 3/10/25/100%%) on the locality inputs at the 14B-720P "
                          "shape")
@@ -116,6 +125,67 @@ def blas_threads():
     except Exception:
         pass
     return len(os.sched_getaffinity(0))
+
+
+def log(msg):
+    """Progress line on stderr (stdout carries only the JSON line)."""
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def cpu_model():
+    """Model name of the host CPU (from /proc/cpuinfo)."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+SCRATCH_BYTES = 512 << 20
+
+
+class CacheFlush:
+    """Overwrites a 512 MB device buffer: more than the MI355X's 256 MB
+    Infinity Cache plus its 8 x 4 MB of L2, so the call after it starts with
+    cold caches (inputs resident in HBM only)."""
+
+    def __init__(self, dev):
+        self.buf = torch.empty(SCRATCH_BYTES // 4, dtype=torch.int32, device=dev)
+        self.n = 0
+
+    def __call__(self):
+        self.n += 1
+        self.buf.fill_(self.n)
+
+
+def time_calls(phases, steps, warmup, flush=None):
+    """Per-phase HIP-event times (ms) of `steps` repetitions of the phases
+    [(name, fn), ...], after `warmup` untimed repetitions, all on the current
+    stream (the stream the library launches on).  Warm: the phases run back
+    to back.  Cold (flush given): the cache flush runs before every timed
+    phase, outside its events.  Returns {name: [ms, ...]}."""
+    for _ in range(warmup):
+        for _, fn in phases:
+            fn()
+    torch.cuda.synchronize()
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in phases] for _ in range(steps)]
+    for s_ in range(steps):
+        for (_, fn), (e0, e1) in zip(phases, ev[s_]):
+            if flush is not None:
+                flush()
+            e0.record()
+            fn()
+            e1.record()
+    torch.cuda.synchronize()
+    return {name: [ev[s_][i][0].elapsed_time(ev[s_][i][1]) for s_ in range(steps)]
+            for i, (name, _) in enumerate(phases)}
+
+
+def med(x):
+    return round(float(np.median(x)), 4)
 
 
 def bench_comp(args, sa, W, dev, wl, q, k, v, o_s, sparse_ms):
@@ -275,6 +345,55 @@ def bench_bwd(args, sa, dev, wl, q, k, v, o, lse, idx, cnt):
                      "frac": round(tf / PEAK_BF16_TFLOPS, 4), "traffic": None,
                      "flops_per_launch": alg,
                      "note": "algorithmic flops: 2.5x the forward's over the selected blocks"},
+    }
+
+
+def bench_path(args, sa, W, dev, name):
+    """select + schedule + fwd (bf16, row top-k) on another workload: ms per
+    call (warm median, and cold with the caches flushed before each call) and
+    the forward's roofline over the selected blocks."""
+    wl = W.WORKLOADS[name]
+    B, H, N, d, block = wl.batch, wl.heads, wl.seqlen, wl.head_dim, wl.block
+    nb = -(-N // block)
+    kk = sa.sparse_attn_keep_count(wl.keep_bp, nb)
+    q, k, v = (t.to(dev) for t in W.make_inputs(wl))
+    idx = torch.empty(B, H, nb, kk, dtype=torch.int32, device=dev)
+    cnt = torch.empty(B, H, nb, dtype=torch.int32, device=dev)
+    o = torch.empty_like(q)
+    lse = torch.empty(B, H, N, dtype=torch.float32, device=dev)
+    desc = sa.make_desc(q, k, v, o, block=block)
+    ws_sel = torch.empty(sa.sparse_attn_workspace_size(desc, sa.SA_OP_SELECT, kk),
+                         dtype=torch.uint8, device=dev)
+    ws_sch = torch.empty(sa.sparse_attn_workspace_size(desc, sa.SA_OP_SCHEDULE, kk),
+                         dtype=torch.uint8, device=dev)
+    order = torch.empty(sa.sparse_attn_num_tiles(desc), dtype=torch.int32, device=dev)
+    phases = [
+        ("select", lambda: sa.sparse_attn_select(q, k, kk, block=block, idx=idx, cnt=cnt,
+                                                 ws=ws_sel)),
+        ("schedule", lambda: sa.sparse_attn_schedule(cnt, N, kk, block=block, order=order,
+                                                     ws=ws_sch)),
+        ("fwd", lambda: sa.sparse_attn_fwd(q, k, v, idx, cnt, block=block, order=order, o=o,
+                                           lse=lse)),
+    ]
+    warm = time_calls(phases, args.steps, args.warmup)
+    cold = time_calls(phases, max(3, args.steps // 2), 1, flush=args.flusher)
+    flops = selected_flops(cnt.cpu().numpy(), idx.cpu().numpy(), N, block, d)
+    dense = 4 * B * H * N * N * d
+    fwd_ms = med(warm["fwd"])
+    tf = flops / (fwd_ms * 1e-3) / 1e12
+    step_ms = sum(med(warm[n]) for n, _ in phases)
+    return {
+        "workload": name, "generator": wl.gen,
+        "shape": {"batch": B, "heads": H, "seqlen": N, "grid": list(wl.grid), "block": block,
+                  "keep_blocks": kk, "key_blocks": nb},
+        "ms_per_call": {n: med(warm[n]) for n, _ in phases},
+        "ms_per_call_cold": {n: med(cold[n]) for n, _ in phases},
+        "ms_per_step": round(step_ms, 4),
+        "dense_equiv_tflops_step": round(dense / (step_ms * 1e-3) / 1e12, 2),
+        "roofline": {"kernel": "fwd_bf16_kernel", "bound": "mfma", "achieved": round(tf, 2),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tf / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "flops_per_launch": flops},
     }
 
 
@@ -500,6 +619,7 @@ def main():
     nb = -(-N // block)
     k = sa.sparse_attn_keep_count(wl.keep_bp, nb)
 
+    log(f"generating {wl.name}")
     q, kk, v = (t.to(dev) for t in W.make_inputs(wl))
     idx = torch.empty(B, H, nb, k, dtype=torch.int32, device=dev)
     cnt = torch.empty(B, H, nb, dtype=torch.int32, device=dev)
@@ -542,6 +662,26 @@ def main():
     sch_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
     fwd_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in ev]))
 
+    args.flusher = CacheFlush(dev) if args.cold == "on" else None
+    phases = [
+        ("select", lambda: sa.sparse_attn_select(q, kk, k, block=block, idx=idx, cnt=cnt,
+                                                 ws=ws_sel)),
+        ("schedule", lambda: sa.sparse_attn_schedule(cnt, N, k, block=block, order=order,
+                                                     ws=ws_sch)),
+        ("fwd", lambda: sa.sparse_attn_fwd(q, kk, v, idx, cnt, block=block, order=order, o=o,
+                                           lse=lse)),
+    ]
+    timing = {"warm_median_ms": {n: med([e[i].elapsed_time(e[i + 1]) for e in ev])
+                                 for i, (n, _) in enumerate(phases)}}
+    if args.flusher is not None:
+        cold = time_calls(phases, args.steps, 1, flush=args.flusher)
+        cold_step = time_calls([("step", step)], args.steps, 0, flush=args.flusher)["step"]
+        timing["cold_median_ms"] = {n: med(cold[n]) for n, _ in phases}
+        timing["cold_step_median_ms"] = med(cold_step)
+        timing["cold_note"] = ("a 512 MB device buffer is overwritten before every timed call "
+                               "(and before every timed step), so L2 and the Infinity Cache "
+                               "hold none of its inputs; medians of HIP-event times")
+
     flops = selected_flops(cnt.cpu().numpy(), idx.cpu().numpy(), N, block, d)
     dense = 4 * B * H * N * N * d
     fwd_tflops = flops / (fwd_ms * 1e-3) / 1e12
@@ -570,6 +710,13 @@ def main():
         "fwd_dense_equiv_tflops": round(dense / (fwd_ms * 1e-3) / 1e12, 2),
         "fwd_mfma_frac": round(fwd_tflops / PEAK_BF16_TFLOPS, 4),
         "select_gbs": round(sel_bytes / (sel_ms * 1e-3) / 1e9, 1),
+        "select_roofline": {
+            "kernels": ["pool_kernel", "score_kernel", "topk_row_kernel"], "bound": "hbm",
+            "achieved": round(sel_bytes / (sel_ms * 1e-3) / 1e9, 1), "peak": PEAK_HBM_GBS,
+            "unit": "GB/s", "frac": round(sel_bytes / (sel_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+            "traffic": None, "algorithmic_bytes_per_call": sel_bytes,
+            "note": "Q and K read once, lists written; the whole selection call"},
+        "timing": timing,
         "roofline": {
             "kernel": "fwd_bf16_kernel", "bound": "mfma",
             "achieved": round(fwd_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
@@ -581,17 +728,30 @@ def main():
         },
     }
 
+    log(f"headline step {ms_step:.3f} ms (fwd {fwd_ms:.3f} ms)")
     if args.comp == "on":
+        log("compensation")
         out["compensation"] = bench_comp(args, sa, W, dev, wl, q, kk, v, o, ms_step)
     if args.fp8 == "on":
+        log("fp8")
         out["fp8"] = bench_fp8(args, sa, W, dev)
     if args.causal == "on":
+        log("causal")
         out["causal"] = bench_causal(args, sa, W, dev, wl, q, kk, v)
     if args.bwd == "on":
+        log("backward")
         out["backward"] = bench_bwd(args, sa, dev, wl, q, kk, v, o, lse, idx, cnt)
     if args.linear == "on":
+        log("linear")
         out["linear_w8a8"] = bench_linear(args, sa, W, dev)
+    if args.wan13b == "on":
+        log("wan13b_480p")
+        out["wan13b_480p"] = bench_path(args, sa, W, dev, "wan13b_480p")
+    if args.normal == "on":
+        log("wan14b_720p_normal")
+        out["wan14b_720p_normal"] = bench_path(args, sa, W, dev, "wan14b_720p_normal")
     if args.sweep == "on":
+        log("sweep")
         out["sweep"] = bench_sweep(args, sa, W, dev)
 
     if args.copy_calib:
@@ -609,25 +769,36 @@ def main():
         out["copy_calib"] = {"bytes_each_way": 1 << 30, "ms": e0.elapsed_time(e1) / 5}
 
     if args.cpu_baseline == "on":
+        log("cpu baseline")
         import oracle as O
         tau = W.softmax_scale(d)
-        sample = sorted({0, H - 1})[:max(1, args.cpu_heads)]
-        heads_data = [[t.to(torch.float64).numpy() for t in W.make_head(wl, 0, h)]
-                      for h in sample]
-        t0 = time.perf_counter()
-        for qf, kf, vf in heads_data:
+        nh = max(1, min(args.cpu_heads, H))
+        sample = sorted({int(round(i * (H - 1) / max(1, nh - 1))) for i in range(nh)})
+        t_sel = t_fwd = 0.0
+        for h in sample:
+            log(f"  oracle head {h}")
+            qf, kf, vf = (t.to(torch.float64).numpy() for t in W.make_head(wl, 0, h))
+            t0 = time.perf_counter()
             ri, rc = O.select_head(qf, kf, block, wl.keep_bp)
+            t1 = time.perf_counter()
             O.sparse_attention(qf, kf, vf, ri, rc, block, tau)
-        secs = time.perf_counter() - t0
-        per_call = secs * (B * H) / len(sample)
+            t2 = time.perf_counter()
+            t_sel += t1 - t0
+            t_fwd += t2 - t1
+        scale_h = (B * H) / len(sample)
+        per_call = (t_sel + t_fwd) * scale_h
         out["cpu_baseline"] = {
             "value": round(dense / per_call / 1e12, 6),
             "unit": "dense-equiv TFLOP/s",
             "ms_per_call": round(per_call * 1e3, 1),
+            "ms_per_call_select": round(t_sel * scale_h * 1e3, 1),
+            "ms_per_call_fwd": round(t_fwd * scale_h * 1e3, 1),
             "cores": blas_threads(),
+            "cpu_model": cpu_model(),
             "kind": "oracle",
-            "sample": f"fp64 NumPy oracle, select + attention of heads {sample} of {H} "
-                      f"({secs:.1f} s), scaled x{B * H / len(sample):g} to the full layer",
+            "sample": f"fp64 NumPy oracle, select + attention of {len(sample)} of {H} heads "
+                      f"{sample} ({t_sel + t_fwd:.1f} s: select {t_sel:.1f} s, attention "
+                      f"{t_fwd:.1f} s), scaled x{scale_h:g} to the full layer",
         }
     print(json.dumps(out), flush=True)
 

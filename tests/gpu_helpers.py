@@ -13,6 +13,11 @@ BF16_REL_L2 = 1e-2
 BF16_MAX_ABS = 2e-2
 FP8_REL_L2 = 5e-2
 LSE_ABS = 2e-3
+# fp8 path: the row sum is taken over the probabilities rounded to e4m3
+# (nearest even, 3 mantissa bits), each within a relative 2^-4 of its exact
+# value, so the sum (and exp(LSE)) is within a relative 2^-4 as well and LSE
+# within log(1 + 2^-4); 2e-3 more covers the fp32 arithmetic.
+FP8_LSE_ABS = float(np.log1p(2.0 ** -4)) + 2e-3
 
 
 def say(*a):

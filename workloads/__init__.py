@@ -81,6 +81,10 @@ WORKLOADS = {
     # same shape, fp8 operands, with channel outliers in Q and K
     "wan14b_720p_fp8": Workload("wan14b_720p_fp8", 1, 40, (21, 45, 80), 128, 64, 300,
                                 "outliers", 3),
+    # same shape with i.i.d. normal Q, K, V: selection without locality, so
+    # neighbouring query blocks share few key blocks (a low-reuse bound)
+    "wan14b_720p_normal": Workload("wan14b_720p_normal", 1, 40, (21, 45, 80), 128, 64, 300,
+                                   "normal", 5),
     # sparsity sweep at the 14B 720P shape with locality + long-range hot blocks
     "sweep": Workload("sweep", 1, 40, (21, 45, 80), 128, 64, 300, "locality", 4,
                       sweep=tuple((b, k) for b in (64, 128)
