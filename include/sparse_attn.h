@@ -161,6 +161,24 @@ int sparse_attn_schedule(const sparse_attn_desc* desc, const int32_t* cnt, int32
                          int32_t* order, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * sparse_attn_schedule without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops that forbid
+ * allocation): the same launch order as sparse_attn_schedule, bit for bit,
+ * with its class counters in a 64 KiB device array inside the library, one
+ * per GPU, held until the process ends.  The array of the current device is
+ * used (the stream must belong to it); its address is looked up on the first
+ * call on each device.  Every call on one GPU shares that array, so calls
+ * that overlap on one GPU (other streams, other threads) race; calls
+ * ordered on one stream do not.  No memory is allocated.
+ *  cnt, kmax, order  as for sparse_attn_schedule
+ * Errors: as sparse_attn_schedule, with SA_ERR_UNSUPPORTED when the problem
+ * needs more than the array holds (more than 1,047,552 query tiles,
+ * B * H * ceil(L / 64)), and SA_ERR_DEVICE when the array's device address
+ * cannot be obtained. */
+int sparse_attn_schedule_static(const sparse_attn_desc* desc, const int32_t* cnt, int32_t kmax,
+                                int32_t* order, void* stream);
+
+/*
  * Sparse branch O_s = A_M(Q, K, V) (paper §2 Eq. comp-sparse, §4.1), bf16.
  * For query block i with key-block list S_i = idx[b][h][i][0 .. cnt-1] and
  * U_i the tokens of those blocks, every query t of block i gets

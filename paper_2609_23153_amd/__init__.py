@@ -18,7 +18,7 @@ __all__ = [
     "SA_OP_SELECT", "SA_OP_SCHEDULE", "library", "sparse_attn_version",
     "sparse_attn_status_str", "sparse_attn_keep_count", "sparse_attn_workspace_size",
     "sparse_attn_num_tiles", "sparse_attn_select", "sparse_attn_schedule", "sparse_attn_fwd",
-    "sparse_attn_quant_fp8", "sparse_attn_fwd_fp8", "sparse_attn_comp_state",
+    "sparse_attn_schedule_static", "sparse_attn_quant_fp8", "sparse_attn_fwd_fp8", "sparse_attn_comp_state",
     "sparse_attn_comp_out", "SA_OP_COMP_STATE", "COMP_RANK", "make_desc", "EXPORTED_SYMBOLS",
     "sparse_attn_quant_rows_fp8", "sparse_attn_linear_w8a8", "sparse_attn_bwd", "SA_OP_BWD",
 ]
@@ -39,7 +39,7 @@ EXPORTED_SYMBOLS = (
     "sparse_attn_workspace_size", "sparse_attn_num_tiles", "sparse_attn_select",
     "sparse_attn_schedule", "sparse_attn_fwd", "sparse_attn_quant_fp8", "sparse_attn_fwd_fp8",
     "sparse_attn_comp_state", "sparse_attn_comp_out", "sparse_attn_quant_rows_fp8",
-    "sparse_attn_linear_w8a8", "sparse_attn_bwd",
+    "sparse_attn_linear_w8a8", "sparse_attn_bwd", "sparse_attn_schedule_static",
 )
 
 
@@ -85,6 +85,7 @@ def library() -> ctypes.CDLL:
                                                   _P, _P, ctypes.c_int32, _P, ctypes.c_size_t, _P]),
             "sparse_attn_schedule": (ctypes.c_int, [D, _P, ctypes.c_int32, _P, _P,
                                                     ctypes.c_size_t, _P]),
+            "sparse_attn_schedule_static": (ctypes.c_int, [D, _P, ctypes.c_int32, _P, _P]),
             "sparse_attn_fwd": (ctypes.c_int, [D, _P, _P, _P, _P, _P, ctypes.c_int32, _P, _P, _P,
                                                _P]),
             "sparse_attn_quant_fp8": (ctypes.c_int, [D, _P, ctypes.POINTER(ctypes.c_int64),
@@ -230,6 +231,23 @@ def sparse_attn_schedule(cnt, seqlen: int, kmax: int, block: int = 64, order=Non
     st = library().sparse_attn_schedule(ctypes.byref(desc), _ptr(cnt), kmax, _ptr(order),
                                         _ptr(ws), ws.numel(), _stream(cnt))
     _check(st, "sparse_attn_schedule")
+    return order
+
+
+def sparse_attn_schedule_static(cnt, seqlen: int, kmax: int, order, block: int = 64):
+    """sparse_attn_schedule without a workspace (the library's per-GPU device
+    array holds the counters): writes the launch order into the caller's
+    ``order`` (int32 [B * H * ceil(seqlen / 64)]) and allocates nothing."""
+    B, H, _ = cnt.shape
+    _dense(cnt, "cnt")
+    _dense(order, "order")
+    desc = SparseAttnDesc()
+    desc.batch, desc.heads, desc.seqlen, desc.head_dim, desc.block = B, H, seqlen, 128, block
+    if order.numel() != sparse_attn_num_tiles(desc):
+        raise ValueError("order must hold one int32 per query tile")
+    st = library().sparse_attn_schedule_static(ctypes.byref(desc), _ptr(cnt), kmax, _ptr(order),
+                                               _stream(cnt))
+    _check(st, "sparse_attn_schedule_static")
     return order
 
 

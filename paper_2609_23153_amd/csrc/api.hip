@@ -121,6 +121,20 @@ int sparse_attn_schedule(const sparse_attn_desc* desc, const int32_t* cnt, int32
       sa::launch_schedule(s, cnt, kmax, order, ws, static_cast<hipStream_t>(stream)));
 }
 
+int sparse_attn_schedule_static(const sparse_attn_desc* desc, const int32_t* cnt, int32_t kmax,
+                                int32_t* order, void* stream) {
+  Shape s;
+  int st = check_desc(desc, &s);
+  if (st != SA_OK) return st;
+  if (!order) return SA_ERR_INVALID_ARG;
+  if ((st = check_lists(s, cnt, cnt, kmax)) != SA_OK) return st;
+  if (sa::schedule_workspace_bytes(s) > sa::kStaticScheduleScratchBytes) return SA_ERR_UNSUPPORTED;
+  int32_t* scratch = nullptr;
+  if (sa::static_schedule_scratch(&scratch) != hipSuccess) return SA_ERR_DEVICE;
+  return launch_status(
+      sa::launch_schedule(s, cnt, kmax, order, scratch, static_cast<hipStream_t>(stream)));
+}
+
 int sparse_attn_select(const sparse_attn_desc* desc, const void* q, const void* k, int32_t mode,
                        int64_t budget, int32_t* idx, int32_t* cnt, int32_t kmax, void* ws,
                        size_t ws_bytes, void* stream) {

@@ -49,6 +49,12 @@ int64_t num_query_tiles(const Shape& s);
 // Writes the launch order of the 64-row query tiles (int32 [B*H*ceil(N/64)]).
 hipError_t launch_schedule(const Shape& s, const int32_t* cnt, int kmax, int32_t* order,
                            void* ws, hipStream_t stream);
+// Size of the file-scope device array that replaces the schedule workspace in
+// the allocation-free entry point (one per GPU, held until the process ends).
+constexpr size_t kStaticScheduleScratchBytes = 64 * 1024;
+// Device address of the current GPU's copy of that array (looked up once per
+// device); hipSuccess or the HIP error of the lookup.
+hipError_t static_schedule_scratch(int32_t** out);
 
 // ---- forward -------------------------------------------------------------
 struct FwdArgs {

@@ -14,6 +14,8 @@
 // chunks of 1024 tiles: class counts per chunk, one exclusive scan of the
 // counts (classes descending, chunks ascending), and a scatter that writes
 // every tile straight into its launch slot.
+#include <mutex>
+
 #include "common.h"
 #include "launch.h"
 
@@ -185,6 +187,38 @@ int64_t num_query_tiles(const Shape& s) {
 size_t schedule_workspace_bytes(const Shape& s) {
   const int64_t chunks = (num_query_tiles(s) + kChunk - 1) / kChunk;
   return (size_t)(chunks + 1) * kClasses * sizeof(int32_t);
+}
+
+// ---- allocation-free variant ----------------------------------------------
+// The class counters live in one file-scope device array per GPU instead of a
+// caller workspace.  In host code `scratch` names a host-side stand-in, not
+// device memory: the device address of each GPU's copy is looked up once per
+// device (hipGetSymbolAddress with that device current) and only that address
+// is handed to the kernels.
+namespace {
+constexpr int kScratchInts = kStaticScheduleScratchBytes / (int)sizeof(int32_t);
+static __device__ __align__(256) int32_t scratch[kScratchInts];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+int32_t* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t static_schedule_scratch(int32_t** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = static_cast<int32_t*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_schedule(const Shape& s, const int32_t* cnt, int kmax, int32_t* order,

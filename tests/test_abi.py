@@ -292,3 +292,22 @@ def test_bwd_rejects_bad_arguments():
     big = desc(N=75600)
     big.k_stride[2] = 28416
     assert lib.sparse_attn_fwd(ctypes.byref(big), P, P, P, P, P, 7, None, P, None, None) == -2
+
+
+def test_schedule_static_rejects_bad_arguments():
+    """The allocation-free schedule checks its arguments like
+    sparse_attn_schedule and rejects problems whose counters exceed its 64 KiB
+    device array ((chunks of 1024 tiles + 1) x 16 int32) before any HIP call."""
+    lib = sa.library()
+    ds = desc(B=2, H=3, N=1000)
+    call = lambda d, *a: lib.sparse_attn_schedule_static(ctypes.byref(d), *a)
+    assert call(ds, None, 7, P, None) == -1                          # null cnt
+    assert call(ds, P, 7, None, None) == -1                          # null order
+    assert call(ds, P, 0, P, None) == -1                             # kmax 0
+    assert call(desc(block=96), P, 7, P, None) == -2                 # bad descriptor
+    # 1023 chunks of 1024 tiles fit (1024 x 16 x 4 B = 64 KiB), 1024 do not
+    fits = desc(B=1, H=1023, N=1024 * 64)
+    assert lib.sparse_attn_workspace_size(ctypes.byref(fits), sa.SA_OP_SCHEDULE, 7) == 65536
+    over = desc(B=1, H=1023, N=1024 * 64 + 64)
+    assert lib.sparse_attn_workspace_size(ctypes.byref(over), sa.SA_OP_SCHEDULE, 7) > 65536
+    assert call(over, P, 7, P, None) == -2
