@@ -12,7 +12,9 @@
 // 64-key tile: waves 0/1 own query rows 0-31 / 32-63 of the first tile of
 // each pair of tiles in the list, waves 2/3 of the second.  Per wave and tile:
 //   S^T (64 keys x 32 queries) = K . Q^T       4 x v_mfma_scale_..._32x32x64 (scales sk, sq)
-//   P = 2^(x - m) * 2^(8 - kLazy) rounded to e4m3 with v_cvt_pk_fp8_f32
+//   P = 2^(x - m) * 2^(8 - kLazy) rounded to e4m3 with v_cvt_pk_fp8_f32, the
+//       power of two built in integer arithmetic (one FMA and one conversion
+//       per score: exact at integer exponents, linear in between)
 //   O^T (128 x 32)        += V^T . P^T        4 x v_mfma_scale_..._32x32x64 (scales sv, 2^(kLazy-8))
 //   row sums of P          += 1^T . P^T        1 more MFMA against an all-ones channel
 // so the normaliser is the sum of exactly the rounded probabilities the PV
@@ -101,6 +103,15 @@ __device__ __forceinline__ int next_tile(list_ptr list, int n, int total, int sp
   return total;
 }
 
+// v_cvt_u32_f32: truncation to an unsigned integer with the hardware's
+// saturation (negative values and NaN give 0, values >= 2^32 give
+// 0xffffffff), written as asm because C++ leaves negative inputs undefined.
+__device__ __forceinline__ uint32_t cvt_u32_sat(float x) {
+  uint32_t u;
+  asm("v_cvt_u32_f32 %0, %1" : "=v"(u) : "v"(x));
+  return u;
+}
+
 // E8M0 code of a power-of-two fp32 scale (its biased exponent).
 __device__ __forceinline__ int e8m0(float s) { return (int)((__float_as_uint(s) >> 23) & 0xffu); }
 
@@ -139,7 +150,10 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
   const int c = min(max(p.cnt[(int64_t)bh * p.nb + iblk], 0), p.kmax);
   const int total = c * spb;
 
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  // the wave index is uniform across a wave: read it into a scalar register
+  // so that everything derived from it (the tile a wave computes, its
+  // scales, the mask test) stays scalar
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int rh = wave & 1, par = wave >> 1;  // row half, tile parity
   const int g = lane >> 5, l32 = lane & 31;
 
@@ -348,12 +362,16 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
     }
     // lane holds keys 32*rt + 8*(r>>2) + 4*g + (r&3) of query l32
     if (start + kTile > tile_hi || start < tile_lo) {
+      // (the opaque move keeps the per-key arithmetic inside the branch)
+      int st = __builtin_amdgcn_readfirstlane(start);
+      asm volatile("" : "+s"(st));
+      const int hi = key_hi - st - 4 * g, lo = key_lo - st - 4 * g;
 #pragma unroll
       for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int key = start + 32 * rt + 8 * (r >> 2) + 4 * g + (r & 3);
-          if (key >= key_hi || key < key_lo) s[rt][r] = -INFINITY;
+          const int off = 32 * rt + 8 * (r >> 2) + (r & 3);  // key - start - 4g
+          if (off >= hi || off < lo) s[rt][r] = -INFINITY;
         }
     }
 
@@ -378,7 +396,15 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
     // P^T as B operand: slot 16*rt + r <- s[rt][r]; values 2^(x - m) * 2^(8 - kLazy)
     // rounded to e4m3
     i32x8 pk;
-    const float mofs = kLog2PScale - msafe;  // the factor kPScale folded into the exponent
+    // P * 2^6 = 2^y with y = tau*log2(e)*s - m + 6, as the fp32 whose bit
+    // pattern is (y + 127) * 2^23 truncated to an integer: exact at integer
+    // y and linear in the mantissa between them (at most 6.2% above 2^y, the
+    // same relative excess for a given fractional part of y).  One FMA and
+    // one conversion per score instead of an FMA and a transcendental; the
+    // e4m3 rounding that follows keeps 3 mantissa bits anyway.  Negative
+    // patterns (y < -127, and masked scores) convert to 0, i.e. P = 0.
+    const float cexp = p.scale_log2 * 8388608.f;                    // tau log2(e) 2^23
+    const float kexp = (kLog2PScale + 127.f - msafe) * 8388608.f;  // (6 + 127 - m) 2^23
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
 #pragma unroll
@@ -386,7 +412,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
         float x[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u)
-          x[u] = __builtin_amdgcn_exp2f(fmaf(s[rt][r + u], p.scale_log2, mofs));
+          x[u] = __uint_as_float(cvt_u32_sat(fmaf(s[rt][r + u], cexp, kexp)));
         int w = __builtin_amdgcn_cvt_pk_fp8_f32(x[0], x[1], 0, false);
         w = __builtin_amdgcn_cvt_pk_fp8_f32(x[2], x[3], w, true);
         pk[4 * rt + r / 4] = w;
