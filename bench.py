@@ -711,7 +711,7 @@ def main():
         "fwd_mfma_frac": round(fwd_tflops / PEAK_BF16_TFLOPS, 4),
         "select_gbs": round(sel_bytes / (sel_ms * 1e-3) / 1e9, 1),
         "select_roofline": {
-            "kernels": ["pool_kernel", "score_kernel", "topk_row_kernel"], "bound": "hbm",
+            "kernels": ["pool_kernel", "score_topk_kernel"], "bound": "hbm",
             "achieved": round(sel_bytes / (sel_ms * 1e-3) / 1e9, 1), "peak": PEAK_HBM_GBS,
             "unit": "GB/s", "frac": round(sel_bytes / (sel_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
             "traffic": None, "algorithmic_bytes_per_call": sel_bytes,

@@ -53,8 +53,16 @@ enum {
   SA_SELECT_HEAD_TOPK = 1 /* ragged: `budget` (query, key) block pairs per head */
 };
 
-/* Workspace consumers (second argument of sparse_attn_workspace_size). */
-enum { SA_OP_SELECT = 0, SA_OP_SCHEDULE = 1, SA_OP_COMP_STATE = 2, SA_OP_BWD = 3 };
+/* Workspace consumers (second argument of sparse_attn_workspace_size):
+ * SA_OP_SELECT is the row mode of sparse_attn_select, SA_OP_SELECT_HEAD its
+ * whole-head mode. */
+enum {
+  SA_OP_SELECT = 0,
+  SA_OP_SCHEDULE = 1,
+  SA_OP_COMP_STATE = 2,
+  SA_OP_BWD = 3,
+  SA_OP_SELECT_HEAD = 4
+};
 
 /*
  * Problem descriptor (host struct).
@@ -106,15 +114,22 @@ const char* sparse_attn_status_str(int status);
 int32_t sparse_attn_keep_count(int32_t keep_bp, int32_t nkb);
 
 /* Bytes of device workspace that `op` needs for this problem; `kmax` is the
- * row stride of the index list (ignored for SA_OP_SELECT).  Returns 0 for an
- * invalid descriptor or op. */
+ * row stride of the index list (ignored for SA_OP_SELECT and
+ * SA_OP_SELECT_HEAD).  Returns 0 for an invalid descriptor or op.
+ * Row-mode selection with nkb <= 1192 keeps the block scores on chip and
+ * needs B*H*(2048*nkb + 32768*ceil(nkb/32) + 8*nkb) bytes; above that, and
+ * in the whole-head mode, the fp64 score matrix (8*nkb^2 bytes per head) is
+ * part of it. */
 size_t sparse_attn_workspace_size(const sparse_attn_desc* desc, int32_t op, int32_t kmax);
 
 /*
  * Block selection M_phi (paper §2 Eq. comp-sparse; §4.3 keeps mask
  * selection in BF16, so it reads the bf16 Q and K).
  *   score s_ij = (sum_{t in I_i} q_t) . (sum_{u in J_j} k_u) / (n_i n_j),
- * the mean unscaled logit of block (i, j), pooled and dotted in fp64.
+ * the mean unscaled logit of block (i, j), pooled and dotted in fp64.  The
+ * row mode with nkb <= 1192 ranks bf16-matrix-core approximations of the
+ * scores whose error is bounded, and rescores in fp64 the blocks whose bound
+ * reaches across the k-th score, so its lists are those of the fp64 scores.
  *  q, k    bf16 [B][H][L][d] via desc strides (o_stride and v_stride unused)
  *  mode    SA_SELECT_ROW_TOPK: each query block keeps the `budget` key blocks
  *          with the largest score under (score desc, block index asc);
@@ -130,6 +145,7 @@ size_t sparse_attn_workspace_size(const sparse_attn_desc* desc, int32_t op, int3
  *          ascending in the first cnt entries, -1 after them
  *  cnt     int32 [B][H][nqb] out: number of kept blocks per query block
  *  ws      device workspace of ws_bytes >= sparse_attn_workspace_size(SA_OP_SELECT)
+ *          for SA_SELECT_ROW_TOPK, (SA_OP_SELECT_HEAD) for SA_SELECT_HEAD_TOPK
  */
 int sparse_attn_select(const sparse_attn_desc* desc, const void* q, const void* k,
                        int32_t mode, int64_t budget, int32_t* idx, int32_t* cnt,

@@ -15,7 +15,7 @@ import torch
 
 __all__ = [
     "LIB_PATH", "SparseAttnError", "SA_SELECT_ROW_TOPK", "SA_SELECT_HEAD_TOPK",
-    "SA_OP_SELECT", "SA_OP_SCHEDULE", "library", "sparse_attn_version",
+    "SA_OP_SELECT", "SA_OP_SCHEDULE", "SA_OP_SELECT_HEAD", "library", "sparse_attn_version",
     "sparse_attn_status_str", "sparse_attn_keep_count", "sparse_attn_workspace_size",
     "sparse_attn_num_tiles", "sparse_attn_select", "sparse_attn_schedule", "sparse_attn_fwd",
     "sparse_attn_schedule_static", "sparse_attn_quant_fp8", "sparse_attn_fwd_fp8", "sparse_attn_comp_state",
@@ -31,7 +31,7 @@ LIB_PATH = os.environ.get("SPARSE_ATTN_LIB") or os.path.join(
 
 SA_SELECT_ROW_TOPK = 0
 SA_SELECT_HEAD_TOPK = 1
-SA_OP_SELECT, SA_OP_SCHEDULE, SA_OP_COMP_STATE, SA_OP_BWD = 0, 1, 2, 3
+SA_OP_SELECT, SA_OP_SCHEDULE, SA_OP_COMP_STATE, SA_OP_BWD, SA_OP_SELECT_HEAD = 0, 1, 2, 3, 4
 COMP_RANK = 64
 
 EXPORTED_SYMBOLS = (
@@ -205,7 +205,8 @@ def sparse_attn_select(q, k, budget: int, block: int = 64, mode: int = SA_SELECT
         cnt = torch.empty(B, H, nb, dtype=torch.int32, device=q.device)
     _dense(idx, "idx"), _dense(cnt, "cnt")
     if ws is None:
-        ws = _workspace(desc, SA_OP_SELECT, kmax, q.device)
+        op = SA_OP_SELECT if mode == SA_SELECT_ROW_TOPK else SA_OP_SELECT_HEAD
+        ws = _workspace(desc, op, kmax, q.device)
     st = library().sparse_attn_select(ctypes.byref(desc), _ptr(q), _ptr(k), mode, budget,
                                       _ptr(idx), _ptr(cnt), kmax, _ptr(ws), ws.numel(),
                                       _stream(q))

@@ -96,6 +96,7 @@ size_t sparse_attn_workspace_size(const sparse_attn_desc* desc, int32_t op, int3
   if (check_desc(desc, &s) != SA_OK) return 0;
   switch (op) {
     case SA_OP_SELECT: return sa::select_workspace_bytes(s);
+    case SA_OP_SELECT_HEAD: return sa::select_head_workspace_bytes(s);
     case SA_OP_SCHEDULE: return kmax >= 1 ? sa::schedule_workspace_bytes(s) : 0;
     case SA_OP_COMP_STATE: return sa::comp_state_workspace_bytes(s);
     case SA_OP_BWD: return sa::bwd_workspace_bytes(s);
@@ -153,7 +154,9 @@ int sparse_attn_select(const sparse_attn_desc* desc, const void* q, const void* 
   } else {
     return SA_ERR_INVALID_ARG;
   }
-  if (ws_bytes < sa::select_workspace_bytes(s)) return SA_ERR_WORKSPACE;
+  if (ws_bytes < (mode == SA_SELECT_ROW_TOPK ? sa::select_workspace_bytes(s)
+                                              : sa::select_head_workspace_bytes(s)))
+    return SA_ERR_WORKSPACE;
   hipStream_t hs = static_cast<hipStream_t>(stream);
   if (mode == SA_SELECT_ROW_TOPK)
     return launch_status(sa::launch_select_row(s, q, to_strides(desc->q_stride), k,

@@ -34,8 +34,11 @@ __host__ __device__ inline int causal_hi(const Shape& s, int t) {
 }
 
 // ---- selection -----------------------------------------------------------
-// Workspace layout: qhat [B*H*nb*128] f64 | khat [same] | scores [B*H*nb*nb] f64
-size_t select_workspace_bytes(const Shape& s);
+// Workspace: qhat [B*H*nb*128] f64 | khat [same] | then, row mode with
+// nb <= 1192, the split operands and norms of the fused kernel, otherwise the
+// scores [B*H*nb*nb] f64 (whole-head mode: and the radix-select state).
+size_t select_workspace_bytes(const Shape& s);       // row mode
+size_t select_head_workspace_bytes(const Shape& s);  // whole-head mode
 hipError_t launch_select_row(const Shape& s, const void* q, Strides qs, const void* k,
                              Strides ks, int topk, int kmax, int32_t* idx, int32_t* cnt,
                              void* ws, hipStream_t stream);

@@ -6,6 +6,15 @@
 //   pool   : Q and K streamed once from HBM; per block, the fp64 sum of the
 //            bf16 token vectors (exact for bf16 inputs whose exponents span
 //            fewer than ~38 binades, so it does not depend on summation order)
+//   row mode, nb <= kFStrideBig (the scores never reach HBM):
+//   score_topk : per 32 query blocks, approximate scores of every key block
+//            on the bf16 matrix cores from a two-term bf16 split of the
+//            pooled sums, kept in LDS; per query block the k-th largest
+//            approximation and a rigorous error bound split the key blocks
+//            into certainly kept, certainly dropped and a band between; only
+//            the band is rescored in fp64 (see the comment above
+//            score_topk_kernel)
+//   otherwise:
 //   score  : per (batch, head) an fp64 GEMM qhat . khat^T scaled by
 //            1 / (n_i n_j)  -> scores in the workspace
 //   topk   : one wavefront per query block; a bitwise search over
@@ -21,53 +30,177 @@
 namespace sa {
 namespace {
 
-constexpr int kPoolThreads = 256;
-constexpr int kMaxBlock = 128;  // largest supported block size
+typedef __attribute__((__vector_size__(4 * sizeof(double)))) double f64x4;
+typedef __attribute__((__vector_size__(2 * sizeof(double)))) double f64x2;
 
-// One workgroup pools one block of Q (blockIdx.z == 0) or K (== 1).
-__global__ __launch_bounds__(kPoolThreads) void pool_kernel(
+// x of the lane N places lower within its row of 16 lanes (cyclically), by
+// DPP: no LDS round trip.  `idle` is returned for a disabled source lane.
+template <int N>
+__device__ __forceinline__ uint32_t row_ror(uint32_t x, uint32_t idle) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)idle, (int)x, 0x120 + N, 0xF, 0xF, false);
+}
+// Whole-wave max / min, the result in every lane: a butterfly over the 16
+// lanes of a row, then over rows through v_permlane16_swap / 32_swap.
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
+  x = max(x, row_ror<8>(x, 0u));
+  x = max(x, row_ror<4>(x, 0u));
+  x = max(x, row_ror<2>(x, 0u));
+  x = max(x, row_ror<1>(x, 0u));
+  const auto a = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  x = max(a[0], a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+  return max(b[0], b[1]);
+}
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) {
+  x = min(x, row_ror<8>(x, ~0u));
+  x = min(x, row_ror<4>(x, ~0u));
+  x = min(x, row_ror<2>(x, ~0u));
+  x = min(x, row_ror<1>(x, ~0u));
+  const auto a = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  x = min(a[0], a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+  return min(b[0], b[1]);
+}
+// fp64 x of lane l plus x of lane l ^ 16 (XOR16) or l ^ 32.
+template <bool XOR16>
+__device__ __forceinline__ double add_swapped(double x) {
+  const uint64_t u = (uint64_t)__double_as_longlong(x);
+  const uint32_t lo = (uint32_t)u, hi = (uint32_t)(u >> 32);
+  const auto l2 = XOR16 ? __builtin_amdgcn_permlane16_swap(lo, lo, false, false)
+                        : __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
+  const auto h2 = XOR16 ? __builtin_amdgcn_permlane16_swap(hi, hi, false, false)
+                        : __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
+  const double a = __longlong_as_double((long long)(((uint64_t)h2[0] << 32) | l2[0]));
+  const double b = __longlong_as_double((long long)(((uint64_t)h2[1] << 32) | l2[1]));
+  return a + b;
+}
+template <int N>
+__device__ __forceinline__ double row_ror_f64(double x) {
+  const uint64_t u = (uint64_t)__double_as_longlong(x);
+  const uint32_t lo = row_ror<N>((uint32_t)u, 0u), hi = row_ror<N>((uint32_t)(u >> 32), 0u);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+// Whole-wave fp64 sum (every lane gets a sum of all 64 values, in a
+// lane-dependent but fixed order).
+__device__ __forceinline__ double wave_sum_f64(double x) {
+  x += row_ror_f64<8>(x);
+  x += row_ror_f64<4>(x);
+  x += row_ror_f64<2>(x);
+  x += row_ror_f64<1>(x);
+  x = add_swapped<true>(x);
+  return add_swapped<false>(x);
+}
+
+// Fused row selection: query blocks per workgroup, and the 16-deep k-steps of
+// the split operands (steps 0..7: high parts of channels 16 s .. 16 s + 15,
+// steps 8..15: low parts of the same channels).
+constexpr int kFRows = 32;
+constexpr int kFSteps = 16;
+
+// Smallest fp32 >= x (x >= 0 or NaN).
+__device__ __forceinline__ float f32_round_up(double x) {
+  float f = (float)x;
+  if ((double)f < x) f = __uint_as_float(__float_as_uint(f) + 1u);
+  return f;
+}
+
+// Outputs of the pooling besides the fp64 sums, for the fused row selection
+// (all null otherwise): the sums split as hi + lo, hi = bf16(sum) and
+// lo = bf16(sum - hi), in MFMA operand order
+// [B*H][tile of 32 blocks][k-step][lane][8 channels] (lane = block % 32 +
+// 32 * (channel / 8 % 2)), and norm[b] = |sum| / n_b rounded up to fp32.
+struct PoolSplit {
+  uint16_t* qfrag;
+  uint16_t* kfrag;
+  float* qnorm;
+  float* knorm;
+  int ntiles;  // ceil(nb / 32)
+};
+
+// One wave pools one block of Q (blockIdx.z == 0) or K (== 1); a workgroup
+// takes 4 consecutive blocks of one (batch, head).  Lane l loads 16 bytes
+// (channels 8 (l % 16) .. +7) of rows l / 16, l / 16 + 4, ..., all loads in
+// flight before the sums; the four row groups are then added across lanes
+// (v_permlane16 / 32_swap).  No LDS.
+constexpr int kPoolWaves = 4;
+
+template <int BLOCK>
+__global__ __launch_bounds__(kPoolWaves * kWave) void pool_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, Strides qs, Strides ks,
-    int H, int N, int block, int nb, double* __restrict__ qhat, double* __restrict__ khat) {
+    int H, int N, int nb, double* __restrict__ qhat, double* __restrict__ khat,
+    PoolSplit split) {
   const bool is_k = blockIdx.z != 0;
   const uint16_t* x = is_k ? k : q;
   const Strides st = is_k ? ks : qs;
   double* out = is_k ? khat : qhat;
   const int bh = blockIdx.y;
   const int b = bh / H, h = bh - b * H;
-  const int i = blockIdx.x;
-  const int t0 = i * block;
-  const int n_i = min(block, N - t0);
+  const int i = blockIdx.x * kPoolWaves + (threadIdx.x >> 6);
+  if (i >= nb) return;  // uniform per wave
+  const int lane = threadIdx.x & (kWave - 1);
+  const int t0 = i * BLOCK;
+  const int n_i = min(BLOCK, N - t0);
   const uint16_t* base = x + b * st.b + h * st.h + (int64_t)t0 * st.n;
-
-  const int col8 = threadIdx.x & 15;  // 8 channels = 16 bytes
-  const int r0 = threadIdx.x >> 4;    // 16 row groups
+  const int c8 = lane & 15, r0 = lane >> 4;
+  constexpr int kLoads = BLOCK / 4;
+  u32x4 w[kLoads];
+#pragma unroll
+  for (int m = 0; m < kLoads; ++m) {
+    const int r = r0 + 4 * m;
+    w[m] = r < n_i ? ld16(base + (int64_t)r * st.n + c8 * 8) : (u32x4){0u, 0u, 0u, 0u};
+  }
   double acc[8];
 #pragma unroll
   for (int c = 0; c < 8; ++c) acc[c] = 0.0;
-  // block <= 128: at most 8 rows per thread, all loads issued before the sums
-  u32x4 w[kMaxBlock / 16];
 #pragma unroll
-  for (int m = 0; m < kMaxBlock / 16; ++m) {
-    const int r = r0 + 16 * m;
-    w[m] = r < n_i ? ld16(base + (int64_t)r * st.n + col8 * 8) : (u32x4){0u, 0u, 0u, 0u};
-  }
-#pragma unroll
-  for (int m = 0; m < kMaxBlock / 16; ++m)
+  for (int m = 0; m < kLoads; ++m)
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       acc[2 * e] += (double)bf16_lo(w[m][e]);
       acc[2 * e + 1] += (double)bf16_hi(w[m][e]);
     }
-  __shared__ double red[16][kHeadDim + 1];
+  // every lane of the four row groups ends with the block's sums of its
+  // 8 channels (exact: the order does not matter)
 #pragma unroll
-  for (int c = 0; c < 8; ++c) red[r0][col8 * 8 + c] = acc[c];
-  __syncthreads();
-  if (threadIdx.x < kHeadDim) {
-    double s = 0.0;
+  for (int c = 0; c < 8; ++c) acc[c] = add_swapped<false>(add_swapped<true>(acc[c]));
+  double* o = out + ((int64_t)bh * nb + i) * kHeadDim + 8 * c8;
+  if (r0 == 0) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) s += red[r][threadIdx.x];
-    out[((int64_t)bh * nb + i) * kHeadDim + threadIdx.x] = s;
+    for (int c = 0; c < 8; c += 2) *reinterpret_cast<f64x2*>(o + c) = (f64x2){acc[c], acc[c + 1]};
   }
+  if (split.qfrag == nullptr) return;  // uniform
+  // s = hi + lo + rest with |s - hi| <= 2^-8 |s| (fp32 then bf16 rounding,
+  // up to 2^-23 more), s - hi exact in fp64, |rest| <= 2^-16 |s| (1 + 2^-14)
+  u32x4 whi, wlo;
+  double sq = 0.0;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    uint32_t hh[2], ll[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const double sv = acc[2 * e + u];
+      hh[u] = f32_to_bf16_rne((float)sv);
+      ll[u] = f32_to_bf16_rne((float)(sv - (double)__uint_as_float(hh[u] << 16)));
+      sq = fma(sv, sv, sq);
+    }
+    whi[e] = hh[0] | (hh[1] << 16);
+    wlo[e] = ll[0] | (ll[1] << 16);
+  }
+  if (r0 == 0) {
+    uint16_t* frag = is_k ? split.kfrag : split.qfrag;
+    const int64_t slot = (((int64_t)bh * split.ntiles + (i >> 5)) * kFSteps + (c8 >> 1)) * kWave +
+                         (i & 31) + 32 * (c8 & 1);
+    st16(frag + slot * 8, whi);
+    st16(frag + (slot + 8 * kWave) * 8, wlo);
+  }
+  // |sum|^2 over the 16 lanes of a row (each row holds all 128 channels)
+  sq += row_ror_f64<8>(sq);
+  sq += row_ror_f64<4>(sq);
+  sq += row_ror_f64<2>(sq);
+  sq += row_ror_f64<1>(sq);
+  if (lane == 0)
+    (is_k ? split.knorm : split.qnorm)[(int64_t)bh * nb + i] =
+        f32_round_up(sqrt(sq) / (double)n_i);
 }
 
 // fp64 score GEMM on the matrix cores: one 64x64 tile of
@@ -83,8 +216,6 @@ constexpr int kSTile = 64;
 constexpr int kSDepth = 32;
 constexpr int kSStride = 34;
 constexpr int kSChunks = kSTile * kSDepth / 2 / 256;  // 16-byte chunks per thread per operand
-typedef __attribute__((__vector_size__(4 * sizeof(double)))) double f64x4;
-typedef __attribute__((__vector_size__(2 * sizeof(double)))) double f64x2;
 
 __global__ __launch_bounds__(256) void score_kernel(const double* __restrict__ qhat,
                                                    const double* __restrict__ khat, int N,
@@ -171,17 +302,6 @@ __device__ __forceinline__ uint64_t order_key(double s) {
   if (s == 0.0) s = 0.0;
   const uint64_t u = (uint64_t)__double_as_longlong(s);
   return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
-}
-
-__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) x = max(x, (uint32_t)__shfl_xor((int)x, o, kWave));
-  return x;
-}
-__device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) x = min(x, (uint32_t)__shfl_xor((int)x, o, kWave));
-  return x;
 }
 
 // Largest 32-bit T with count(member && v >= T) >= k over the wave (the k-th
@@ -390,6 +510,423 @@ hipError_t launch_topk_any(const double* scores, int nb, int rows, int k, int km
   return launch_topk<64>(scores, nb, rows, k, kmax, k_per_row, cs, idx, cnt, stream);
 }
 
+// ---- fused score + top-k (row mode) ---------------------------------------
+// One workgroup of 8 waves per 32 query blocks of a (batch, head); scores for
+// all nb key blocks stay in LDS as order-preserving 32-bit keys.
+//
+// Approximation.  With the pooled sums split as q = q1 + q2 + rq and
+// k = k1 + k2 + rk (bf16 parts from the pooling, |rq| <= 2^-16 |q| (1 + 2^-14)
+// per channel), a = (q1.k1 + q1.k2 + q2.k1) / (n_i n_j) is one chain of 24
+// bf16 MFMAs (exact products, fp32 sums) and a multiply by the fp32
+// reciprocal.  Per channel, the dropped terms q2 k2 + q1 rk + q2 rk + rq k are
+// below 3.1 * 2^-16 |q_c k_c| (1 + 2^-7); the 384 products sum to at most
+// 1.02 sum|q_c k_c|, and any order of 383 additions, each off by at most one
+// fp32 ulp of its result, adds 383 * 2^-23 of that; the scaling adds 3 * 2^-24.
+// In all |a - s| <= 9.5e-5 sum|q_c k_c| / (n_i n_j), and by Cauchy-Schwarz
+// sum|q_c k_c| <= |q| |k|, so with qn = |q_i| / n_i and kn_max = max_j
+// |k_j| / n_j (both rounded up by the pooling)
+//     E = 2^-13 qn kn_max + 2^-120 (1 + qn n_i + kn_max block)
+// bounds the error of every score of the row, the second term covering
+// values the matrix cores flush to zero.  It holds while qn n_i and
+// kn_max block stay below 2^60 (no fp32 overflow); other rows, and rows with
+// non-finite inputs, take the exact path.  The fp64 scores of the other paths
+// differ from s by ~1e-16 relative, far inside E.
+//
+// Classification.  With a_k, a_k1 the k-th and (k+1)-th largest
+// approximations of the row, a key block with a > a_k1 + 2E outranks every
+// block outside the k largest approximations, so it is among the k largest
+// scores; one with a < a_k - 2E is below at least k scores and is dropped.
+// The rest (the band) gets its exact fp64 score, and the k - (certain) best
+// of the band under (score desc, index asc) are kept.  When the thresholds
+// are compared as fp32 keys, they are rounded outwards.  The band is empty
+// unless the gap between the k-th and (k+1)-th score is within 4E; a band of
+// more than 64 blocks (heavy ties), an inconsistent count, or a row outside
+// the bound's range takes the exact path: every candidate rescored in fp64
+// and the selection of the unfused kernel run on the 64-bit keys.
+constexpr int kFWaves = 8;
+constexpr int kFThreads = kFWaves * kWave;
+constexpr int kFStrideBig = 1192;   // LDS key-row stride = largest nb: 152.6 KB of keys
+constexpr int kFStrideSmall = 584;  // 74.8 KB: two workgroups per CU
+constexpr double kScoreRelErr = 1.0 / 8192;
+
+// Order-preserving 32-bit key of an fp32 score (larger score -> larger key);
+// -0 and +0 map to the same key; every finite score maps above 0.
+__device__ __forceinline__ uint32_t order_key32(float a) {
+  if (a == 0.f) a = 0.f;
+  const uint32_t u = __float_as_uint(a);
+  return (u >> 31) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float key32_value(uint32_t key) {
+  return __uint_as_float((key >> 31) ? (key ^ 0x80000000u) : ~key);
+}
+
+// fp64 score of one block pair from the pooled sums.
+__device__ __forceinline__ double exact_score(const double* __restrict__ qrow,
+                                              const double* __restrict__ krow, int nn) {
+  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll 4
+  for (int c = 0; c < kHeadDim; c += 4) {
+    const f64x2 a0 = *reinterpret_cast<const f64x2*>(qrow + c);
+    const f64x2 a1 = *reinterpret_cast<const f64x2*>(qrow + c + 2);
+    const f64x2 b0 = *reinterpret_cast<const f64x2*>(krow + c);
+    const f64x2 b1 = *reinterpret_cast<const f64x2*>(krow + c + 2);
+    acc[0] = fma(a0[0], b0[0], acc[0]);
+    acc[1] = fma(a0[1], b0[1], acc[1]);
+    acc[2] = fma(a1[0], b1[0], acc[2]);
+    acc[3] = fma(a1[1], b1[1], acc[3]);
+  }
+  return ((acc[0] + acc[1]) + (acc[2] + acc[3])) / (double)nn;
+}
+
+// True for the lanes holding the `need` largest member keys (hi, lo words),
+// ties to the lower lane.  Requires 1 <= need <= count(member).
+__device__ __forceinline__ bool select_lanes(uint32_t hi, uint32_t lo, bool member, int need) {
+  const uint32_t h[1] = {hi}, l[1] = {lo};
+  const bool m[1] = {member};
+  bool exact;
+  const uint32_t thi = kth_largest32<1>(h, m, need, &exact);
+  if (exact) return member && hi >= thi;
+  const int gt = __popcll(__ballot(member && hi > thi));
+  const bool grp[1] = {member && hi == thi};
+  bool ex2;
+  const uint32_t tlo = kth_largest32<1>(l, grp, need - gt, &ex2);
+  const int gt2 = __popcll(__ballot(grp[0] && lo > tlo));
+  const bool eq = grp[0] && lo == tlo;
+  const int rank = __popcll(__ballot(eq) & lanes_below_mask());
+  return (member && (hi > thi || (hi == thi && lo > tlo))) || (eq && rank < need - gt - gt2);
+}
+
+// Exact path of one row: every candidate in [jlo, jhi) rescored in fp64.
+template <int KPL>
+__device__ void exact_row_select(const double* __restrict__ qrow,
+                                 const double* __restrict__ khead, const Shape& cs, int ni,
+                                 int jlo, int jhi, int k, int32_t* out) {
+  const int lane = threadIdx.x & (kWave - 1);
+  uint32_t hi[KPL], lo[KPL];
+  bool mem[KPL];
+  int jj[KPL];
+#pragma unroll
+  for (int t = 0; t < KPL; ++t) {
+    const int j = lane + kWave * t;
+    jj[t] = j;
+    mem[t] = j >= jlo && j < jhi;
+    uint64_t key = 0ull;
+    if (mem[t]) {
+      const int nj = min(cs.block, cs.N - j * cs.block);
+      key = order_key(exact_score(qrow, khead + (int64_t)j * kHeadDim, ni * nj));
+    }
+    hi[t] = (uint32_t)(key >> 32);
+    lo[t] = (uint32_t)key;
+  }
+  select_emit<KPL>(hi, lo, mem, jj, k, out);
+}
+
+template <int NBP>
+__global__ __launch_bounds__(kFThreads) void score_topk_kernel(
+    const uint16_t* __restrict__ qfrag, const uint16_t* __restrict__ kfrag,
+    const float* __restrict__ qnorm, const float* __restrict__ knorm,
+    const double* __restrict__ qhat, const double* __restrict__ khat, Shape cs, int k_all,
+    int kmax, int ntiles, int per_xcd, int32_t* __restrict__ idx, int32_t* __restrict__ cnt) {
+  constexpr int KPL = (NBP + kWave - 1) / kWave;
+  __shared__ uint32_t keys[kFRows * NBP];
+  __shared__ uint32_t cand[kFWaves][2][kWave];
+  __shared__ float wmax[kFWaves];
+  const int nb = cs.nb;
+  // Consecutive tiles (the same head's key blocks) run on one XCD: workgroup
+  // w goes to XCD w % 8, which takes the logical tiles [x, x + 1) * per_xcd.
+  const int logical = (int)(blockIdx.x & 7) * per_xcd + (int)(blockIdx.x >> 3);
+  if (logical >= cs.B * cs.H * ntiles) return;  // uniform
+  const int bh = logical / ntiles, it = logical - bh * ntiles;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int l32 = lane & 31, g = lane >> 5;
+
+  // qn of this wave's rows wave + 8 m (lane m), loaded ahead of the products
+  float qn_rows = 0.f;
+  if (lane < kFRows / kFWaves && it * kFRows + wave + kFWaves * lane < nb)
+    qn_rows = qnorm[(int64_t)bh * nb + it * kFRows + wave + kFWaves * lane];
+  // kn_max of the head (a non-finite norm makes it +inf)
+  float m = 0.f;
+  for (int j = threadIdx.x; j < nb; j += kFThreads) {
+    const float v = knorm[(int64_t)bh * nb + j];
+    m = v <= 3.4028235e38f ? fmaxf(m, v) : __builtin_huge_valf();
+  }
+  m = wave_max(m);
+  if (lane == 0) wmax[wave] = m;
+
+  {  // approximate scores of the 32 query blocks against every key block
+    const u32x4* qsrc =
+        reinterpret_cast<const u32x4*>(qfrag) + ((int64_t)bh * ntiles + it) * kFSteps * kWave + lane;
+    bf16x8 qa[kFSteps];
+#pragma unroll
+    for (int st = 0; st < kFSteps; ++st) qa[st] = __builtin_bit_cast(bf16x8, qsrc[st * kWave]);
+    const u32x4* ksrc =
+        reinterpret_cast<const u32x4*>(kfrag) + (int64_t)bh * ntiles * kFSteps * kWave + lane;
+    auto load = [&](bf16x8 (&kb)[kFSteps], int jt) {
+#pragma unroll
+      for (int st = 0; st < kFSteps; ++st)
+        kb[st] = __builtin_bit_cast(bf16x8, ksrc[((int64_t)jt * kFSteps + st) * kWave]);
+    };
+    auto products = [&](const bf16x8 (&kb)[kFSteps]) {
+      f32x16 acc = {};
+#pragma unroll
+      for (int st = 0; st < 8; ++st)
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[8 + st], kb[st], acc, 0, 0, 0);
+#pragma unroll
+      for (int st = 0; st < 8; ++st)
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[st], kb[8 + st], acc, 0, 0, 0);
+#pragma unroll
+      for (int st = 0; st < 8; ++st)
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[st], kb[st], acc, 0, 0, 0);
+      return acc;
+    };
+    // Keys of a tile: lane holds key block j, query blocks 8 (r / 4) + 4 g +
+    // r % 4 of the tile (rows past nb are written but never read).  Every
+    // query block is scaled as if it held `block` tokens: only the last one
+    // can be shorter, and a common factor of its row keeps its order (its
+    // error bound is scaled by the same factor).  fma(.., +0) turns -0 to +0.
+    auto store_keys = [&](const f32x16& acc, int jt) {
+      const int j = jt * 32 + l32;
+      if (j < nb) {
+        const float inv =
+            __builtin_amdgcn_rcpf((float)(cs.block * min(cs.block, cs.N - j * cs.block)));
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const uint32_t u = __float_as_uint(fmaf(acc[r], inv, 0.f));
+          keys[(8 * (r >> 2) + 4 * g + (r & 3)) * NBP + j] =
+              u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);
+        }
+      }
+    };
+    // Two operand buffers: the next tile's loads are in flight during the
+    // current tile's products, and the previous tile's keys are stored while
+    // the current tile's products run.  The loads are unconditional (clamped
+    // to the last tile) so that the waits before the products count only the
+    // current tile's.
+    bf16x8 ka[kFSteps], kc[kFSteps];
+    f32x16 prev = {};
+    int jprev = -1;
+    load(ka, min(wave, ntiles - 1));
+    for (int jt = wave; jt < ntiles; jt += 2 * kFWaves) {
+      load(kc, min(jt + kFWaves, ntiles - 1));
+      __builtin_amdgcn_sched_barrier(0);
+      f32x16 cur = products(ka);
+      if (jprev >= 0) store_keys(prev, jprev);
+      prev = cur;
+      jprev = jt;
+      __builtin_amdgcn_sched_barrier(0);
+      load(ka, min(jt + 2 * kFWaves, ntiles - 1));
+      __builtin_amdgcn_sched_barrier(0);
+      if (jt + kFWaves < ntiles) {
+        cur = products(kc);
+        store_keys(prev, jprev);
+        prev = cur;
+        jprev = jt + kFWaves;
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (jprev >= 0) store_keys(prev, jprev);
+  }
+  __syncthreads();
+  float kn_max = wmax[0];
+#pragma unroll
+  for (int w = 1; w < kFWaves; ++w) kn_max = fmaxf(kn_max, wmax[w]);
+  const uint64_t below = lanes_below_mask();
+  const double* khead = khat + (int64_t)bh * nb * kHeadDim;
+  uint32_t* ckey = cand[wave][0];
+  uint32_t* cidx = cand[wave][1];
+
+  for (int rm = 0; rm < kFRows / kFWaves; ++rm) {
+    const int rr = wave + kFWaves * rm;
+    const int i = it * kFRows + rr;
+    if (i >= nb) break;  // uniform
+    const int64_t row = (int64_t)bh * nb + i;
+    const int ni = min(cs.block, cs.N - i * cs.block);
+    // candidate key blocks, as in the unfused row top-k
+    int jlo = 0, jhi = nb;
+    if (cs.causal_chunk > 0) {
+      const int first = i * cs.block;
+      const int last = min(first + cs.block, cs.N) - 1;
+      jlo = causal_lo(cs, first) / cs.block;
+      jhi = (causal_hi(cs, last) + cs.block - 1) / cs.block;
+    }
+    const int k = min(k_all, jhi - jlo);
+    int32_t* out = idx + row * kmax;
+    const double* qrow = qhat + row * kHeadDim;
+    const float qn = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(qn_rows), rm));
+    // the keys of a short last row are scaled by ni / block, and so is E
+    const double E = (kScoreRelErr * (double)qn * (double)kn_max +
+                      0x1p-120 * (1.0 + (double)qn * ni + (double)kn_max * cs.block)) *
+                     ((double)ni / cs.block);
+    const bool bounded = (double)qn * ni <= 0x1p60 && (double)kn_max * cs.block <= 0x1p60;
+    // keys of a_k - 2E rounded down and a_k1 + 2E rounded up
+    uint32_t KLO = 0, KHI = 0;
+    auto thresholds = [&](uint32_t kk, uint32_t kk1) {
+      const double lo = (double)key32_value(kk) - 2.0 * E;
+      const double hi = (double)key32_value(kk1) + 2.0 * E;
+      const float flo = (float)lo, fhi = (float)hi;
+      KLO = order_key32(flo) - ((double)flo > lo ? 1u : 0u);
+      KHI = order_key32(fhi) + ((double)fhi < hi ? 1u : 0u);
+    };
+    if (k >= jhi - jlo) {
+      for (int p = lane; p < k; p += kWave) out[p] = jlo + p;
+    } else if (!bounded) {
+      exact_row_select<KPL>(qrow, khead, cs, ni, jlo, jhi, k, out);
+    } else {
+      uint32_t key[KPL];
+      uint32_t mk = 0;  // 0: not a candidate (below every score's key)
+#pragma unroll
+      for (int t = 0; t < KPL; ++t) {
+        const int j = lane + kWave * t;
+        key[t] = (j >= jlo && j < jhi) ? keys[rr * NBP + j] : 0u;
+        mk = max(mk, key[t]);
+      }
+      // As in the unfused kernel, the k-th largest lane maximum P bounds the
+      // k-th key from below; the keys >= P are compacted in index order.
+      bool done = false, have = false;
+      const bool enough = __popcll(__ballot(mk != 0u)) >= k;
+      uint32_t P = 0;
+      int c = 0;
+      if (enough) {
+        const uint32_t mv[1] = {mk};
+        const bool mm[1] = {mk != 0u};
+        bool ex;
+        P = kth_largest32<1>(mv, mm, k, &ex);
+#pragma unroll
+        for (int t = 0; t < KPL; ++t) {
+          const bool ok = key[t] >= P;
+          const uint64_t m = __ballot(ok);
+          const int pos = c + __popcll(m & below);
+          if (ok && pos < kWave) {
+            ckey[pos] = key[t];
+            cidx[pos] = (uint32_t)(lane + kWave * t);
+          }
+          c += __popcll(m);
+        }
+      }
+      if (enough && c <= kWave) {
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's writes landed
+        __builtin_amdgcn_wave_barrier();
+        const bool cm = lane < c;
+        const uint32_t ck = cm ? ckey[lane] : 0u;
+        const int cj = cm ? (int)cidx[lane] : 0;
+        const uint32_t cv[1] = {ck};
+        const bool cmm[1] = {cm};
+        bool ex;
+        // below P only when exactly k keys are >= P: then P itself separates them
+        const uint32_t T = max(kth_largest32<1>(cv, cmm, k, &ex), P);
+        // a_k and a_k1: the extremes on either side of T, or T itself when it
+        // is tied across the k-th place
+        uint32_t kk = T, kk1 = T;
+        if (__popcll(__ballot(cm && ck >= T)) == k) {
+          kk = wave_min_u32(cm && ck >= T ? ck : ~0u);
+          if (c > k) {
+            kk1 = wave_max_u32(cm && ck < T ? ck : 0u);
+          } else {  // the (k+1)-th key is the row's largest below P
+            uint32_t mx = 0u;
+#pragma unroll
+            for (int t = 0; t < KPL; ++t) mx = max(mx, key[t] < P ? key[t] : 0u);
+            kk1 = wave_max_u32(mx);
+          }
+        }
+        thresholds(kk, kk1);
+        have = true;
+        // empty band: the k keys above KHI are all among the candidates
+        const bool sel = cm && ck > KHI;
+        const uint64_t m = __ballot(sel);
+        if (KLO > KHI && __popcll(m) == k) {
+          if (sel) out[__popcll(m & below)] = cj;
+          done = true;
+        }
+      }
+      if (!done) {
+        if (!have) {
+          bool mem[KPL];
+#pragma unroll
+          for (int t = 0; t < KPL; ++t) mem[t] = key[t] != 0u;
+          bool ex;
+          const uint32_t T = kth_largest32<KPL>(key, mem, k, &ex);
+          int cge = 0;
+          uint32_t mn = ~0u, mx = 0u;
+#pragma unroll
+          for (int t = 0; t < KPL; ++t) {
+            const bool ge = key[t] >= T && key[t] != 0u;
+            cge += __popcll(__ballot(ge));
+            if (ge) mn = min(mn, key[t]);
+            else mx = max(mx, key[t]);
+          }
+          if (cge == k) thresholds(wave_min_u32(mn), wave_max_u32(mx));
+          else thresholds(T, T);
+        }
+        int cin = 0, cband = 0;
+#pragma unroll
+        for (int t = 0; t < KPL; ++t) {
+          cin += __popcll(__ballot(key[t] > KHI));
+          cband += __popcll(__ballot(key[t] != 0u && key[t] <= KHI && key[t] >= KLO));
+        }
+        if (cband <= kWave && cin <= k && cin + cband >= k) {
+          // compact the band's indices; rescore them in fp64, all lanes on
+          // one block at a time (lane l: channels 2 l, 2 l + 1)
+          int base = 0;
+#pragma unroll
+          for (int t = 0; t < KPL; ++t) {
+            const bool b = key[t] != 0u && key[t] <= KHI && key[t] >= KLO;
+            const uint64_t m = __ballot(b);
+            if (b) cidx[base + __popcll(m & below)] = (uint32_t)(lane + kWave * t);
+            base += __popcll(m);
+          }
+          __builtin_amdgcn_s_waitcnt(0xC07F);
+          __builtin_amdgcn_wave_barrier();
+          const f64x2 qv = *reinterpret_cast<const f64x2*>(qrow + 2 * lane);
+          uint32_t bhi = 0u, blo = 0u;
+          for (int m0 = 0; m0 < cband; m0 += 4) {  // uniform
+            f64x2 kv[4];
+            int jm[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              jm[u] = (int)cidx[min(m0 + u, cband - 1)];
+              kv[u] = *reinterpret_cast<const f64x2*>(khead + (int64_t)jm[u] * kHeadDim + 2 * lane);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const double d = wave_sum_f64(fma(qv[0], kv[u][0], qv[1] * kv[u][1]));
+              const int nj = min(cs.block, cs.N - jm[u] * cs.block);
+              const uint64_t k64 = order_key(d / (double)(ni * nj));
+              if (lane == m0 + u) {
+                bhi = (uint32_t)(k64 >> 32);
+                blo = (uint32_t)k64;
+              }
+            }
+          }
+          const bool sel_band = cin < k && select_lanes(bhi, blo, lane < cband, k - cin);
+          ckey[lane] = sel_band ? 1u : 0u;
+          __builtin_amdgcn_s_waitcnt(0xC07F);
+          __builtin_amdgcn_wave_barrier();
+          int taken = 0;
+          base = 0;
+#pragma unroll
+          for (int t = 0; t < KPL; ++t) {
+            const bool b = key[t] != 0u && key[t] <= KHI && key[t] >= KLO;
+            const uint64_t bmask = __ballot(b);
+            const bool sel = key[t] > KHI || (b && ckey[base + __popcll(bmask & below)] != 0u);
+            base += __popcll(bmask);
+            const uint64_t m = __ballot(sel);
+            const int pos = taken + __popcll(m & below);
+            if (sel && pos < k) out[pos] = lane + kWave * t;
+            taken += __popcll(m);
+          }
+        } else {
+          exact_row_select<KPL>(qrow, khead, cs, ni, jlo, jhi, k, out);
+        }
+      }
+    }
+    for (int p = k + lane; p < kmax; p += kWave) out[p] = -1;
+    if (lane == 0) cnt[row] = k;
+    // (the next row rewrites this wave's cand slots: a wave's LDS accesses
+    // complete in order, so the reads above see this row's values)
+  }
+}
+
 // ---- whole-head ragged selection ------------------------------------------
 // Per (batch, head): every query block keeps its best key block; the other
 // (budget - nqb) pairs are the largest of the remaining ones under (score
@@ -596,7 +1133,34 @@ __global__ __launch_bounds__(kRowKThreads) void head_rowk_kernel(int nb, int kma
 
 }  // namespace
 
+static void launch_pool(const Shape& s, const void* q, Strides qs, const void* k, Strides ks,
+                        double* qhat, double* khat, const PoolSplit& sp, hipStream_t stream) {
+  const dim3 grid((s.nb + kPoolWaves - 1) / kPoolWaves, (unsigned)(s.B * s.H), 2);
+  const auto* qq = static_cast<const uint16_t*>(q);
+  const auto* kk = static_cast<const uint16_t*>(k);
+  if (s.block == 64)
+    pool_kernel<64><<<grid, kPoolWaves * kWave, 0, stream>>>(qq, kk, qs, ks, s.H, s.N, s.nb,
+                                                             qhat, khat, sp);
+  else
+    pool_kernel<128><<<grid, kPoolWaves * kWave, 0, stream>>>(qq, kk, qs, ks, s.H, s.N, s.nb,
+                                                              qhat, khat, sp);
+}
+
+// Row mode: pooled sums, then either the fused path's split operands and
+// norms (nb <= kFStrideBig) or the score matrix.
 size_t select_workspace_bytes(const Shape& s) {
+  const size_t bh = (size_t)s.B * s.H;
+  const size_t pooled = bh * s.nb * kHeadDim * sizeof(double) * 2;
+  if (s.nb <= kFStrideBig) {
+    const size_t ntiles = (s.nb + kFRows - 1) / kFRows;
+    return pooled + 2 * bh * ntiles * kFSteps * kWave * 8 * sizeof(uint16_t) +
+           2 * bh * s.nb * sizeof(float);
+  }
+  return pooled + bh * s.nb * s.nb * sizeof(double);
+}
+
+// Whole-head mode: pooled sums, the score matrix and the radix-select state.
+size_t select_head_workspace_bytes(const Shape& s) {
   const size_t bh = (size_t)s.B * s.H;
   const size_t rows = bh * s.nb;
   return bh * s.nb * kHeadDim * sizeof(double) * 2 + bh * s.nb * s.nb * sizeof(double) +
@@ -610,9 +1174,7 @@ static hipError_t launch_pool_score(const Shape& s, const void* q, Strides qs, c
   double* qhat = static_cast<double*>(ws);
   double* khat = qhat + bh * s.nb * kHeadDim;
   double* scores = khat + bh * s.nb * kHeadDim;
-  pool_kernel<<<dim3(s.nb, bh, 2), kPoolThreads, 0, stream>>>(
-      static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), qs, ks, s.H, s.N,
-      s.block, s.nb, qhat, khat);
+  launch_pool(s, q, qs, k, ks, qhat, khat, PoolSplit{}, stream);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int tiles = (s.nb + kSTile - 1) / kSTile;
@@ -625,6 +1187,32 @@ static hipError_t launch_pool_score(const Shape& s, const void* q, Strides qs, c
 hipError_t launch_select_row(const Shape& s, const void* q, Strides qs, const void* k,
                              Strides ks, int topk, int kmax, int32_t* idx, int32_t* cnt,
                              void* ws, hipStream_t stream) {
+  if (s.nb <= kFStrideBig) {
+    const size_t bh = (size_t)s.B * s.H;
+    const int ntiles = (s.nb + kFRows - 1) / kFRows;
+    const size_t frag = bh * ntiles * kFSteps * kWave * 8;  // uint16 per operand
+    double* qhat = static_cast<double*>(ws);
+    double* khat = qhat + bh * s.nb * kHeadDim;
+    PoolSplit sp;
+    sp.qfrag = reinterpret_cast<uint16_t*>(khat + bh * s.nb * kHeadDim);
+    sp.kfrag = sp.qfrag + frag;
+    sp.qnorm = reinterpret_cast<float*>(sp.kfrag + frag);
+    sp.knorm = sp.qnorm + bh * s.nb;
+    sp.ntiles = ntiles;
+    launch_pool(s, q, qs, k, ks, qhat, khat, sp, stream);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int per_xcd = (int)((bh * ntiles + 7) / 8);
+    if (s.nb <= kFStrideSmall)
+      score_topk_kernel<kFStrideSmall><<<8 * per_xcd, kFThreads, 0, stream>>>(
+          sp.qfrag, sp.kfrag, sp.qnorm, sp.knorm, qhat, khat, s, topk, kmax, ntiles, per_xcd,
+          idx, cnt);
+    else
+      score_topk_kernel<kFStrideBig><<<8 * per_xcd, kFThreads, 0, stream>>>(
+          sp.qfrag, sp.kfrag, sp.qnorm, sp.knorm, qhat, khat, s, topk, kmax, ntiles, per_xcd,
+          idx, cnt);
+    return hipGetLastError();
+  }
   double* scores = nullptr;
   hipError_t e = launch_pool_score(s, q, qs, k, ks, ws, &scores, stream);
   if (e != hipSuccess) return e;

@@ -59,10 +59,21 @@ def test_workspace_size_formula():
     lib = sa.library()
     ds = desc(B=1, H=40, N=75600)
     nb = 1182
-    # pooled q/k (fp64), scores (fp64), then the whole-head mode's state: per
-    # head 32 B of radix state and a 256-bin histogram, per row 3 int32
+    # row mode: pooled q/k (fp64), the bf16 hi/lo operands of the on-chip
+    # scores in tiles of 32 blocks (16 KB per tile and operand), fp32 norms
     assert lib.sparse_attn_workspace_size(ctypes.byref(ds), 0, 36) == \
+        40 * nb * 128 * 8 * 2 + 2 * 40 * 37 * 16384 + 2 * 40 * nb * 4
+    # whole-head mode: pooled q/k, scores (fp64), then per head 32 B of radix
+    # state and a 256-bin histogram, per row 3 int32
+    assert lib.sparse_attn_workspace_size(ctypes.byref(ds), sa.SA_OP_SELECT_HEAD, 36) == \
         40 * nb * 128 * 8 * 2 + 40 * nb * nb * 8 + 40 * 32 + 40 * 256 * 4 + 3 * 40 * nb * 4
+    # row mode past 1192 blocks: pooled q/k and the fp64 score matrix
+    big = desc(B=1, H=2, N=1193 * 64)
+    assert lib.sparse_attn_workspace_size(ctypes.byref(big), 0, 36) == \
+        2 * 1193 * 128 * 8 * 2 + 2 * 1193 * 1193 * 8
+    edge = desc(B=1, H=2, N=1192 * 64)
+    assert lib.sparse_attn_workspace_size(ctypes.byref(edge), 0, 36) == \
+        2 * 1192 * 128 * 8 * 2 + 2 * 2 * 38 * 16384 + 2 * 2 * 1192 * 4
     # scheduler: 16 class counters per chunk of 1024 query tiles, plus one row
     assert lib.sparse_attn_workspace_size(ctypes.byref(ds), 1, 36) == (47 + 1) * 16 * 4
     assert lib.sparse_attn_workspace_size(ctypes.byref(ds), 1, 0) == 0
@@ -113,6 +124,16 @@ def test_select_rejects_bad_arguments():
     assert call(P, P, 1, 63, P, P, 7, P, WS, None) == -1            # head budget < nqb
     assert call(P, P, 1, 64 * 64 + 1, P, P, 7, P, WS, None) == -1   # head budget > nqb*nkb
     assert call(P, P, 0, 7, P, P, 7, P, 100, None) == -3            # workspace too small
+    # each mode checks against its own size (at 1182 blocks the whole-head
+    # mode's score matrix makes it the larger)
+    big = desc(N=75600)
+    row = lib.sparse_attn_workspace_size(ctypes.byref(big), sa.SA_OP_SELECT, 7)
+    head = lib.sparse_attn_workspace_size(ctypes.byref(big), sa.SA_OP_SELECT_HEAD, 7)
+    assert 0 < row < head
+    sel = lambda *a: lib.sparse_attn_select(ctypes.byref(big), *a)
+    assert sel(P, P, 0, 7, P, P, 7, P, row - 1, None) == -3
+    assert sel(P, P, 1, 5000, P, P, 64, P, row, None) == -3
+    assert sel(P, P, 1, 5000, P, P, 64, P, head - 1, None) == -3
     ds.q_stride[2] = 130                                            # stride not multiple of 8
     assert call(P, P, 0, 7, P, P, 7, P, WS, None) == -1
 
