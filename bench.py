@@ -549,7 +549,9 @@ def bench_fp8(args, sa, W, dev):
     cnt = torch.empty(B, H, nb, dtype=torch.int32, device=dev)
     o = torch.empty_like(q)
     lse = torch.empty(B, H, N, dtype=torch.float32, device=dev)
-    x8 = [torch.empty(B, H, N, d, dtype=torch.uint8, device=dev) for _ in range(3)]
+    # Q row-major, K and V in the forward's tile layouts
+    x8 = [torch.empty(B, H, N, d, dtype=torch.uint8, device=dev)] + \
+        [torch.empty(B, H, -(-N // 64), 8192, dtype=torch.uint8, device=dev) for _ in range(2)]
     sc = [torch.empty(B, H, nb, dtype=torch.float32, device=dev) for _ in range(3)]
     desc = sa.make_desc(q, kk, v, o, block=block)
     ws_sel = torch.empty(sa.sparse_attn_workspace_size(desc, sa.SA_OP_SELECT, k),
@@ -565,8 +567,9 @@ def bench_fp8(args, sa, W, dev):
         sa.sparse_attn_select(q, kk, k, block=block, idx=idx, cnt=cnt, ws=ws_sel)
         if e:
             e[1].record()
-        for t, a8, s8 in zip((q, kk, v), x8, sc):
-            sa.sparse_attn_quant_fp8(t, block=block, x8=a8, scale=s8)
+        sa.sparse_attn_quant_fp8(q, block=block, x8=x8[0], scale=sc[0])
+        sa.sparse_attn_quant_fp8_tiles(kk, sa.SA_FP8_K, block=block, x8=x8[1], scale=sc[1])
+        sa.sparse_attn_quant_fp8_tiles(v, sa.SA_FP8_V, block=block, x8=x8[2], scale=sc[2])
         if e:
             e[2].record()
         sa.sparse_attn_schedule(cnt, N, k, block=block, order=order, ws=ws_sch)

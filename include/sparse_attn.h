@@ -228,14 +228,43 @@ int sparse_attn_fwd(const sparse_attn_desc* desc, const void* q, const void* k,
 int sparse_attn_quant_fp8(const sparse_attn_desc* desc, const void* x, const int64_t x_stride[3],
                           uint8_t* x8, float* scale, void* stream);
 
+/* Operands of sparse_attn_quant_fp8_tiles. */
+enum { SA_FP8_K = 0, SA_FP8_V = 1 };
+
+/*
+ * The quantisation of sparse_attn_quant_fp8 (same codes, same scales), with
+ * the codes written in the order in which the fp8 forward's matrix cores
+ * consume K (operand SA_FP8_K) or V (SA_FP8_V), so that the forward reads
+ * them with contiguous loads and no staging.  Per (b, h): T = ceil(L / 64)
+ * tiles of 64 keys, 8192 bytes each; in tile t (keys 64 t .. 64 t + 63),
+ * byte 16 c + e (c < 512, e < 16), with c = 64 f + l + 32 g (l < 32, g < 2):
+ *   SA_FP8_K, f = 2 (2 rt + ks) + hf: key 64 t + 32 rt + l,
+ *             channel 64 ks + 32 g + 16 hf + e
+ *   SA_FP8_V, f = 2 dt + hf (dt < 4): channel 32 dt + l,
+ *             key 64 t + 32 hf + 8 (e / 4) + 4 g + e % 4
+ * Keys at or past L are code 0.
+ *  x        bf16 [B][H][L][d] via x_stride (head_dim must be 128)
+ *  operand  SA_FP8_K or SA_FP8_V (else SA_ERR_INVALID_ARG)
+ *  x8       uint8 out, sparse_attn_fp8_tiles_bytes(desc) bytes, [B][H][T][8192]
+ *  scale    fp32 out, contiguous [B][H][nb]
+ */
+int sparse_attn_quant_fp8_tiles(const sparse_attn_desc* desc, const void* x,
+                                const int64_t x_stride[3], int32_t operand, uint8_t* x8,
+                                float* scale, void* stream);
+
+/* Bytes of one tile-layout operand, B * H * ceil(L / 64) * 8192; -1 for an
+ * invalid descriptor. */
+int64_t sparse_attn_fp8_tiles_bytes(const sparse_attn_desc* desc);
+
 /*
  * Sparse branch on fp8 operands: the same result as sparse_attn_fwd computed
  * on the dequantised Q = sq * q8, K = sk * k8, V = sv * v8, with QK^T and PV on
  * the fp8 matrix cores; the probabilities are rounded to e4m3 for the PV
- * product.  q8, k8, v8 are contiguous [B][H][L][d] e4m3 and sq, sk, sv are
- * [B][H][nb] power-of-two scales, both as written by sparse_attn_quant_fp8.
- * o (via desc->o_stride), lse, idx, cnt, kmax and order are as for
- * sparse_attn_fwd.
+ * product.  q8 is contiguous [B][H][L][d] e4m3 as written by
+ * sparse_attn_quant_fp8; k8 and v8 are in the tile layouts written by
+ * sparse_attn_quant_fp8_tiles (SA_FP8_K, SA_FP8_V); sq, sk, sv are the
+ * [B][H][nb] power-of-two scales of those calls.  o (via desc->o_stride),
+ * lse, idx, cnt, kmax and order are as for sparse_attn_fwd.
  */
 int sparse_attn_fwd_fp8(const sparse_attn_desc* desc, const uint8_t* q8, const float* sq,
                         const uint8_t* k8, const float* sk, const uint8_t* v8, const float* sv,

@@ -18,7 +18,8 @@ __all__ = [
     "SA_OP_SELECT", "SA_OP_SCHEDULE", "SA_OP_SELECT_HEAD", "library", "sparse_attn_version",
     "sparse_attn_status_str", "sparse_attn_keep_count", "sparse_attn_workspace_size",
     "sparse_attn_num_tiles", "sparse_attn_select", "sparse_attn_schedule", "sparse_attn_fwd",
-    "sparse_attn_schedule_static", "sparse_attn_quant_fp8", "sparse_attn_fwd_fp8", "sparse_attn_comp_state",
+    "sparse_attn_schedule_static", "sparse_attn_quant_fp8", "sparse_attn_quant_fp8_tiles",
+    "sparse_attn_fp8_tiles_bytes", "SA_FP8_K", "SA_FP8_V", "sparse_attn_fwd_fp8", "sparse_attn_comp_state",
     "sparse_attn_comp_out", "SA_OP_COMP_STATE", "COMP_RANK", "make_desc", "EXPORTED_SYMBOLS",
     "sparse_attn_quant_rows_fp8", "sparse_attn_linear_w8a8", "sparse_attn_bwd", "SA_OP_BWD",
 ]
@@ -37,7 +38,8 @@ COMP_RANK = 64
 EXPORTED_SYMBOLS = (
     "sparse_attn_version", "sparse_attn_status_str", "sparse_attn_keep_count",
     "sparse_attn_workspace_size", "sparse_attn_num_tiles", "sparse_attn_select",
-    "sparse_attn_schedule", "sparse_attn_fwd", "sparse_attn_quant_fp8", "sparse_attn_fwd_fp8",
+    "sparse_attn_schedule", "sparse_attn_fwd", "sparse_attn_quant_fp8",
+    "sparse_attn_quant_fp8_tiles", "sparse_attn_fp8_tiles_bytes", "sparse_attn_fwd_fp8",
     "sparse_attn_comp_state", "sparse_attn_comp_out", "sparse_attn_quant_rows_fp8",
     "sparse_attn_linear_w8a8", "sparse_attn_bwd", "sparse_attn_schedule_static",
 )
@@ -90,6 +92,9 @@ def library() -> ctypes.CDLL:
                                                _P]),
             "sparse_attn_quant_fp8": (ctypes.c_int, [D, _P, ctypes.POINTER(ctypes.c_int64),
                                                      _P, _P, _P]),
+            "sparse_attn_quant_fp8_tiles": (ctypes.c_int, [D, _P, ctypes.POINTER(ctypes.c_int64),
+                                                             ctypes.c_int32, _P, _P, _P]),
+            "sparse_attn_fp8_tiles_bytes": (ctypes.c_int64, [D]),
             "sparse_attn_fwd_fp8": (ctypes.c_int, [D, _P, _P, _P, _P, _P, _P, _P, _P,
                                                    ctypes.c_int32, _P, _P, _P, _P]),
             "sparse_attn_comp_state": (ctypes.c_int, [D, ctypes.c_int32, _P, _I64P, _P, _P, _P,
@@ -289,11 +294,35 @@ def sparse_attn_quant_fp8(x, block: int = 64, x8=None, scale=None):
     return x8, scale
 
 
+SA_FP8_K, SA_FP8_V = 0, 1
+
+
+def sparse_attn_quant_fp8_tiles(x, operand: int, block: int = 64, x8=None, scale=None):
+    """The quantisation of sparse_attn_quant_fp8 with the codes in the fp8
+    forward's K (SA_FP8_K) or V (SA_FP8_V) operand order.  Returns (x8 uint8
+    [B, H, ceil(N / 64), 8192], scale fp32 [B, H, nb])."""
+    B, H, N, _ = x.shape
+    desc = make_desc(x, block=block)
+    if x8 is None:
+        x8 = torch.empty(B, H, -(-N // 64), 8192, dtype=torch.uint8, device=x.device)
+    if scale is None:
+        scale = torch.empty(B, H, _num_blocks(N, block), dtype=torch.float32, device=x.device)
+    _dense(x8, "x8", torch.uint8)
+    if x8.numel() < library().sparse_attn_fp8_tiles_bytes(ctypes.byref(desc)):
+        raise ValueError("x8 is smaller than sparse_attn_fp8_tiles_bytes")
+    xs = (ctypes.c_int64 * 3)(*_strides(x))
+    st = library().sparse_attn_quant_fp8_tiles(ctypes.byref(desc), _ptr(x), xs, operand,
+                                               _ptr(x8), _ptr(scale), _stream(x))
+    _check(st, "sparse_attn_quant_fp8_tiles")
+    return x8, scale
+
+
 def sparse_attn_fwd_fp8(q8, sq, k8, sk, v8, sv, idx, cnt, block: int = 64,
                         softmax_scale: float = 0.0, with_lse: bool = True, order=None, o=None,
                         lse=None, causal=None):
-    """Block-sparse attention forward on e4m3 operands from
-    sparse_attn_quant_fp8.  Returns (o bf16 [B, H, N, 128], lse or None)."""
+    """Block-sparse attention forward on e4m3 operands: q8 from
+    sparse_attn_quant_fp8, k8 and v8 from sparse_attn_quant_fp8_tiles
+    (SA_FP8_K, SA_FP8_V).  Returns (o bf16 [B, H, N, 128], lse or None)."""
     B, H, N, d = q8.shape
     kmax = idx.shape[-1]
     _dense(idx, "idx"), _dense(cnt, "cnt"), _dense(order, "order")

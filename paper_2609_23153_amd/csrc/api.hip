@@ -212,6 +212,25 @@ int sparse_attn_quant_fp8(const sparse_attn_desc* desc, const void* x, const int
       sa::launch_quant_fp8(s, x, to_strides(x_stride), x8, scale, static_cast<hipStream_t>(stream)));
 }
 
+int sparse_attn_quant_fp8_tiles(const sparse_attn_desc* desc, const void* x,
+                                const int64_t x_stride[3], int32_t operand, uint8_t* x8,
+                                float* scale, void* stream) {
+  Shape s;
+  int st = check_desc(desc, &s);
+  if (st != SA_OK) return st;
+  if (!x || !x_stride || !x8 || !scale) return SA_ERR_INVALID_ARG;
+  if (operand != SA_FP8_K && operand != SA_FP8_V) return SA_ERR_INVALID_ARG;
+  if (!aligned16(x) || !aligned16(x8) || !strides_ok(x_stride)) return SA_ERR_INVALID_ARG;
+  return launch_status(sa::launch_quant_fp8_tiles(s, x, to_strides(x_stride), operand == SA_FP8_V,
+                                                  x8, scale, static_cast<hipStream_t>(stream)));
+}
+
+int64_t sparse_attn_fp8_tiles_bytes(const sparse_attn_desc* desc) {
+  Shape s;
+  if (check_desc(desc, &s) != SA_OK) return -1;
+  return (int64_t)s.B * s.H * ((s.N + 63) / 64) * 8192;
+}
+
 int sparse_attn_fwd_fp8(const sparse_attn_desc* desc, const uint8_t* q8, const float* sq,
                         const uint8_t* k8, const float* sk, const uint8_t* v8, const float* sv,
                         const int32_t* idx, const int32_t* cnt, int32_t kmax,

@@ -7,49 +7,38 @@
 // as E8M0 block scales of v_mfma_scale_f32_32x32x64_f8f6f4, so the scores come
 // out dequantised with no extra VALU work.
 //
-// One workgroup = 4 wavefronts = one 64-row query tile; two workgroups share
-// a CU.  A 32x32x64 fp8 MFMA contracts 64 keys, so each wave takes a whole
-// 64-key tile: waves 0/1 own query rows 0-31 / 32-63 of the first tile of
-// each pair of tiles in the list, waves 2/3 of the second.  Per wave and tile:
-//   S^T (64 keys x 32 queries) = K . Q^T       4 x v_mfma_scale_..._32x32x64 (scales sk, sq)
+// One wavefront per 64-row query tile, one wave per SIMD, no LDS: K and V
+// arrive in the matrix cores' operand order (written so by the tile-layout
+// quantisation), so each key tile is two sets of eight 16-byte loads per
+// lane, every load instruction reading 1 KB contiguous, issued one tile
+// ahead.  A key tile is used by exactly one wave, so nothing would be shared
+// through LDS.  Per 64-key tile:
+//   S^T (64 keys x 64 queries) = K . Q^T    8 x v_mfma_scale_..._32x32x64 (scales sk, sq),
+//                                           one half of the queries at a time
 //   P = 2^(x - m) * 2^(8 - kLazy) rounded to e4m3 with v_cvt_pk_fp8_f32, the
 //       power of two built in integer arithmetic (one FMA and one conversion
 //       per score: exact at integer exponents, linear in between)
-//   O^T (128 x 32)        += V^T . P^T        4 x v_mfma_scale_..._32x32x64 (scales sv, 2^(kLazy-8))
-//   row sums of P          += 1^T . P^T        1 more MFMA against an all-ones channel
+//   O^T (128 x 64)        += V^T . P^T        8 x v_mfma_scale_..._32x32x64 (scales sv, 2^(kLazy-8))
+//   row sums of P          += 1^T . P^T        2 more MFMAs against an all-ones channel
 // so the normaliser is the sum of exactly the rounded probabilities the PV
-// product uses, accumulated (and rescaled) by the matrix cores.
-// Copies: pairs of K and V tiles go global -> LDS with buffer_load ... lds
-// issued from inline asm.  K pairs are double- and V pairs triple-buffered
-// (80 KB of LDS): each step reads its K fragments, releases the K buffer at
-// one barrier and refills it with the pair two steps ahead; the V buffer the
-// previous step read is refilled at the start of the step.  The V^T operand
-// is read from the row-major V tile with ds_read_b64_tr_b8.  The two
-// tile-parity waves of a row-half merge their softmax states at the end.
+// product uses, accumulated (and rescaled) by the matrix cores.  The next
+// tile's first score products are issued before the current tile's PV
+// products, so the softmax of one runs while the matrix cores work on the
+// other.
 #include "common.h"
 #include "launch.h"
 
 namespace sa {
 namespace {
 
-constexpr int kThreads = 256;
 constexpr int kRowBytes = kHeadDim;             // 128 B per e4m3 row
-constexpr int kTileBytes = kTile * kRowBytes;   // 8 KB per K or V tile
-constexpr int kPairBytes = 2 * kTileBytes;      // one pair of tiles
-constexpr float kLazy = 2.f;  // log2 headroom before the accumulator is rescaled
-constexpr float kPScale = 64.f;                  // 2^(8 - kLazy): P in (0, 256] before e4m3
-constexpr float kLog2PScale = 6.f;               // log2(kPScale)
+constexpr int kOpTileBytes = kTile * kRowBytes; // 8 KB: one 64-key tile in operand order
+constexpr float kLazy = 2.f;  // log2 headroom of P above the reference before a shift
+constexpr int kMaxShift = 100;  // largest shift of P's frame (keeps fp32 sums finite)
+constexpr float kLog2PScale = 6.f;               // log2 of 2^(8 - kLazy): P in (0, 256] before e4m3
 constexpr int kPScaleInvE8m0 = 127 - 6;          // E8M0 code of 2^-(8 - kLazy)
 constexpr int kOneE8m0 = 127;                    // E8M0 code of 1
 constexpr int kFp8One = 0x38383838;              // four e4m3 ones
-
-// 16-byte-chunk swizzles of 128-byte rows (row = row within the tile):
-// conflict-free for the K A-operand reads (16 rows, one chunk per pass) and
-// the V transpose reads (rows k0 + {0..3, 8..11}, two chunks per pass).
-__device__ __forceinline__ int swz_k(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
-__device__ __forceinline__ int swz_v(int row, int chunk) {
-  return chunk ^ ((((row >> 1) & 1) << 1) | (((row >> 3) & 1) << 2));
-}
 
 typedef __attribute__((__vector_size__(2 * sizeof(int)))) int i32x2;
 typedef const __attribute__((address_space(4))) int32_t* list_ptr;
@@ -115,27 +104,9 @@ __device__ __forceinline__ uint32_t cvt_u32_sat(float x) {
 // E8M0 code of a power-of-two fp32 scale (its biased exponent).
 __device__ __forceinline__ int e8m0(float s) { return (int)((__float_as_uint(s) >> 23) & 0xffu); }
 
-// Global byte offset of the logical chunk that the swizzle stores at LDS slot
-// `slot` of tile row `row`.
-__device__ __forceinline__ uint32_t dma_offset(int row, int slot, bool is_v) {
-  const int chunk = is_v ? swz_v(row, slot) : swz_k(row, slot);
-  return (uint32_t)row * kRowBytes + (uint32_t)chunk * 16u;
-}
 
-// s_waitcnt with the other counters at their maxima (no wait on them).
-__device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
-__device__ __forceinline__ void wait_vm8() { __builtin_amdgcn_s_waitcnt(0x0F78); }
-__device__ __forceinline__ void wait_vm16() { __builtin_amdgcn_s_waitcnt(0x4F70); }
-__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
-
-__global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
-  // Distinct LDS objects per buffer keep every access at a constant base.
-  __shared__ __attribute__((aligned(1024))) uint8_t kp0[kPairBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t kp1[kPairBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t vp0[kPairBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t vp1[kPairBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t vp2[kPairBytes];
-
+__global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(1, 1))) void fwd_fp8_kernel(
+    Params p) {
   const int item = p.order ? p.order[blockIdx.x] : (int)blockIdx.x;
   const int bh = item / p.ntiles;
   const int qt = item - bh * p.ntiles;
@@ -144,269 +115,162 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
   const int iblk = q0 / p.block;
   const int spb = p.block / kTile;
   // List and scales are read-only here: reading them through the constant
-  // address space makes the uniform reads scalar loads, which vmcnt does not
-  // count.
+  // address space makes the uniform reads scalar loads.
   const list_ptr list = (list_ptr)(p.idx + ((int64_t)bh * p.nb + iblk) * p.kmax);
   const int c = min(max(p.cnt[(int64_t)bh * p.nb + iblk], 0), p.kmax);
   const int total = c * spb;
-
-  // the wave index is uniform across a wave: read it into a scalar register
-  // so that everything derived from it (the tile a wave computes, its
-  // scales, the mask test) stays scalar
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-  const int rh = wave & 1, par = wave >> 1;  // row half, tile parity
+  const int lane = threadIdx.x & (kWave - 1);
   const int g = lane >> 5, l32 = lane & 31;
 
-  // Allowed keys [key_lo, key_hi) of this lane's query (the causal window,
-  // and the sequence end); a tile needs the per-score mask unless it lies
-  // inside every row's range: [lo of the tile's last row, hi of its first).
-  const int qtok = min(q0 + rh * 32 + l32, p.N - 1);
-  const int key_lo = causal_lo(p.cs, qtok), key_hi = causal_hi(p.cs, qtok);
+  // Allowed keys [key_lo, key_hi) of this lane's queries (one per half of
+  // the tile); a tile needs the per-score mask unless it lies inside every
+  // row's range: [lo of the tile's last row, hi of its first).
+  int key_lo[2], key_hi[2];
+#pragma unroll
+  for (int qh = 0; qh < 2; ++qh) {
+    const int qtok = min(q0 + 32 * qh + l32, p.N - 1);
+    key_lo[qh] = causal_lo(p.cs, qtok);
+    key_hi[qh] = causal_hi(p.cs, qtok);
+  }
   const int tile_lo = causal_lo(p.cs, min(q0 + kTile - 1, p.N - 1));
   const int tile_hi = causal_hi(p.cs, q0);
 
-  const int64_t head = (int64_t)bh * p.N * kRowBytes;
-  const uint32_t bytes = (uint32_t)p.N * kRowBytes;
-  const auto kr = make_rsrc(p.k + head, bytes);
-  const auto vr = make_rsrc(p.v + head, bytes);
+  const int64_t qhead = (int64_t)bh * p.N * kRowBytes;
+  const auto qr = make_rsrc(p.q + qhead, (uint32_t)p.N * kRowBytes);
+  const int64_t ophead = (int64_t)bh * p.ntiles * kOpTileBytes;
+  const uint32_t opbytes = (uint32_t)p.ntiles * kOpTileBytes;
+  const auto kr = make_rsrc(p.k + ophead, opbytes);
+  const auto vr = make_rsrc(p.v + ophead, opbytes);
   const scale_ptr skh = (scale_ptr)(p.sk + (int64_t)bh * p.nb);
   const scale_ptr svh = (scale_ptr)(p.sv + (int64_t)bh * p.nb);
   const int sq_code = e8m0(((scale_ptr)p.sq)[(int64_t)bh * p.nb + iblk]);
 
-  // Copies of a pair into [tile A | tile B]: each wave moves rows 16w .. 16w+15
-  // of each tile (two 1 KB copies of 8 rows), lane l writing LDS slot l%8 of
-  // row l/8 of those 8 rows.
-  uint32_t koff[2], voff[2];
+  // Q fragments (B operand of K . Q^T): query q0 + 32 qh + l32, bytes
+  // 64 ks + 32 g .. +31 of its row (rows past N read as zeros).
+  i32x8 qf[2][2];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int row = 16 * wave + 8 * i + (lane >> 3);
-    koff[i] = dma_offset(row, lane & 7, false);
-    voff[i] = dma_offset(row, lane & 7, true);
-  }
-  const int wv = __builtin_amdgcn_readfirstlane(wave);
-  auto dma_pair = [&](uint8_t* dst, __amdgpu_buffer_rsrc_t r, const uint32_t (&off)[2], int a0,
-                      int b0) {
-    // the wave's row offset passes through an opaque move, so the compiler
-    // adds the constant buffer offsets per copy instead of holding every
-    // (buffer, copy) address live across the loop
-    uint32_t wrow;
-    asm volatile("s_mov_b32 %0, %1" : "=s"(wrow) : "s"((uint32_t)(16 * wv) * kRowBytes));
-    const uint32_t base = lds_addr(dst) + wrow;
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-        dma16(base + t * kTileBytes + 8 * i * kRowBytes, r, off[i],
-              (uint32_t)(t ? b0 : a0) * kRowBytes);
-  };
-
-  // Pair cursor: pairs P0 (being computed), P1 and P2 as start rows (ta*,
-  // tb*; N when missing: such tiles read zeros and all their keys are
-  // masked, and the loop ends when P0 has no first tile) and key blocks (ja*,
-  // jb*); nb2 is the list position of the last tile taken.  The list entries
-  // after P2 and the scales of P1 are read one step ahead.
-  auto block_of = [&](int n) { return n < total ? sld(list, (uint32_t)(n >> (spb - 1))) : 0; };
-  int ta0 = p.N, tb0 = p.N, ta1 = p.N, tb1 = p.N, ta2 = p.N, tb2 = p.N;
-  const int na0 = next_tile(list, 0, total, spb, p.block, p.nb, p.N, &ta0);
-  const int nb0 = next_tile(list, na0 + 1, total, spb, p.block, p.nb, p.N, &tb0);
-  const int na1 = next_tile(list, nb0 + 1, total, spb, p.block, p.nb, p.N, &ta1);
-  const int nb1 = next_tile(list, na1 + 1, total, spb, p.block, p.nb, p.N, &tb1);
-  const int na2 = next_tile(list, nb1 + 1, total, spb, p.block, p.nb, p.N, &ta2);
-  int nb2 = next_tile(list, na2 + 1, total, spb, p.block, p.nb, p.N, &tb2);
-  int ja1 = block_of(na1), jb1 = block_of(nb1);
-  int ja2 = block_of(na2), jb2 = block_of(nb2);
-  // scale codes of the current pair: (K, V) for tiles A and B
-  const int ja0 = block_of(na0), jb0 = block_of(nb0);
-  int sk_a = e8m0(sld(skh, ja0)), sv_a = e8m0(sld(svh, ja0)), sk_b = e8m0(sld(skh, jb0)),
-      sv_b = e8m0(sld(svh, jb0));
-
-  // Prologue: the Q tile is staged through vp2 (K swizzle) while the K and V
-  // pairs P0 and P1 are issued; step 0 refills vp2 with V(P2) once every wave
-  // holds its Q fragment.  Every step issues the same number of copies, so
-  // the vmcnt arithmetic below is uniform.
-  {
-    const auto qr = make_rsrc(p.q + head, bytes);
-    const uint32_t base = lds_addr(vp2) + (uint32_t)(16 * wv) * kRowBytes;
-#pragma unroll
-    for (int i = 0; i < 2; ++i) dma16(base + 8 * i * kRowBytes, qr, koff[i], (uint32_t)q0 * kRowBytes);
-  }
-  dma_pair(kp0, kr, koff, ta0, tb0);
-  dma_pair(vp0, vr, voff, ta0, tb0);
-  dma_pair(vp1, vr, voff, ta1, tb1);
-  dma_pair(kp1, kr, koff, ta1, tb1);
-  wait_vm16();  // this wave's rows of Q have landed
-  barrier_keep_loads();
-
-  // Q fragment (B operand of K.Q^T): query row 32*rh + l32, bytes
-  // 64*ks + 32*g .. +31 of the row.
-  i32x8 qf[2];
-  {
-    const int row = rh * 32 + l32;
+  for (int qh = 0; qh < 2; ++qh)
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
-      const int c0 = 4 * ks + 2 * g;
-      const u32x4 lo = *reinterpret_cast<const u32x4*>(vp2 + row * kRowBytes + swz_k(row, c0) * 16);
-      const u32x4 hi = *reinterpret_cast<const u32x4*>(vp2 + row * kRowBytes + swz_k(row, c0 + 1) * 16);
+      const uint32_t off = (uint32_t)(q0 + 32 * qh + l32) * kRowBytes + 64 * ks + 32 * g;
+      const u32x4 lo = buf_ld16(qr, off), hi = buf_ld16(qr, off + 16);
 #pragma unroll
       for (int x = 0; x < 4; ++x) {
-        qf[ks][x] = (int)lo[x];
-        qf[ks][4 + x] = (int)hi[x];
+        qf[qh][ks][x] = (int)lo[x];
+        qf[qh][ks][4 + x] = (int)hi[x];
       }
     }
-  }
-  wait_lgkm0();
-  barrier_keep_loads();  // vp2 (Q) is free for V(P2)
 
-  f32x16 acc[4], accl;  // O^T, and the row sums in register 0 of lanes 0..31
+  // Operand-order tile loads (t: 64-key tile of the head): K fragment
+  // (rt, ks) = chunks 2 (2 rt + ks) and 2 (2 rt + ks) + 1, V^T fragment dt =
+  // chunks 2 dt and 2 dt + 1, each chunk 1 KB (16 bytes per lane).
+  auto load_k = [&](i32x8 (&kf)[2][2], int t) __attribute__((always_inline)) {
+    const uint32_t base = (uint32_t)__builtin_amdgcn_readfirstlane(t) * kOpTileBytes;
 #pragma unroll
-  for (int dt = 0; dt < 4; ++dt)
+    for (int f = 0; f < 4; ++f) {
+      const u32x4 lo = buf_ld16(kr, 16 * lane + 2048 * f, base);
+      const u32x4 hi = buf_ld16(kr, 16 * lane + 2048 * f + 1024, base);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc[dt][r] = 0.f;
-#pragma unroll
-  for (int r = 0; r < 16; ++r) accl[r] = 0.f;
-  // all-ones channel 0 of the row-sum A operand: lanes holding channel 0
-  i32x8 ones;
-#pragma unroll
-  for (int x = 0; x < 8; ++x) ones[x] = l32 == 0 ? kFp8One : 0;
-  float m2 = -INFINITY;
-
-  // V^T transpose read: lane 16G + 2e + h supplies the 8 bytes of key
-  // 16a + 8(e>>2) + 4(G>>1) + (e&3) at channels 32*dt + 16(G&1) + 8h .. +7;
-  // lane l then holds channel 32*dt + (l&31) of slots 8a .. 8a+7.
-  const int G = lane >> 4, e8 = (lane >> 1) & 7, h8 = lane & 1;
-  const int vrow0 = 8 * (e8 >> 2) + 4 * (G >> 1) + (e8 & 3);  // + 16a
-
-  wait_vm8();  // K(P0), V(P0) landed (V(P1), K(P1) may still fly)
-  barrier_keep_loads();
-
-  // Next valid tile at or after index `ahead` whose raw list entry `pre`
-  // was prefetched: the common case decodes it directly, an invalid entry
-  // falls back to a scan of the list.
-  auto advance = [&](int ahead, int pre, int* st, int* jout) {
-    *st = p.N;
-    *jout = 0;
-    if (ahead >= total) return total;
-    const int j = __builtin_amdgcn_readfirstlane(pre);
-    const int s0 = j * p.block + (ahead & (spb - 1)) * kTile;
-    if (j >= 0 && j < p.nb && s0 < p.N) {
-      *st = s0;
-      *jout = j;
-      return ahead;
+      for (int x = 0; x < 4; ++x) {
+        kf[f >> 1][f & 1][x] = (int)lo[x];
+        kf[f >> 1][f & 1][4 + x] = (int)hi[x];
+      }
     }
-    const int m = next_tile(list, ahead + 1, total, spb, p.block, p.nb, p.N, st);
-    *jout = block_of(m);
-    return m;
   };
-
-  // One pair: compute from K pair buffer `kc` and V pair buffer `vc`; `vn`
-  // (read by the previous step) receives V(P2) at once and `kc` receives
-  // K(P2) after the barrier that follows the K fragment reads.
-  auto step = [&](uint8_t* kc, const uint8_t* vc, uint8_t* vn) {
-    dma_pair(vn, vr, voff, ta2, tb2);
-    const uint8_t* kt = kc + par * kTileBytes;
-    i32x8 kf[2][2];  // [row tile][k-step]
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt) {
-      const int row = rt * 32 + l32;
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        const int c0 = 4 * ks + 2 * g;
-        const u32x4 lo = *reinterpret_cast<const u32x4*>(kt + row * kRowBytes + swz_k(row, c0) * 16);
-        const u32x4 hi =
-            *reinterpret_cast<const u32x4*>(kt + row * kRowBytes + swz_k(row, c0 + 1) * 16);
-#pragma unroll
-        for (int x = 0; x < 4; ++x) {
-          kf[rt][ks][x] = (int)lo[x];
-          kf[rt][ks][4 + x] = (int)hi[x];
-        }
-      }
-    }
-    // one step ahead: scales of P1, list entries after P2
-    const float fka = sld(skh, ja1), fva = sld(svh, ja1), fkb = sld(skh, jb1), fvb = sld(svh, jb1);
-    const int pre1 = sld(list, (uint32_t)min((nb2 + 1) >> (spb - 1), p.kmax - 1));
-    const int pre2 = sld(list, (uint32_t)min((nb2 + 2) >> (spb - 1), p.kmax - 1));
-    wait_lgkm0();
-    barrier_keep_loads();  // every wave holds its K fragments: kc is free
-    dma_pair(kc, kr, koff, ta2, tb2);
-
-    const uint8_t* vt = vc + par * kTileBytes;
-    i32x8 vf[4];
+  auto load_v = [&](i32x8 (&vf)[4], int t) __attribute__((always_inline)) {
+    const uint32_t base = (uint32_t)__builtin_amdgcn_readfirstlane(t) * kOpTileBytes;
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) {
-      const int lc = 2 * dt + (G & 1);  // logical 16-B chunk of channels 32dt + 16(G&1)
+      const u32x4 lo = buf_ld16(vr, 16 * lane + 2048 * dt, base);
+      const u32x4 hi = buf_ld16(vr, 16 * lane + 2048 * dt + 1024, base);
 #pragma unroll
-      for (int a = 0; a < 4; ++a) {
-        const int row = vrow0 + 16 * a;
-        const i32x2 t = __builtin_amdgcn_ds_read_tr8_b64_v2i32(
-            (__attribute__((address_space(3))) i32x2*)(vt + row * kRowBytes +
-                                                       swz_v(row, lc) * 16 + h8 * 8));
-        vf[dt][2 * a] = t[0];
-        vf[dt][2 * a + 1] = t[1];
+      for (int x = 0; x < 4; ++x) {
+        vf[dt][x] = (int)lo[x];
+        vf[dt][4 + x] = (int)hi[x];
       }
     }
+  };
 
-    const int start = par ? tb0 : ta0;
-    const int sk_code = par ? sk_b : sk_a;
-    const int sv_code = par ? sv_b : sv_a;
+  // O^T per query half, and the row sums of both halves in registers 0 and
+  // 1 of lanes 0..31 (rows 0 and 1 of one 32x32 product)
+  f32x16 acc[2][4], accl;
+  // all-ones row qh of the row-sum A operand: lanes holding row qh
+  i32x8 ones[2];
+#pragma unroll
+  for (int qh = 0; qh < 2; ++qh)
+#pragma unroll
+    for (int x = 0; x < 8; ++x) ones[qh][x] = l32 == qh ? kFp8One : 0;
+  // Reference max per query (log2 units), fixed for the whole row once set:
+  // a tile whose max lies above it by more than kLazy computes its P against
+  // ref + e (e a whole number) and enters the products with the extra scale
+  // 2^e through the per-lane E8M0 scale of the P operand, so no vector
+  // instruction ever rescales the accumulators.  A shift beyond kMaxShift
+  // (fp32 headroom) restarts the row from its first tile with the new max.
+  float mref[2] = {-INFINITY, -INFINITY};
+  const float cexp = p.scale_log2 * 8388608.f;  // tau log2(e) 2^23
+  bool restart = false;
 
-    // ---- S^T = K . Q^T (two 32-key row tiles) -----------------------------
-    f32x16 s[2];
+  // Keys outside the causal window or past N get a score of -inf; a tile
+  // needs the per-score test unless it lies inside every row's range: [lo
+  // of the tile's last row, hi of its first).  The test runs between the
+  // pipeline's blocks, only for such tiles.
+  auto needs_mask = [&](int start) __attribute__((always_inline)) {
+    return start + kTile > tile_hi || start < tile_lo;
+  };
+  auto apply_mask = [&](f32x16 (&s)[2], int start, int qh) __attribute__((always_inline)) {
+    int st = __builtin_amdgcn_readfirstlane(start);
+    asm volatile("" : "+s"(st));
+    const int hi = key_hi[qh] - st - 4 * g, lo = key_lo[qh] - st - 4 * g;
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int off = 32 * rt + 8 * (r >> 2) + (r & 3);  // key - start - 4g
+        if (off >= hi || off < lo) s[rt][r] = -INFINITY;
+      }
+  };
+
+  // S^T of one tile for query half qh: lane holds keys 32 rt + 8 (r / 4) +
+  // 4 g + r % 4 of query 32 qh + l32
+  auto scores = [&](const i32x8 (&kf)[2][2], int sk_code, int qh, f32x16 (&s)[2]) __attribute__((always_inline)) {
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[rt][r] = 0.f;
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks)
-        s[rt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(kf[rt][ks], qf[ks], s[rt], 0, 0,
-                                                                 0, sk_code, 0, sq_code);
+      s[rt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(kf[rt][0], qf[qh][0], (f32x16){}, 0,
+                                                              0, 0, sk_code, 0, sq_code);
+      s[rt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(kf[rt][1], qf[qh][1], s[rt], 0, 0,
+                                                              0, sk_code, 0, sq_code);
     }
-    // lane holds keys 32*rt + 8*(r>>2) + 4*g + (r&3) of query l32
-    if (start + kTile > tile_hi || start < tile_lo) {
-      // (the opaque move keeps the per-key arithmetic inside the branch)
-      int st = __builtin_amdgcn_readfirstlane(start);
-      asm volatile("" : "+s"(st));
-      const int hi = key_hi - st - 4 * g, lo = key_lo - st - 4 * g;
-#pragma unroll
-      for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int off = 32 * rt + 8 * (r >> 2) + (r & 3);  // key - start - 4g
-          if (off >= hi || off < lo) s[rt][r] = -INFINITY;
-        }
-    }
+  };
 
-    // ---- online softmax --------------------------------------------------
+  // Softmax numerators of one tile for query half qh: P^T as the B operand,
+  // slot 16 rt + r <- s[rt][r], values 2^(x - ref - e) * 2^(8 - kLazy) in
+  // e4m3; bscale = E8M0 code of 2^(e - (8 - kLazy)).  Branch-free (a shift
+  // beyond kMaxShift only raises `restart`).
+  auto softmax = [&](const f32x16 (&s)[2], int qh, i32x8& pk, int& bscale) __attribute__((always_inline)) {
     float mx = s[0][0];
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[rt][r]);
-    mx *= p.scale_log2;
-    if (__any(mx > m2 + kLazy)) {  // wave-uniform: raise the reference max
-      const float mnew = fmaxf(m2, pair_max32(mx));
-      const float alpha = __builtin_amdgcn_exp2f(m2 - (mnew == -INFINITY ? 0.f : mnew));
-      accl[0] *= alpha;
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[dt][r] *= alpha;
-      m2 = mnew;
-    }
-    const float msafe = m2 == -INFINITY ? 0.f : m2;
-    // P^T as B operand: slot 16*rt + r <- s[rt][r]; values 2^(x - m) * 2^(8 - kLazy)
-    // rounded to e4m3
-    i32x8 pk;
-    // P * 2^6 = 2^y with y = tau*log2(e)*s - m + 6, as the fp32 whose bit
-    // pattern is (y + 127) * 2^23 truncated to an integer: exact at integer
-    // y and linear in the mantissa between them (at most 6.2% above 2^y, the
-    // same relative excess for a given fractional part of y).  One FMA and
-    // one conversion per score instead of an FMA and a transcendental; the
+    mx = pair_max32(mx) * p.scale_log2;  // the tile's max for this query (both lanes)
+    const float ref = mref[qh] == -INFINITY ? mx : mref[qh];  // first tile with an allowed key
+    const float over = mx - ref - kLazy;  // NaN (both -inf) and -inf give e = 0
+    int e = over > 0.f ? (int)__builtin_ceilf(over) : 0;
+    const bool far = e > kMaxShift;
+    restart |= __any(far);
+    mref[qh] = far ? mx : ref;
+    e = far ? 0 : e;
+    bscale = kPScaleInvE8m0 + e;
+    // P * 2^6 = 2^y with y = tau*log2(e)*s - ref - e + 6, as the fp32 whose
+    // bit pattern is (y + 127) * 2^23 truncated to an integer: exact at
+    // integer y and linear in the mantissa between them (at most 6.2% above
+    // 2^y, the same relative excess for a given fractional part of y); the
     // e4m3 rounding that follows keeps 3 mantissa bits anyway.  Negative
     // patterns (y < -127, and masked scores) convert to 0, i.e. P = 0.
-    const float cexp = p.scale_log2 * 8388608.f;                    // tau log2(e) 2^23
-    const float kexp = (kLog2PScale + 127.f - msafe) * 8388608.f;  // (6 + 127 - m) 2^23
+    const float mloc = mref[qh] == -INFINITY ? 0.f : mref[qh] + (float)e;
+    const float kexp = (kLog2PScale + 127.f - mloc) * 8388608.f;  // (6 + 127 - m) 2^23
 #pragma unroll
-    for (int rt = 0; rt < 2; ++rt) {
+    for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
       for (int r = 0; r < 16; r += 4) {
         float x[4];
@@ -417,100 +281,173 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_fp8_kernel(Params p) {
         w = __builtin_amdgcn_cvt_pk_fp8_f32(x[2], x[3], w, true);
         pk[4 * rt + r / 4] = w;
       }
-    }
-
-    // ---- O^T += V^T . P^T, row sums += 1^T . P^T ----------------------------
-#pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
-      acc[dt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vf[dt], pk, acc[dt], 0, 0, 0,
-                                                                sv_code, 0, kPScaleInvE8m0);
-    accl = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(ones, pk, accl, 0, 0, 0, kOneE8m0, 0,
-                                                           kPScaleInvE8m0);
-
-    // advance the cursor
-    ta0 = ta1;
-    tb0 = tb1;
-    ta1 = ta2;
-    tb1 = tb2;
-    ja1 = ja2;
-    jb1 = jb2;
-    sk_a = e8m0(fka);
-    sv_a = e8m0(fva);
-    sk_b = e8m0(fkb);
-    sv_b = e8m0(fvb);
-    const int prev = nb2;
-    const int n2 = advance(prev + 1, pre1, &ta2, &ja2);
-    if (n2 == prev + 1) {
-      nb2 = advance(n2 + 1, pre2, &tb2, &jb2);
-    } else {
-      nb2 = next_tile(list, n2 + 1, total, spb, p.block, p.nb, p.N, &tb2);
-      jb2 = block_of(nb2);
-    }
-    // keep the whole pair's work ahead of the wait
-    __builtin_amdgcn_sched_barrier(0);
-    wait_vm8();  // K(P1), V(P1) landed; V(P2), K(P2) may fly
-    barrier_keep_loads();  // also: every wave is done reading vc
   };
-  // step n reads K pair buffer n%2 and V pair buffer n%3, refills V (n+2)%3
-  while (ta0 < p.N) {
-    step(kp0, vp0, vp2);
-    if (ta0 >= p.N) break;
-    step(kp1, vp1, vp0);
-    if (ta0 >= p.N) break;
-    step(kp0, vp2, vp1);
-    if (ta0 >= p.N) break;
-    step(kp1, vp0, vp2);
-    if (ta0 >= p.N) break;
-    step(kp0, vp1, vp0);
-    if (ta0 >= p.N) break;
-    step(kp1, vp2, vp1);
-  }
-  wait_vm0();
-  __syncthreads();
 
-  // ---- merge the two tile-parity waves, normalise, store -----------------
-  // the row sum of query l32 sits in register 0 of lane l32
-  float lsum = __shfl(accl[0], l32, kWave);
-  float* mrg = reinterpret_cast<float*>(rh ? vp0 : kp0);  // 66 x 64 floats per row-half
-  if (par == 1) {
+  // O^T += V^T . P^T and row sums += 1^T . P^T for one tile
+  auto pv = [&](const i32x8 (&vf)[4], const i32x8 (&pk)[2], int sv_code, const int (&bs)[2]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int qh = 0; qh < 2; ++qh) {
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+        acc[qh][dt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+            vf[dt], pk[qh], acc[qh][dt], 0, 0, 0, sv_code, 0, bs[qh]);
+      accl = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(ones[qh], pk[qh], accl, 0, 0, 0,
+                                                             kOneE8m0, 0, bs[qh]);
+    }
+  };
+
+  auto block_of = [&](int n) __attribute__((always_inline)) { return n < total ? sld(list, (uint32_t)(n >> (spb - 1))) : 0; };
+#pragma unroll
+  for (int qh = 0; qh < 2; ++qh)
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mrg[(dt * 16 + r) * kWave + lane] = acc[dt][r];
-    mrg[64 * kWave + lane] = m2;
-    mrg[65 * kWave + lane] = lsum;
+      for (int r = 0; r < 16; ++r) acc[qh][dt][r] = 0.f;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) accl[r] = 0.f;
+
+  // Software pipeline over the list.  Tile 0 is the current tile n, tile 1
+  // the next, tile 2 the one after (n == total: none; a missing tile is
+  // replaced by tile 0, whose products are then discarded).  On entry to a
+  // step: P(n, half 0) in pk[0], S(n, half 1) in sa, V(n) in vf, K(n+1) in kf.
+  // A step computes, in blocks whose matrix and vector work interleave,
+  //   [1] S(n+1, half 0)           with  softmax(n, half 1)
+  //   [2] S(n+1, half 1), then K(n+2) starts to load into kf
+  //   [3] PV(n)                    with  softmax(n+1, half 0)
+  // and V(n+1) loads once PV(n) has been issued.  P(n+1, half 0) overwrites
+  // P(n, half 0) after the products that read it have been issued.
+  int st0 = p.N, st1 = p.N;
+  const int n_first = next_tile(list, 0, total, spb, p.block, p.nb, p.N, &st0);
+  const int st_first = st0;
+  if (n_first < total) {
+    i32x8 kf[2][2], vf[4], pk[2];
+    int bs[2];
+    f32x16 sa[2], sb[2];
+    int n0 = 0, n1 = 0, j0 = 0, j1 = 0;
+    // read one step ahead (scalar loads): the list entry after tile 1, the
+    // K scale of tile 1 and the V scale of tile 0
+    int raw = 0;
+    float skf = 1.f, svf = 1.f;
+    auto prefetch = [&]() __attribute__((always_inline)) {
+      raw = sld(list, (uint32_t)min((n1 + 1) >> (spb - 1), p.kmax - 1));
+      skf = sld(skh, j1);
+      svf = sld(svh, j0);
+    };
+    auto prologue = [&]() __attribute__((always_inline)) {
+      n0 = n_first;
+      st0 = st_first;
+      n1 = next_tile(list, n0 + 1, total, spb, p.block, p.nb, p.N, &st1);
+      j0 = block_of(n0);
+      j1 = block_of(n1);
+      load_k(kf, st0 >> 6);
+      load_v(vf, st0 >> 6);
+      const int sk0 = e8m0(sld(skh, j0));
+      scores(kf, sk0, 0, sb);
+      scores(kf, sk0, 1, sa);
+      load_k(kf, (n1 < total ? st1 : st0) >> 6);
+      if (needs_mask(st0)) {
+        apply_mask(sb, st0, 0);
+        apply_mask(sa, st0, 1);
+      }
+      softmax(sb, 0, pk[0], bs[0]);
+      prefetch();
+    };
+    for (;;) {
+    prologue();
+    for (;;) {
+      const bool has1 = n1 < total;
+      const int sv0 = e8m0(svf), sk1 = e8m0(skf);
+      // tile 2: the prefetched entry decodes it unless it is invalid (then
+      // the list is scanned)
+      int n2 = total, st2 = p.N, j2 = 0;
+      if (has1 && n1 + 1 < total) {
+        const int j = __builtin_amdgcn_readfirstlane(raw);
+        const int s0 = j * p.block + ((n1 + 1) & (spb - 1)) * kTile;
+        if (j >= 0 && j < p.nb && s0 < p.N) {
+          n2 = n1 + 1;
+          st2 = s0;
+          j2 = j;
+        } else {
+          n2 = next_tile(list, n1 + 2, total, spb, p.block, p.nb, p.N, &st2);
+          j2 = block_of(n2);
+        }
+      }
+      const int st1x = has1 ? st1 : st0;
+      const bool m1 = needs_mask(st1x);
+      // [1]
+      scores(kf, sk1, 0, sb);
+      softmax(sa, 1, pk[1], bs[1]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, 28, 0);  // then vector work
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      // [2]
+      scores(kf, sk1, 1, sa);
+      load_k(kf, (n2 < total ? st2 : st0) >> 6);
+      if (m1) {
+        apply_mask(sb, st1x, 0);
+        apply_mask(sa, st1x, 1);
+      }
+      // [3]
+      pv(vf, pk, sv0, bs);
+      softmax(sb, 0, pk[0], bs[0]);
+#pragma unroll
+      for (int i = 0; i < 10; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 12, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      load_v(vf, st1x >> 6);
+      if (restart) break;
+      if (!has1) break;
+      n0 = n1;
+      st0 = st1;
+      j0 = j1;
+      n1 = n2;
+      st1 = st2;
+      j1 = j2;
+      prefetch();
+    }
+    if (!restart) break;
+    // a shift beyond kMaxShift: start over from the first tile with the
+    // raised reference (products with zero operands clear the sums)
+    restart = false;
+    const i32x8 z = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+    for (int qh = 0; qh < 2; ++qh)
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+        acc[qh][dt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+            z, z, (f32x16){}, 0, 0, 0, kOneE8m0, 0, kOneE8m0);
+    accl = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(z, z, (f32x16){}, 0, 0, 0,
+                                                           kOneE8m0, 0, kOneE8m0);
+    }
   }
-  __syncthreads();
-  if (par == 0) {
-    const float m_o = mrg[64 * kWave + lane];
-    const float l_o = mrg[65 * kWave + lane];
-    const float mm = fmaxf(m2, m_o);
-    const float ms = mm == -INFINITY ? 0.f : mm;
-    const float a0 = __builtin_amdgcn_exp2f(m2 - ms);
-    const float a1 = __builtin_amdgcn_exp2f(m_o - ms);
-    const float l = lsum * a0 + l_o * a1;
+
+  // ---- normalise, store ---------------------------------------------------
+#pragma unroll
+  for (int qh = 0; qh < 2; ++qh) {
+    // the row sum of query 32 qh + l32 sits in register qh of lane l32
+    const float l = __shfl(accl[qh], l32, kWave);
     const float inv = l > 0.f ? 1.f / l : 0.f;
-    const float c0 = a0 * inv, c1 = a1 * inv;
-    const int row = q0 + rh * 32 + l32;
+    const int row = q0 + 32 * qh + l32;
     if (row < p.N) {
       uint16_t* op = p.o + b * p.os.b + h * p.os.h + (int64_t)row * p.os.n;
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          float x[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            x[r] = acc[dt][4 * j + r] * c0 + mrg[(dt * 16 + 4 * j + r) * kWave + lane] * c1;
           u32x2 w;
-          w[0] = pack_bf16x2(x[0], x[1]);
-          w[1] = pack_bf16x2(x[2], x[3]);
+          w[0] = pack_bf16x2(acc[qh][dt][4 * j] * inv, acc[qh][dt][4 * j + 1] * inv);
+          w[1] = pack_bf16x2(acc[qh][dt][4 * j + 2] * inv, acc[qh][dt][4 * j + 3] * inv);
           *reinterpret_cast<u32x2*>(op + dt * 32 + 8 * j + 4 * g) = w;
         }
       }
       if (p.lse && g == 0)
         p.lse[(int64_t)bh * p.N + row] =
-            l > 0.f ? (mm + __builtin_amdgcn_logf(l)) * 0.69314718055994531f : -INFINITY;
+            l > 0.f ? (mref[qh] + __builtin_amdgcn_logf(l)) * 0.69314718055994531f : -INFINITY;
     }
   }
 }
@@ -539,7 +476,7 @@ hipError_t launch_fwd_fp8(const Shape& s, const FwdArgs& a, hipStream_t stream) 
   p.ntiles = (s.N + kTile - 1) / kTile;
   p.scale_log2 = a.softmax_scale * 1.4426950408889634f;
   p.cs = s;
-  fwd_fp8_kernel<<<s.B * s.H * p.ntiles, kThreads, 0, stream>>>(p);
+  fwd_fp8_kernel<<<s.B * s.H * p.ntiles, kWave, 0, stream>>>(p);
   return hipGetLastError();
 }
 

@@ -130,6 +130,10 @@ hipError_t launch_bwd(const Shape& s, const BwdIn& in, void* ws, hipStream_t str
 // ---- fp8 quantisation ----------------------------------------------------
 hipError_t launch_quant_fp8(const Shape& s, const void* x, Strides xs, uint8_t* x8,
                             float* scale, hipStream_t stream);
+// The same codes in the fp8 forward's K (is_v false) or V operand order:
+// [B*H][ceil(N / 64)][8192 bytes].
+hipError_t launch_quant_fp8_tiles(const Shape& s, const void* x, Strides xs, bool is_v,
+                                  uint8_t* x8, float* scale, hipStream_t stream);
 
 // ---- W8A8 fp8 linear layers -----------------------------------------------
 // Per-row e4m3 quantisation of bf16 x [rows][cols] (row stride ldx elements)

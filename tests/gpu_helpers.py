@@ -111,3 +111,26 @@ def check_launch_order(order, cnt, kmax, seqlen, block, what=""):
     assert np.all(np.diff(cls) <= 0), (what, "classes increase along sorted positions")
     same = np.diff(cls) == 0
     assert np.all(np.diff(seq)[same] > 0), (what, "equal classes out of raster order")
+
+
+def fp8_tiles_to_rows(x8t, N, operand):
+    """Invert the K (operand 0) or V (operand 1) tile layout of
+    sparse_attn_quant_fp8_tiles: uint8 [B, H, T, 8192] -> ([B, H, N, 128]
+    row-major codes, the codes of the T*64 - N keys past N).  Only index
+    arithmetic: the layout formulas of the header, read backwards."""
+    x = np.asarray(x8t)
+    B, H, T, _ = x.shape
+    c = np.arange(512)[:, None]
+    e = np.arange(16)[None, :]
+    f, lane = c // 64, c % 64
+    l, g = lane % 32, lane // 32
+    if operand == 0:
+        rt, ks, hf = f // 4, (f // 2) % 2, f % 2
+        key, ch = 32 * rt + l + 0 * e, 64 * ks + 32 * g + 16 * hf + e
+    else:
+        dt, hf = f // 2, f % 2
+        key, ch = 32 * hf + 8 * (e // 4) + 4 * g + e % 4, 32 * dt + l + 0 * e
+    rows = np.zeros((B, H, T, 64, 128), dtype=np.uint8)
+    rows[:, :, :, key, ch] = x.reshape(B, H, T, 512, 16)
+    rows = rows.reshape(B, H, T * 64, 128)
+    return rows[:, :, :N], rows[:, :, N:]

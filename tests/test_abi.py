@@ -177,6 +177,14 @@ def test_quant_and_fwd_fp8_reject_bad_arguments():
     assert lib.sparse_attn_quant_fp8(ctypes.byref(ds), MIS, st3, P, P, None) == -1
     bad = (ctypes.c_int64 * 3)(2 * 4096 * 128, 4096 * 128, 129)
     assert lib.sparse_attn_quant_fp8(ctypes.byref(ds), P, bad, P, P, None) == -1
+    qt = lambda *a: lib.sparse_attn_quant_fp8_tiles(ctypes.byref(ds), *a)
+    assert qt(None, st3, sa.SA_FP8_K, P, P, None) == -1             # null x
+    assert qt(P, st3, 2, P, P, None) == -1                          # bad operand
+    assert qt(P, st3, sa.SA_FP8_V, MIS, P, None) == -1              # misaligned x8
+    assert qt(P, bad, sa.SA_FP8_K, P, P, None) == -1                # bad stride
+    assert lib.sparse_attn_fp8_tiles_bytes(ctypes.byref(ds)) == 2 * 64 * 8192
+    assert lib.sparse_attn_fp8_tiles_bytes(ctypes.byref(desc(N=4097))) == 2 * 65 * 8192
+    assert lib.sparse_attn_fp8_tiles_bytes(ctypes.byref(desc(d=64))) == -1
     f = lambda *a: lib.sparse_attn_fwd_fp8(ctypes.byref(ds), *a)
     assert f(P, None, P, P, P, P, P, P, 7, None, P, None, None) == -1    # null sq
     assert f(P, P, P, P, P, P, P, P, 0, None, P, None, None) == -1       # kmax 0

@@ -124,8 +124,8 @@ def test_causal_fp8_forward():
     idx, cnt = select_causal_check(q, k, block, wl.keep_bp, causal, "tiny fp8")
     qd, kd, vd = (t.to(DEV) for t in (q, k, v))
     q8, sq = sa.sparse_attn_quant_fp8(qd, block=block)
-    k8, sk = sa.sparse_attn_quant_fp8(kd, block=block)
-    v8, sv = sa.sparse_attn_quant_fp8(vd, block=block)
+    k8, sk = sa.sparse_attn_quant_fp8_tiles(kd, sa.SA_FP8_K, block=block)
+    v8, sv = sa.sparse_attn_quant_fp8_tiles(vd, sa.SA_FP8_V, block=block)
     o, lse = sa.sparse_attn_fwd_fp8(q8, sq, k8, sk, v8, sv, idx, cnt, block=block, causal=causal)
     torch.cuda.synchronize()
     o, lse = o.cpu(), lse.cpu()

@@ -9,7 +9,8 @@ import torch
 import oracle as O
 import paper_2609_23153_amd as sa
 import workloads as W
-from gpu_helpers import FP8_LSE_ABS, FP8_REL_L2, check_out, oracle_select, rel_l2, say, widen
+from gpu_helpers import (FP8_LSE_ABS, FP8_REL_L2, check_out, fp8_tiles_to_rows, oracle_select,
+                         rel_l2, say, widen)
 
 pytestmark = pytest.mark.gpu
 
@@ -26,12 +27,29 @@ def _gpu():
     torch.cuda.synchronize()
 
 
-def quant_check(x, block, what):
-    """GPU quantisation of x [B, H, N, 128] bf16 vs the oracle, bit-exact."""
+def quant_operands(qd, kd, vd, block):
+    """Q row-major, K and V in the fp8 forward's tile layouts."""
+    q8, sq = sa.sparse_attn_quant_fp8(qd, block=block)
+    k8, sk = sa.sparse_attn_quant_fp8_tiles(kd, sa.SA_FP8_K, block=block)
+    v8, sv = sa.sparse_attn_quant_fp8_tiles(vd, sa.SA_FP8_V, block=block)
+    return q8, sq, k8, sk, v8, sv
+
+
+def quant_check(x, block, what, operand=None):
+    """GPU quantisation of x [B, H, N, 128] bf16 vs the oracle, bit-exact;
+    operand None: the row-major call, else the tile layout of that operand
+    (read back through its inverse, and every code past N zero)."""
     B, H, N, _ = x.shape
-    x8, sc = sa.sparse_attn_quant_fp8(x.to(DEV), block=block)
+    if operand is None:
+        x8, sc = sa.sparse_attn_quant_fp8(x.to(DEV), block=block)
+    else:
+        x8t = torch.full((B, H, -(-N // 64), 8192), 0x5A, dtype=torch.uint8, device=DEV)
+        x8, sc = sa.sparse_attn_quant_fp8_tiles(x.to(DEV), operand, block=block, x8=x8t)
     torch.cuda.synchronize()
     x8, sc = x8.cpu().numpy(), sc.cpu().numpy()
+    if operand is not None:
+        x8, pad = fp8_tiles_to_rows(x8, N, operand)
+        assert (pad == 0).all(), (what, "codes past N")
     for b in range(B):
         for h in range(H):
             codes, scales = O.quantize_fp8_blocks(widen(x[b, h]), block)
@@ -53,24 +71,35 @@ def test_quant_fp8_bitexact(N, block):
     x[1, 0, :block] = -0.0                                  # negative zeros
     x[1, 1, 5, 7] = 448.0 * 2.0 ** -3                       # amax exactly 448 * 2^e
     x[1, 2, block:2 * block] = torch.round(x[1, 2, block:2 * block] * 4) / 4  # many ties
-    quant_check(x.to(torch.bfloat16), block, f"N={N} b={block}")
+    xb = x.to(torch.bfloat16)
+    quant_check(xb, block, f"N={N} b={block}")
+    quant_check(xb, block, f"N={N} b={block} K tiles", operand=sa.SA_FP8_K)
+    quant_check(xb, block, f"N={N} b={block} V tiles", operand=sa.SA_FP8_V)
+
+
+@pytest.mark.parametrize("N,block", [(4160, 128), (8200, 128), (64, 64), (65, 64)])
+def test_quant_fp8_tiles_tails(N, block):
+    """Tile layouts where the last 64-key tile is partial or (block 128,
+    N mod 128 in (0, 64]) the block's second tile lies past N."""
+    g = torch.Generator().manual_seed(7 * N + block)
+    x = (torch.randn(1, 2, N, 128, generator=g) * 2).to(torch.bfloat16)
+    for op, name in ((sa.SA_FP8_K, "K"), (sa.SA_FP8_V, "V")):
+        quant_check(x, block, f"N={N} b={block} {name} tiles", operand=op)
 
 
 def test_quant_fp8_outlier_workload_heads():
     wl = W.WORKLOADS["wan14b_720p_fp8"]
     heads = sorted({h for h, _ in W._outlier_pairs(wl)[0]} | {0})[:3]
     q, k, v = W.make_inputs(wl, heads=heads)
-    for name, t in (("q", q), ("k", k), ("v", v)):
-        quant_check(t, wl.block, f"wan14b_720p_fp8 {name} heads {heads}")
+    for name, t, op in (("q", q, None), ("k", k, sa.SA_FP8_K), ("v", v, sa.SA_FP8_V)):
+        quant_check(t, wl.block, f"wan14b_720p_fp8 {name} heads {heads}", operand=op)
 
 
 def fp8_fwd_and_check(q, k, v, idx, cnt, block, what, rows_of=None):
     """Quantise on the GPU, run the fp8 forward, compare with the oracle on
     the oracle's own dequantised operands."""
     qd, kd, vd = (t.to(DEV) for t in (q, k, v))
-    q8, sq = sa.sparse_attn_quant_fp8(qd, block=block)
-    k8, sk = sa.sparse_attn_quant_fp8(kd, block=block)
-    v8, sv = sa.sparse_attn_quant_fp8(vd, block=block)
+    q8, sq, k8, sk, v8, sv = quant_operands(qd, kd, vd, block)
     order = sa.sparse_attn_schedule(cnt, q.shape[2], idx.shape[-1], block=block)
     o, lse = sa.sparse_attn_fwd_fp8(q8, sq, k8, sk, v8, sv, idx, cnt, block=block, order=order)
     torch.cuda.synchronize()
@@ -146,9 +175,7 @@ def test_wan14b_fp8_full_size_sampled():
     nb = O.block_count(wl.seqlen, wl.block)
     kk = O.keep_count(wl.keep_bp, nb)
     idx, cnt = sa.sparse_attn_select(qd, kd, kk)
-    q8, sq = sa.sparse_attn_quant_fp8(qd)
-    k8, sk = sa.sparse_attn_quant_fp8(kd)
-    v8, sv = sa.sparse_attn_quant_fp8(vd)
+    q8, sq, k8, sk, v8, sv = quant_operands(qd, kd, vd, 64)
     order = sa.sparse_attn_schedule(cnt, wl.seqlen, kk)
     o, lse = sa.sparse_attn_fwd_fp8(q8, sq, k8, sk, v8, sv, idx, cnt, order=order)
     o0, l0 = sa.sparse_attn_fwd_fp8(q8, sq, k8, sk, v8, sv, idx, cnt)
@@ -191,9 +218,7 @@ def test_fwd_fp8_order_does_not_change_results(N, block):
     from test_gpu_parity import tail_lists
     g = torch.Generator().manual_seed(N + 7 * block)
     x = [torch.randn(2, 3, N, 128, generator=g).to(torch.bfloat16).to(DEV) for _ in range(3)]
-    q8, sq = sa.sparse_attn_quant_fp8(x[0], block=block)
-    k8, sk = sa.sparse_attn_quant_fp8(x[1], block=block)
-    v8, sv = sa.sparse_attn_quant_fp8(x[2], block=block)
+    q8, sq, k8, sk, v8, sv = quant_operands(x[0], x[1], x[2], block)
     nb = O.block_count(N, block)
     idx, cnt = tail_lists(nb, min(nb, 9), seed=N + 3, B=2, H=3)
     idx, cnt = idx.to(DEV), cnt.to(DEV)
