@@ -36,29 +36,49 @@ PEAK_FP8_TFLOPS = 5000.0    # MI355X dense fp8 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
 
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "fwd_bf16_wan14b_720p_hbm_traffic.txt")
-FWD_BF16_SOURCES = ("fwd_bf16.hip", "common.h", "launch.h", "sched.hip")  # sched.hip: the launch order
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "hbm_traffic_wan14b_720p.txt")
+# sources each kernel's counters depend on (sched.hip: the launch order;
+# quant_fp8.hip: the fp8 operand layout)
+TRAFFIC_SOURCES = {
+    "fwd_bf16_kernel": ("fwd_bf16.hip", "common.h", "launch.h", "sched.hip"),
+    "fwd_fp8_kernel": ("fwd_fp8.hip", "quant_fp8.hip", "common.h", "launch.h", "sched.hip"),
+    "pool_kernel": ("select.hip", "common.h", "launch.h"),
+    "score_topk_kernel": ("select.hip", "common.h", "launch.h"),
+}
 
 
-def measured_traffic(workload):
-    """HBM bytes per launch of fwd_bf16_kernel from the committed rocprofv3
+def source_hash(kernel):
+    h = hashlib.sha256()
+    for f in TRAFFIC_SOURCES[kernel]:
+        with open(os.path.join(ROOT, "paper_2609_23153_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3
     FETCH_SIZE / WRITE_SIZE summary (copy-calibrated), or None when that
-    summary does not cover this workload or the kernel sources have changed
-    since the counters were taken."""
-    if workload != "wan14b_720p" or not os.path.exists(TRAFFIC_PROFILE):
+    summary does not cover the kernel on this workload or the kernel's sources
+    have changed since the counters were taken."""
+    if not os.path.exists(TRAFFIC_PROFILE):
         return None
     kv = {}
     for line in open(TRAFFIC_PROFILE):
         if not line.startswith("#") and ":" in line:
             key, val = line.split(":", 1)
             kv[key.strip()] = val.strip()
-    h = hashlib.sha256()
-    for f in FWD_BF16_SOURCES:
-        with open(os.path.join(ROOT, "paper_2609_23153_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
-    if kv.get("fwd_bf16_source_sha256") != h.hexdigest():
+    if kv.get(f"{kernel}.workload") != workload:
         return None
-    return int(float(kv["traffic_bytes_per_launch"]))
+    if kv.get(f"{kernel}.source_sha256") != source_hash(kernel):
+        return None
+    return int(float(kv[f"{kernel}.traffic_bytes_per_launch"]))
+
+
+def sel_traffic(workload):
+    """HBM bytes of the selection call (pool + on-chip score/top-k), when both
+    kernels' counters cover the workload and sources."""
+    a, b = measured_traffic("pool_kernel", workload), measured_traffic("score_topk_kernel", workload)
+    return None if a is None or b is None else a + b
 
 
 def parse_args():
@@ -602,7 +622,8 @@ def bench_fp8(args, sa, W, dev):
         "quant_gbs": round(qbytes / (ms[1] * 1e-3) / 1e9, 1),
         "roofline": {"kernel": "fwd_fp8_kernel", "bound": "mfma", "achieved": round(tf, 2),
                      "peak": PEAK_FP8_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(tf / PEAK_FP8_TFLOPS, 4), "traffic": None,
+                     "frac": round(tf / PEAK_FP8_TFLOPS, 4),
+                     "traffic": measured_traffic("fwd_fp8_kernel", wl.name),
                      "flops_per_launch": flops},
     }
 
@@ -717,14 +738,14 @@ def main():
             "kernels": ["pool_kernel", "score_topk_kernel"], "bound": "hbm",
             "achieved": round(sel_bytes / (sel_ms * 1e-3) / 1e9, 1), "peak": PEAK_HBM_GBS,
             "unit": "GB/s", "frac": round(sel_bytes / (sel_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
-            "traffic": None, "algorithmic_bytes_per_call": sel_bytes,
+            "traffic": sel_traffic(wl.name), "algorithmic_bytes_per_call": sel_bytes,
             "note": "Q and K read once, lists written; the whole selection call"},
         "timing": timing,
         "roofline": {
             "kernel": "fwd_bf16_kernel", "bound": "mfma",
             "achieved": round(fwd_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
             "frac": round(fwd_tflops / PEAK_BF16_TFLOPS, 4),
-            "traffic": measured_traffic(wl.name),
+            "traffic": measured_traffic("fwd_bf16_kernel", wl.name),
             "flops_per_launch": flops,
             "algorithmic_bytes_per_launch": 4 * B * H * N * d * 2 + B * H * N * 4
                                             + B * H * nb * (k + 1) * 4,

@@ -45,31 +45,23 @@ def test_selected_flops_dense_lists_equal_dense_attention():
     assert bench.selected_flops(cnt, idx, N, block, d) == 2 * 4 * N * N * d
 
 
-def _summary_values():
-    kv = {}
-    for line in open(bench.TRAFFIC_PROFILE):
-        if not line.startswith("#") and ":" in line:
-            k, v = line.split(":", 1)
-            kv[k.strip()] = v.strip()
-    return kv
-
-
-def _source_hash():
-    h = hashlib.sha256()
-    for f in bench.FWD_BF16_SOURCES:
-        with open(os.path.join(bench.ROOT, "paper_2609_23153_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
-    return h.hexdigest()
-
-
-def test_traffic_follows_the_committed_summary_only_while_sources_match(tmp_path, monkeypatch):
-    kv = _summary_values()
-    expect = int(float(kv["traffic_bytes_per_launch"]))
-    got = bench.measured_traffic("wan14b_720p")
-    assert got == (expect if kv["fwd_bf16_source_sha256"] == _source_hash() else None)
-    assert bench.measured_traffic("wan13b_480p") is None  # counters cover one workload only
-    stale = tmp_path / "traffic.txt"
-    stale.write_text(open(bench.TRAFFIC_PROFILE).read().replace(
-        kv["fwd_bf16_source_sha256"], "0" * 64))
-    monkeypatch.setattr(bench, "TRAFFIC_PROFILE", str(stale))
-    assert bench.measured_traffic("wan14b_720p") is None
+def test_traffic_follows_the_summary_only_while_sources_match(tmp_path, monkeypatch):
+    """Per-kernel counter traffic is reported for the summarised workload,
+    and only while the kernel's sources hash to the recorded value."""
+    prof = tmp_path / "traffic.txt"
+    lines = ["# synthetic summary"]
+    for i, kern in enumerate(bench.TRAFFIC_SOURCES):
+        lines += [f"{kern}.workload: wan14b_720p", f"{kern}.source_sha256: {bench.source_hash(kern)}",
+                  f"{kern}.traffic_bytes_per_launch: {1000 + i}"]
+    prof.write_text("\n".join(lines) + "\n")
+    monkeypatch.setattr(bench, "TRAFFIC_PROFILE", str(prof))
+    for i, kern in enumerate(bench.TRAFFIC_SOURCES):
+        assert bench.measured_traffic(kern, "wan14b_720p") == 1000 + i
+        assert bench.measured_traffic(kern, "wan13b_480p") is None  # other workload
+    assert bench.sel_traffic("wan14b_720p") == (1000 + list(bench.TRAFFIC_SOURCES).index("pool_kernel")
+                                              + 1000 + list(bench.TRAFFIC_SOURCES).index("score_topk_kernel"))
+    stale = prof.read_text().replace(bench.source_hash("fwd_fp8_kernel"), "0" * 64)
+    prof.write_text(stale)
+    assert bench.measured_traffic("fwd_fp8_kernel", "wan14b_720p") is None
+    monkeypatch.setattr(bench, "TRAFFIC_PROFILE", str(tmp_path / "missing.txt"))
+    assert bench.measured_traffic("fwd_bf16_kernel", "wan14b_720p") is None
