@@ -117,7 +117,7 @@ int32_t sparse_attn_keep_count(int32_t keep_bp, int32_t nkb);
  * row stride of the index list (ignored for SA_OP_SELECT and
  * SA_OP_SELECT_HEAD).  Returns 0 for an invalid descriptor or op.
  * Row-mode selection with nkb <= 1192 keeps the block scores on chip and
- * needs B*H*(2048*nkb + 32768*ceil(nkb/32) + 8*nkb) bytes; above that, and
+ * needs B*H*(2048*nkb + 16384*ceil(nkb/32) + 4*nkb) bytes; above that, and
  * in the whole-head mode, the fp64 score matrix (8*nkb^2 bytes per head) is
  * part of it. */
 size_t sparse_attn_workspace_size(const sparse_attn_desc* desc, int32_t op, int32_t kmax);

@@ -6,8 +6,9 @@
 //   pool   : Q and K streamed once from HBM; per block, the fp64 sum of the
 //            bf16 token vectors (exact for bf16 inputs whose exponents span
 //            fewer than ~38 binades, so it does not depend on summation order)
-//   row mode, nb <= kFStrideBig (the scores never reach HBM):
-//   score_topk : per 32 query blocks, approximate scores of every key block
+//   row mode, nb <= kFStrideBig (the scores never reach HBM): pool of K only,
+//   score_topk : per 32 query blocks, their pooling (same arithmetic as the
+//            pool launch), then approximate scores of every key block
 //            on the bf16 matrix cores from a two-term bf16 split of the
 //            pooled sums, kept in LDS; per query block the k-th largest
 //            approximation and a rigorous error bound split the key blocks
@@ -104,75 +105,68 @@ __device__ __forceinline__ float f32_round_up(double x) {
   return f;
 }
 
-// Outputs of the pooling besides the fp64 sums, for the fused row selection
-// (all null otherwise): the sums split as hi + lo, hi = bf16(sum) and
+// Outputs of the K pooling besides the fp64 sums, for the fused row
+// selection (null otherwise): the sums split as hi + lo, hi = bf16(sum) and
 // lo = bf16(sum - hi), in MFMA operand order
 // [B*H][tile of 32 blocks][k-step][lane][8 channels] (lane = block % 32 +
 // 32 * (channel / 8 % 2)), and norm[b] = |sum| / n_b rounded up to fp32.
 struct PoolSplit {
-  uint16_t* qfrag;
-  uint16_t* kfrag;
-  float* qnorm;
-  float* knorm;
+  uint16_t* frag;
+  float* norm;
   int ntiles;  // ceil(nb / 32)
 };
 
-// One wave pools one block of Q (blockIdx.z == 0) or K (== 1); a workgroup
-// takes 4 consecutive blocks of one (batch, head).  Lane l loads 16 bytes
-// (channels 8 (l % 16) .. +7) of rows l / 16, l / 16 + 4, ..., all loads in
-// flight before the sums; the four row groups are then added across lanes
-// (v_permlane16 / 32_swap).  No LDS.
-constexpr int kPoolWaves = 4;
-
+// Pooled sums of the block of tokens [t0, t0 + BLOCK) ∩ [0, N) of one head
+// (x: its token 0) by one wave: lane l loads 16 bytes (channels
+// 8 (l % 16) .. +7) of rows l / 16, l / 16 + 4, ..., all loads in flight
+// before the fp64 sums; the four row groups are then added across lanes
+// (v_permlane16 / 32_swap), so every lane ends with the block's sums of its 8
+// channels (exact: the order does not matter).  Rows past N load token N - 1
+// (no branch around the loads, which would make the compiler wait on each)
+// and count as zero.
 template <int BLOCK>
-__global__ __launch_bounds__(kPoolWaves * kWave) void pool_kernel(
-    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, Strides qs, Strides ks,
-    int H, int N, int nb, double* __restrict__ qhat, double* __restrict__ khat,
-    PoolSplit split) {
-  const bool is_k = blockIdx.z != 0;
-  const uint16_t* x = is_k ? k : q;
-  const Strides st = is_k ? ks : qs;
-  double* out = is_k ? khat : qhat;
-  const int bh = blockIdx.y;
-  const int b = bh / H, h = bh - b * H;
-  const int i = blockIdx.x * kPoolWaves + (threadIdx.x >> 6);
-  if (i >= nb) return;  // uniform per wave
+__device__ __forceinline__ void pool_load(const uint16_t* __restrict__ x, int64_t stride_n,
+                                          int t0, int N, u32x4 (&w)[BLOCK / 4]) {
   const int lane = threadIdx.x & (kWave - 1);
-  const int t0 = i * BLOCK;
-  const int n_i = min(BLOCK, N - t0);
-  const uint16_t* base = x + b * st.b + h * st.h + (int64_t)t0 * st.n;
   const int c8 = lane & 15, r0 = lane >> 4;
-  constexpr int kLoads = BLOCK / 4;
-  u32x4 w[kLoads];
 #pragma unroll
-  for (int m = 0; m < kLoads; ++m) {
-    const int r = r0 + 4 * m;
-    w[m] = r < n_i ? ld16(base + (int64_t)r * st.n + c8 * 8) : (u32x4){0u, 0u, 0u, 0u};
-  }
-  double acc[8];
+  for (int m = 0; m < BLOCK / 4; ++m)
+    w[m] = ld16(x + (int64_t)min(t0 + r0 + 4 * m, N - 1) * stride_n + c8 * 8);
+  __builtin_amdgcn_sched_barrier(0);  // every load issued before the sums start
+}
+template <int BLOCK>
+__device__ __forceinline__ void pool_reduce(const u32x4 (&w)[BLOCK / 4], int t0, int N,
+                                            double (&acc)[8]) {
+  const int r0 = (threadIdx.x & (kWave - 1)) >> 4;
 #pragma unroll
   for (int c = 0; c < 8; ++c) acc[c] = 0.0;
 #pragma unroll
-  for (int m = 0; m < kLoads; ++m)
+  for (int m = 0; m < BLOCK / 4; ++m) {
+    const bool in = t0 + r0 + 4 * m < N;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      acc[2 * e] += (double)bf16_lo(w[m][e]);
-      acc[2 * e + 1] += (double)bf16_hi(w[m][e]);
+      const uint32_t v = in ? w[m][e] : 0u;
+      acc[2 * e] += (double)bf16_lo(v);
+      acc[2 * e + 1] += (double)bf16_hi(v);
     }
-  // every lane of the four row groups ends with the block's sums of its
-  // 8 channels (exact: the order does not matter)
+  }
 #pragma unroll
   for (int c = 0; c < 8; ++c) acc[c] = add_swapped<false>(add_swapped<true>(acc[c]));
-  double* o = out + ((int64_t)bh * nb + i) * kHeadDim + 8 * c8;
-  if (r0 == 0) {
-#pragma unroll
-    for (int c = 0; c < 8; c += 2) *reinterpret_cast<f64x2*>(o + c) = (f64x2){acc[c], acc[c + 1]};
-  }
-  if (split.qfrag == nullptr) return;  // uniform
-  // s = hi + lo + rest with |s - hi| <= 2^-8 |s| (fp32 then bf16 rounding,
-  // up to 2^-23 more), s - hi exact in fp64, |rest| <= 2^-16 |s| (1 + 2^-14)
-  u32x4 whi, wlo;
-  double sq = 0.0;
+}
+template <int BLOCK>
+__device__ __forceinline__ void pool_sums(const uint16_t* __restrict__ x, int64_t stride_n,
+                                          int t0, int N, double (&acc)[8]) {
+  u32x4 w[BLOCK / 4];
+  pool_load<BLOCK>(x, stride_n, t0, N, w);
+  pool_reduce<BLOCK>(w, t0, N, acc);
+}
+
+// The split of 8 pooled sums s = hi + lo + rest, packed as bf16 (|s - hi| <=
+// 2^-8 |s| after the fp32 then bf16 roundings, up to 2^-23 more; s - hi exact
+// in fp64; |rest| <= 2^-16 |s| (1 + 2^-14)), and the sum of their squares.
+__device__ __forceinline__ void split_hi_lo(const double (&acc)[8], u32x4& whi, u32x4& wlo,
+                                            double& sq) {
+  sq = 0.0;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     uint32_t hh[2], ll[2];
@@ -186,21 +180,57 @@ __global__ __launch_bounds__(kPoolWaves * kWave) void pool_kernel(
     whi[e] = hh[0] | (hh[1] << 16);
     wlo[e] = ll[0] | (ll[1] << 16);
   }
+}
+
+// |sum|^2 over the 16 lanes of a row (each row of lanes holds all 128 channels)
+__device__ __forceinline__ double row_sum16(double x) {
+  x += row_ror_f64<8>(x);
+  x += row_ror_f64<4>(x);
+  x += row_ror_f64<2>(x);
+  x += row_ror_f64<1>(x);
+  return x;
+}
+
+// One wave pools one block of Q (blockIdx.z + z0 == 0) or K (== 1); a
+// workgroup takes 4 consecutive blocks of one (batch, head).  No LDS.
+constexpr int kPoolWaves = 4;
+
+template <int BLOCK>
+__global__ __launch_bounds__(kPoolWaves * kWave) void pool_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, Strides qs, Strides ks,
+    int H, int N, int nb, int z0, double* __restrict__ qhat, double* __restrict__ khat,
+    PoolSplit split) {
+  const bool is_k = (int)blockIdx.z + z0 != 0;
+  const uint16_t* x = is_k ? k : q;
+  const Strides st = is_k ? ks : qs;
+  double* out = is_k ? khat : qhat;
+  const int bh = blockIdx.y;
+  const int b = bh / H, h = bh - b * H;
+  const int i = blockIdx.x * kPoolWaves + (threadIdx.x >> 6);
+  if (i >= nb) return;  // uniform per wave
+  const int lane = threadIdx.x & (kWave - 1);
+  const int t0 = i * BLOCK;
+  const int n_i = min(BLOCK, N - t0);
+  const int c8 = lane & 15, r0 = lane >> 4;
+  double acc[8];
+  pool_sums<BLOCK>(x + b * st.b + h * st.h, st.n, t0, N, acc);
+  double* o = out + ((int64_t)bh * nb + i) * kHeadDim + 8 * c8;
   if (r0 == 0) {
-    uint16_t* frag = is_k ? split.kfrag : split.qfrag;
+#pragma unroll
+    for (int c = 0; c < 8; c += 2) *reinterpret_cast<f64x2*>(o + c) = (f64x2){acc[c], acc[c + 1]};
+  }
+  if (!is_k || split.frag == nullptr) return;  // uniform
+  u32x4 whi, wlo;
+  double sq;
+  split_hi_lo(acc, whi, wlo, sq);
+  if (r0 == 0) {
     const int64_t slot = (((int64_t)bh * split.ntiles + (i >> 5)) * kFSteps + (c8 >> 1)) * kWave +
                          (i & 31) + 32 * (c8 & 1);
-    st16(frag + slot * 8, whi);
-    st16(frag + (slot + 8 * kWave) * 8, wlo);
+    st16(split.frag + slot * 8, whi);
+    st16(split.frag + (slot + 8 * kWave) * 8, wlo);
   }
-  // |sum|^2 over the 16 lanes of a row (each row holds all 128 channels)
-  sq += row_ror_f64<8>(sq);
-  sq += row_ror_f64<4>(sq);
-  sq += row_ror_f64<2>(sq);
-  sq += row_ror_f64<1>(sq);
-  if (lane == 0)
-    (is_k ? split.knorm : split.qnorm)[(int64_t)bh * nb + i] =
-        f32_round_up(sqrt(sq) / (double)n_i);
+  sq = row_sum16(sq);
+  if (lane == 0) split.norm[(int64_t)bh * nb + i] = f32_round_up(sqrt(sq) / (double)n_i);
 }
 
 // fp64 score GEMM on the matrix cores: one 64x64 tile of
@@ -621,17 +651,20 @@ __device__ void exact_row_select(const double* __restrict__ qrow,
   select_emit<KPL>(hi, lo, mem, jj, k, out);
 }
 
-template <int NBP>
+template <int NBP, int BLOCK>
 __global__ __launch_bounds__(kFThreads) void score_topk_kernel(
-    const uint16_t* __restrict__ qfrag, const uint16_t* __restrict__ kfrag,
-    const float* __restrict__ qnorm, const float* __restrict__ knorm,
-    const double* __restrict__ qhat, const double* __restrict__ khat, Shape cs, int k_all,
-    int kmax, int ntiles, int per_xcd, int32_t* __restrict__ idx, int32_t* __restrict__ cnt) {
+    const uint16_t* __restrict__ q, Strides qs, const uint16_t* __restrict__ kfrag,
+    const float* __restrict__ knorm, double* __restrict__ qhat, const double* __restrict__ khat,
+    Shape cs, int k_all, int kmax, int ntiles, int per_xcd, int32_t* __restrict__ idx,
+    int32_t* __restrict__ cnt) {
   constexpr int KPL = (NBP + kWave - 1) / kWave;
-  __shared__ uint32_t keys[kFRows * NBP];
+  static_assert(kFRows * NBP >= kFSteps * kWave * 4, "operand staging fits the key area");
+  __shared__ __align__(16) uint32_t keys[kFRows * NBP];
   __shared__ uint32_t cand[kFWaves][2][kWave];
   __shared__ float wmax[kFWaves];
+  __shared__ float qn_lds[kFRows];
   const int nb = cs.nb;
+  constexpr int kQB = kFRows / kFWaves;  // query blocks pooled per wave
   // Consecutive tiles (the same head's key blocks) run on one XCD: workgroup
   // w goes to XCD w % 8, which takes the logical tiles [x, x + 1) * per_xcd.
   const int logical = (int)(blockIdx.x & 7) * per_xcd + (int)(blockIdx.x >> 3);
@@ -640,11 +673,51 @@ __global__ __launch_bounds__(kFThreads) void score_topk_kernel(
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l32 = lane & 31, g = lane >> 5;
+  const int c8 = lane & 15, r0 = lane >> 4;
 
-  // qn of this wave's rows wave + 8 m (lane m), loaded ahead of the products
-  float qn_rows = 0.f;
-  if (lane < kFRows / kFWaves && it * kFRows + wave + kFWaves * lane < nb)
-    qn_rows = qnorm[(int64_t)bh * nb + it * kFRows + wave + kFWaves * lane];
+  // Query pooling (the same arithmetic as the K pooling): wave w pools the
+  // tile's query blocks kQB w + u.  The fp64 sums go to qhat for the
+  // rescoring paths; the hi/lo operand words and the norm are parked in the
+  // key area (not in use yet), block kQB w + u in key row w + kFWaves u (hi
+  // words of channels 8 c .. 8 c + 7 at word 4 c, lo words at 64 + 4 c, the
+  // norm at 128).  Blocks past nb pool to zero.
+  const uint16_t* qhead = q + (bh / cs.H) * qs.b + (bh % cs.H) * qs.h;
+  auto park = [&](const double (&acc)[8], int u) __attribute__((always_inline)) {
+    const int i = it * kFRows + kQB * wave + u;
+    if (i < nb && r0 == 0) {
+      double* o = qhat + ((int64_t)bh * nb + i) * kHeadDim + 8 * c8;
+#pragma unroll
+      for (int c = 0; c < 8; c += 2) *reinterpret_cast<f64x2*>(o + c) = (f64x2){acc[c], acc[c + 1]};
+    }
+    u32x4 whi, wlo;
+    double sq;
+    split_hi_lo(acc, whi, wlo, sq);
+    uint32_t* slot = keys + (wave + kFWaves * u) * NBP;
+    if (r0 == 0) {
+      *reinterpret_cast<u32x4*>(slot + 4 * c8) = whi;
+      *reinterpret_cast<u32x4*>(slot + 64 + 4 * c8) = wlo;
+    }
+    sq = row_sum16(sq);
+    const int n_i = min(cs.block, cs.N - i * cs.block);
+    if (lane == 0) slot[128] = __float_as_uint(n_i > 0 ? f32_round_up(sqrt(sq) / (double)n_i) : 0.f);
+  };
+  {  // BLOCK 64: two blocks' loads in flight together
+    constexpr int kPar = BLOCK == 64 ? 2 : 1;
+#pragma unroll
+    for (int u0 = 0; u0 < kQB; u0 += kPar) {
+      u32x4 w[kPar][BLOCK / 4];
+#pragma unroll
+      for (int p = 0; p < kPar; ++p)
+        pool_load<BLOCK>(qhead, qs.n, (it * kFRows + kQB * wave + u0 + p) * BLOCK, cs.N, w[p]);
+#pragma unroll
+      for (int p = 0; p < kPar; ++p) {
+        double acc[8];
+        pool_reduce<BLOCK>(w[p], (it * kFRows + kQB * wave + u0 + p) * BLOCK, cs.N, acc);
+        park(acc, u0 + p);
+      }
+    }
+  }
+
   // kn_max of the head (a non-finite norm makes it +inf)
   float m = 0.f;
   for (int j = threadIdx.x; j < nb; j += kFThreads) {
@@ -653,13 +726,28 @@ __global__ __launch_bounds__(kFThreads) void score_topk_kernel(
   }
   m = wave_max(m);
   if (lane == 0) wmax[wave] = m;
+  __syncthreads();
+  // qn of this wave's rows wave + 8 m (lane m): block rr parked in key row
+  // rr / kQB + kFWaves (rr % kQB)
+  float qn_rows = 0.f;
+  if (lane < kQB) {
+    const int rr = wave + kFWaves * lane;
+    qn_rows = __uint_as_float(keys[(rr / kQB + kFWaves * (rr % kQB)) * NBP + 128]);
+  }
 
   {  // approximate scores of the 32 query blocks against every key block
-    const u32x4* qsrc =
-        reinterpret_cast<const u32x4*>(qfrag) + ((int64_t)bh * ntiles + it) * kFSteps * kWave + lane;
+    // operand step st, lane l: channels 8 (2 (st % 8) + l / 32) .. +7 of
+    // query block l % 32, hi words for st < 8, lo words after
     bf16x8 qa[kFSteps];
+    {
+      const int rb = l32;
+      const uint32_t* src = keys + (rb / kQB + kFWaves * (rb % kQB)) * NBP + 4 * g;
 #pragma unroll
-    for (int st = 0; st < kFSteps; ++st) qa[st] = __builtin_bit_cast(bf16x8, qsrc[st * kWave]);
+      for (int st = 0; st < kFSteps; ++st)
+        qa[st] = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u32x4*>(src + (st < 8 ? 0 : 64) + 8 * (st & 7)));
+    }
+    __syncthreads();  // every wave holds its operands before the keys overwrite them
     const u32x4* ksrc =
         reinterpret_cast<const u32x4*>(kfrag) + (int64_t)bh * ntiles * kFSteps * kWave + lane;
     auto load = [&](bf16x8 (&kb)[kFSteps], int jt) {
@@ -736,7 +824,7 @@ __global__ __launch_bounds__(kFThreads) void score_topk_kernel(
   uint32_t* ckey = cand[wave][0];
   uint32_t* cidx = cand[wave][1];
 
-  for (int rm = 0; rm < kFRows / kFWaves; ++rm) {
+  for (int rm = 0; rm < kQB; ++rm) {
     const int rr = wave + kFWaves * rm;
     const int i = it * kFRows + rr;
     if (i >= nb) break;  // uniform
@@ -1133,16 +1221,19 @@ __global__ __launch_bounds__(kRowKThreads) void head_rowk_kernel(int nb, int kma
 
 }  // namespace
 
+// Pools Q and K (k_only: K alone).
 static void launch_pool(const Shape& s, const void* q, Strides qs, const void* k, Strides ks,
-                        double* qhat, double* khat, const PoolSplit& sp, hipStream_t stream) {
-  const dim3 grid((s.nb + kPoolWaves - 1) / kPoolWaves, (unsigned)(s.B * s.H), 2);
+                        double* qhat, double* khat, const PoolSplit& sp, bool k_only,
+                        hipStream_t stream) {
+  const dim3 grid((s.nb + kPoolWaves - 1) / kPoolWaves, (unsigned)(s.B * s.H), k_only ? 1 : 2);
+  const int z0 = k_only ? 1 : 0;
   const auto* qq = static_cast<const uint16_t*>(q);
   const auto* kk = static_cast<const uint16_t*>(k);
   if (s.block == 64)
-    pool_kernel<64><<<grid, kPoolWaves * kWave, 0, stream>>>(qq, kk, qs, ks, s.H, s.N, s.nb,
+    pool_kernel<64><<<grid, kPoolWaves * kWave, 0, stream>>>(qq, kk, qs, ks, s.H, s.N, s.nb, z0,
                                                              qhat, khat, sp);
   else
-    pool_kernel<128><<<grid, kPoolWaves * kWave, 0, stream>>>(qq, kk, qs, ks, s.H, s.N, s.nb,
+    pool_kernel<128><<<grid, kPoolWaves * kWave, 0, stream>>>(qq, kk, qs, ks, s.H, s.N, s.nb, z0,
                                                               qhat, khat, sp);
 }
 
@@ -1153,8 +1244,8 @@ size_t select_workspace_bytes(const Shape& s) {
   const size_t pooled = bh * s.nb * kHeadDim * sizeof(double) * 2;
   if (s.nb <= kFStrideBig) {
     const size_t ntiles = (s.nb + kFRows - 1) / kFRows;
-    return pooled + 2 * bh * ntiles * kFSteps * kWave * 8 * sizeof(uint16_t) +
-           2 * bh * s.nb * sizeof(float);
+    return pooled + bh * ntiles * kFSteps * kWave * 8 * sizeof(uint16_t) +
+           bh * s.nb * sizeof(float);
   }
   return pooled + bh * s.nb * s.nb * sizeof(double);
 }
@@ -1174,7 +1265,7 @@ static hipError_t launch_pool_score(const Shape& s, const void* q, Strides qs, c
   double* qhat = static_cast<double*>(ws);
   double* khat = qhat + bh * s.nb * kHeadDim;
   double* scores = khat + bh * s.nb * kHeadDim;
-  launch_pool(s, q, qs, k, ks, qhat, khat, PoolSplit{}, stream);
+  launch_pool(s, q, qs, k, ks, qhat, khat, PoolSplit{}, false, stream);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int tiles = (s.nb + kSTile - 1) / kSTile;
@@ -1190,27 +1281,30 @@ hipError_t launch_select_row(const Shape& s, const void* q, Strides qs, const vo
   if (s.nb <= kFStrideBig) {
     const size_t bh = (size_t)s.B * s.H;
     const int ntiles = (s.nb + kFRows - 1) / kFRows;
-    const size_t frag = bh * ntiles * kFSteps * kWave * 8;  // uint16 per operand
+    const size_t frag = bh * ntiles * kFSteps * kWave * 8;  // uint16
     double* qhat = static_cast<double*>(ws);
     double* khat = qhat + bh * s.nb * kHeadDim;
     PoolSplit sp;
-    sp.qfrag = reinterpret_cast<uint16_t*>(khat + bh * s.nb * kHeadDim);
-    sp.kfrag = sp.qfrag + frag;
-    sp.qnorm = reinterpret_cast<float*>(sp.kfrag + frag);
-    sp.knorm = sp.qnorm + bh * s.nb;
+    sp.frag = reinterpret_cast<uint16_t*>(khat + bh * s.nb * kHeadDim);
+    sp.norm = reinterpret_cast<float*>(sp.frag + frag);
     sp.ntiles = ntiles;
-    launch_pool(s, q, qs, k, ks, qhat, khat, sp, stream);
+    // K alone: every workgroup of the fused kernel pools its own query blocks
+    launch_pool(s, q, qs, k, ks, qhat, khat, sp, true, stream);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int per_xcd = (int)((bh * ntiles + 7) / 8);
-    if (s.nb <= kFStrideSmall)
-      score_topk_kernel<kFStrideSmall><<<8 * per_xcd, kFThreads, 0, stream>>>(
-          sp.qfrag, sp.kfrag, sp.qnorm, sp.knorm, qhat, khat, s, topk, kmax, ntiles, per_xcd,
-          idx, cnt);
-    else
-      score_topk_kernel<kFStrideBig><<<8 * per_xcd, kFThreads, 0, stream>>>(
-          sp.qfrag, sp.kfrag, sp.qnorm, sp.knorm, qhat, khat, s, topk, kmax, ntiles, per_xcd,
-          idx, cnt);
+    const auto* qq = static_cast<const uint16_t*>(q);
+#define SA_FUSED(NBP, BLOCK)                                                                   \
+  score_topk_kernel<NBP, BLOCK><<<8 * per_xcd, kFThreads, 0, stream>>>(                         \
+      qq, qs, sp.frag, sp.norm, qhat, khat, s, topk, kmax, ntiles, per_xcd, idx, cnt)
+    if (s.nb <= kFStrideSmall) {
+      if (s.block == 64) SA_FUSED(kFStrideSmall, 64);
+      else SA_FUSED(kFStrideSmall, 128);
+    } else {
+      if (s.block == 64) SA_FUSED(kFStrideBig, 64);
+      else SA_FUSED(kFStrideBig, 128);
+    }
+#undef SA_FUSED
     return hipGetLastError();
   }
   double* scores = nullptr;

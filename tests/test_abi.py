@@ -59,10 +59,11 @@ def test_workspace_size_formula():
     lib = sa.library()
     ds = desc(B=1, H=40, N=75600)
     nb = 1182
-    # row mode: pooled q/k (fp64), the bf16 hi/lo operands of the on-chip
-    # scores in tiles of 32 blocks (16 KB per tile and operand), fp32 norms
+    # row mode: pooled q/k (fp64), the bf16 hi/lo operand of the pooled keys
+    # for the on-chip scores in tiles of 32 blocks (16 KB per tile), fp32 key
+    # norms (the query side is pooled on chip)
     assert lib.sparse_attn_workspace_size(ctypes.byref(ds), 0, 36) == \
-        40 * nb * 128 * 8 * 2 + 2 * 40 * 37 * 16384 + 2 * 40 * nb * 4
+        40 * nb * 128 * 8 * 2 + 40 * 37 * 16384 + 40 * nb * 4
     # whole-head mode: pooled q/k, scores (fp64), then per head 32 B of radix
     # state and a 256-bin histogram, per row 3 int32
     assert lib.sparse_attn_workspace_size(ctypes.byref(ds), sa.SA_OP_SELECT_HEAD, 36) == \
@@ -73,7 +74,7 @@ def test_workspace_size_formula():
         2 * 1193 * 128 * 8 * 2 + 2 * 1193 * 1193 * 8
     edge = desc(B=1, H=2, N=1192 * 64)
     assert lib.sparse_attn_workspace_size(ctypes.byref(edge), 0, 36) == \
-        2 * 1192 * 128 * 8 * 2 + 2 * 2 * 38 * 16384 + 2 * 2 * 1192 * 4
+        2 * 1192 * 128 * 8 * 2 + 2 * 38 * 16384 + 2 * 1192 * 4
     # scheduler: 16 class counters per chunk of 1024 query tiles, plus one row
     assert lib.sparse_attn_workspace_size(ctypes.byref(ds), 1, 36) == (47 + 1) * 16 * 4
     assert lib.sparse_attn_workspace_size(ctypes.byref(ds), 1, 0) == 0
