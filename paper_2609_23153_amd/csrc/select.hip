@@ -925,6 +925,54 @@ __global__ __launch_bounds__(kFThreads) void score_topk_kernel(
         if (KLO > KHI && __popcll(m) == k) {
           if (sel) out[__popcll(m & below)] = cj;
           done = true;
+        } else if (KLO >= P) {
+          // Every key >= KLO is >= P, hence a candidate: the band is the
+          // candidates in [KLO, KHI].  Each band block is rescored in fp64 by
+          // the whole wave (lane l: channels 2 l, 2 l + 1), its 64-bit key
+          // kept by the candidate's lane; the k - (certain) best band lanes
+          // then join the certain ones, all in index order.
+          const bool band = cm && ck >= KLO && ck <= KHI;
+          const uint64_t bm = __ballot(band);
+          const int cin = __popcll(m), cband = __popcll(bm);
+          if (cin <= k && cin + cband >= k) {
+            const f64x2 qv = *reinterpret_cast<const f64x2*>(qrow + 2 * lane);
+            uint32_t bhi = 0u, blo = 0u;
+            uint64_t rest = bm;
+            while (rest != 0ull) {  // uniform; four blocks' loads in flight
+              int lm[4];
+              int last = 0;
+#pragma unroll
+              for (int u = 0; u < 4; ++u) {
+                if (rest != 0ull) {
+                  last = (int)__builtin_ctzll(rest);
+                  rest &= rest - 1ull;
+                }
+                lm[u] = last;
+              }
+              f64x2 kv[4];
+              int jm[4];
+#pragma unroll
+              for (int u = 0; u < 4; ++u) {
+                jm[u] = __builtin_amdgcn_readlane(cj, lm[u]);
+                kv[u] = *reinterpret_cast<const f64x2*>(khead + (int64_t)jm[u] * kHeadDim + 2 * lane);
+              }
+#pragma unroll
+              for (int u = 0; u < 4; ++u) {
+                const double d = wave_sum_f64(fma(qv[0], kv[u][0], qv[1] * kv[u][1]));
+                const int nj = min(cs.block, cs.N - jm[u] * cs.block);
+                const uint64_t k64 = order_key(d / (double)(ni * nj));
+                if (lane == lm[u]) {
+                  bhi = (uint32_t)(k64 >> 32);
+                  blo = (uint32_t)k64;
+                }
+              }
+            }
+            const bool sb = cin < k ? select_lanes(bhi, blo, band, k - cin) : false;
+            const bool keep = sel || sb;
+            const uint64_t km = __ballot(keep);
+            if (keep) out[__popcll(km & below)] = cj;
+            done = true;
+          }
         }
       }
       if (!done) {
