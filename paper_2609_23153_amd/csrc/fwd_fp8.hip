@@ -15,9 +15,10 @@
 // through LDS.  Per 64-key tile:
 //   S^T (64 keys x 64 queries) = K . Q^T    8 x v_mfma_scale_..._32x32x64 (scales sk, sq),
 //                                           one half of the queries at a time
-//   P = 2^(x - m) * 2^(8 - kLazy) rounded to e4m3 with v_cvt_pk_fp8_f32, the
-//       power of two built in integer arithmetic (one FMA and one conversion
-//       per score: exact at integer exponents, linear in between)
+//   P = 2^(x - m) * 2^(8 - kLazy) as e4m3 codes built directly: the code of
+//       2^y, linear in the mantissa between integer y, is 8 (y + 7), so each
+//       score costs one FMA and one v_cvt_pk_u8_f32 that rounds it to a byte
+//       and packs it (exact at integer exponents, linear in between)
 //   O^T (128 x 64)        += V^T . P^T        8 x v_mfma_scale_..._32x32x64 (scales sv, 2^(kLazy-8))
 //   row sums of P          += 1^T . P^T        2 more MFMAs against an all-ones channel
 // so the normaliser is the sum of exactly the rounded probabilities the PV
@@ -90,15 +91,6 @@ __device__ __forceinline__ int next_tile(list_ptr list, int n, int total, int sp
     }
   }
   return total;
-}
-
-// v_cvt_u32_f32: truncation to an unsigned integer with the hardware's
-// saturation (negative values and NaN give 0, values >= 2^32 give
-// 0xffffffff), written as asm because C++ leaves negative inputs undefined.
-__device__ __forceinline__ uint32_t cvt_u32_sat(float x) {
-  uint32_t u;
-  asm("v_cvt_u32_f32 %0, %1" : "=v"(u) : "v"(x));
-  return u;
 }
 
 // E8M0 code of a power-of-two fp32 scale (its biased exponent).
@@ -207,7 +199,7 @@ __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(1, 1))) v
   // instruction ever rescales the accumulators.  A shift beyond kMaxShift
   // (fp32 headroom) restarts the row from its first tile with the new max.
   float mref[2] = {-INFINITY, -INFINITY};
-  const float cexp = p.scale_log2 * 8388608.f;  // tau log2(e) 2^23
+  const float cexp8 = p.scale_log2 * 8.f;  // 8 tau log2(e)
   bool restart = false;
 
   // Keys outside the causal window or past N get a score of -inf; a tile
@@ -261,25 +253,26 @@ __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(1, 1))) v
     mref[qh] = far ? mx : ref;
     e = far ? 0 : e;
     bscale = kPScaleInvE8m0 + e;
-    // P * 2^6 = 2^y with y = tau*log2(e)*s - ref - e + 6, as the fp32 whose
-    // bit pattern is (y + 127) * 2^23 truncated to an integer: exact at
-    // integer y and linear in the mantissa between them (at most 6.2% above
-    // 2^y, the same relative excess for a given fractional part of y); the
-    // e4m3 rounding that follows keeps 3 mantissa bits anyway.  Negative
-    // patterns (y < -127, and masked scores) convert to 0, i.e. P = 0.
+    // P * 2^6 = 2^y with y = tau*log2(e)*s - ref - e + 6 <= kLazy + 6 = 8, as
+    // the e4m3 code 8 (y + 7) rounded to an integer: exponent field
+    // floor(y) + 7, mantissa the first 3 bits of the fraction, i.e. 2^y exact
+    // at integer y and linear in between (at most 6.2% above 2^y, the same
+    // relative excess for a given fraction), at most 120 (2^8; 127 would be
+    // NaN).  v_cvt_pk_u8_f32 rounds to nearest, ties to even, and clamps to
+    // [0, 255] (NaN to 0), measured by an in-bounds probe: y < -7 and masked scores
+    // (-inf) give code 0, P = 0; codes 1..7 (y in [-7, -6)) read as e4m3
+    // subnormals, at most 2^-15 of the tile's largest P.
     const float mloc = mref[qh] == -INFINITY ? 0.f : mref[qh] + (float)e;
-    const float kexp = (kLog2PScale + 127.f - mloc) * 8388608.f;  // (6 + 127 - m) 2^23
+    const float kexp8 = (kLog2PScale + 7.f - mloc) * 8.f;  // 8 (6 + 7 - m): the e4m3 bias
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
       for (int r = 0; r < 16; r += 4) {
-        float x[4];
+        uint32_t w = 0u;
 #pragma unroll
         for (int u = 0; u < 4; ++u)
-          x[u] = __uint_as_float(cvt_u32_sat(fmaf(s[rt][r + u], cexp, kexp)));
-        int w = __builtin_amdgcn_cvt_pk_fp8_f32(x[0], x[1], 0, false);
-        w = __builtin_amdgcn_cvt_pk_fp8_f32(x[2], x[3], w, true);
-        pk[4 * rt + r / 4] = w;
+          w = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(s[rt][r + u], cexp8, kexp8), u, w);
+        pk[4 * rt + r / 4] = (int)w;
       }
   };
 
