@@ -658,7 +658,7 @@ __global__ __launch_bounds__(kFThreads) void score_topk_kernel(
     Shape cs, int k_all, int kmax, int ntiles, int per_xcd, int32_t* __restrict__ idx,
     int32_t* __restrict__ cnt) {
   constexpr int KPL = (NBP + kWave - 1) / kWave;
-  static_assert(kFRows * NBP >= kFSteps * kWave * 4, "operand staging fits the key area");
+  static_assert(NBP % 4 == 0 && NBP >= 129, "a key row holds one parked query block, 16-byte aligned");
   __shared__ __align__(16) uint32_t keys[kFRows * NBP];
   __shared__ uint32_t cand[kFWaves][2][kWave];
   __shared__ float wmax[kFWaves];
