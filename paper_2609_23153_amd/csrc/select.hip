@@ -40,8 +40,14 @@ template <int N>
 __device__ __forceinline__ uint32_t row_ror(uint32_t x, uint32_t idle) {
   return (uint32_t)__builtin_amdgcn_update_dpp((int)idle, (int)x, 0x120 + N, 0xF, 0xF, false);
 }
-// Whole-wave max / min, the result in every lane: a butterfly over the 16
-// lanes of a row, then over rows through v_permlane16_swap / 32_swap.
+// Number of set bits of m below this lane (v_mbcnt).
+__device__ __forceinline__ int rank_below(uint64_t m) {
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                        __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+// Whole-wave max / min, the result in every lane (a wave-uniform value): a
+// butterfly over the 16 lanes of a row, then over rows through
+// v_permlane16_swap / 32_swap.
 __device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
   x = max(x, row_ror<8>(x, 0u));
   x = max(x, row_ror<4>(x, 0u));
@@ -50,7 +56,7 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
   const auto a = __builtin_amdgcn_permlane16_swap(x, x, false, false);
   x = max(a[0], a[1]);
   const auto b = __builtin_amdgcn_permlane32_swap(x, x, false, false);
-  return max(b[0], b[1]);
+  return __builtin_amdgcn_readfirstlane(max(b[0], b[1]));  // the same in every lane
 }
 __device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) {
   x = min(x, row_ror<8>(x, ~0u));
@@ -60,7 +66,7 @@ __device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) {
   const auto a = __builtin_amdgcn_permlane16_swap(x, x, false, false);
   x = min(a[0], a[1]);
   const auto b = __builtin_amdgcn_permlane32_swap(x, x, false, false);
-  return min(b[0], b[1]);
+  return __builtin_amdgcn_readfirstlane(min(b[0], b[1]));
 }
 // fp64 x of lane l plus x of lane l ^ 16 (XOR16) or l ^ 32.
 template <bool XOR16>
@@ -400,7 +406,6 @@ __device__ __forceinline__ void select_emit(const uint32_t (&hi)[KPL], const uin
     for (int t = 0; t < KPL; ++t) gt2 += __popcll(__ballot(grp[t] && lo[t] > tlo));
     need_eq = k - gt - gt2;
   }
-  const uint64_t below = lanes_below_mask();
   int taken = 0, eq_seen = 0;
 #pragma unroll
   for (int t = 0; t < KPL; ++t) {
@@ -410,13 +415,13 @@ __device__ __forceinline__ void select_emit(const uint32_t (&hi)[KPL], const uin
     } else {
       const bool eq = member[t] && hi[t] == thi && lo[t] == tlo;
       const uint64_t eq_mask = __ballot(eq);
-      const int eq_rank = eq_seen + __popcll(eq_mask & below);
+      const int eq_rank = eq_seen + rank_below(eq_mask);
       sel = (member[t] && (hi[t] > thi || (hi[t] == thi && lo[t] > tlo))) ||
             (eq && eq_rank < need_eq);
       eq_seen += __popcll(eq_mask);
     }
     const uint64_t sel_mask = __ballot(sel);
-    if (sel) out[taken + __popcll(sel_mask & below)] = jj[t];
+    if (sel) out[taken + rank_below(sel_mask)] = jj[t];
     taken += __popcll(sel_mask);
   }
 }
@@ -487,14 +492,13 @@ __global__ __launch_bounds__(256) void topk_row_kernel(const double* __restrict_
   }
   if (fast) {
     // compact the candidates in ascending index order, one per lane
-    const uint64_t below = lanes_below_mask();
-    int base = 0;
+      int base = 0;
 #pragma unroll
     for (int t = 0; t < KPL; ++t) {
       const bool ok = hi[t] >= P;
       const uint64_t m = __ballot(ok);
       if (ok) {
-        const int pos = base + __popcll(m & below);
+        const int pos = base + rank_below(m);
         cand[wv][0][pos] = hi[t];
         cand[wv][1][pos] = lo[t];
         cand[wv][2][pos] = (uint32_t)jj[t];
@@ -622,7 +626,7 @@ __device__ __forceinline__ bool select_lanes(uint32_t hi, uint32_t lo, bool memb
   const uint32_t tlo = kth_largest32<1>(l, grp, need - gt, &ex2);
   const int gt2 = __popcll(__ballot(grp[0] && lo > tlo));
   const bool eq = grp[0] && lo == tlo;
-  const int rank = __popcll(__ballot(eq) & lanes_below_mask());
+  const int rank = rank_below(__ballot(eq));
   return (member && (hi > thi || (hi == thi && lo > tlo))) || (eq && rank < need - gt - gt2);
 }
 
@@ -819,7 +823,6 @@ __global__ __launch_bounds__(kFThreads) void score_topk_kernel(
   float kn_max = wmax[0];
 #pragma unroll
   for (int w = 1; w < kFWaves; ++w) kn_max = fmaxf(kn_max, wmax[w]);
-  const uint64_t below = lanes_below_mask();
   const double* khead = khat + (int64_t)bh * nb * kHeadDim;
   uint32_t* ckey = cand[wave][0];
   uint32_t* cidx = cand[wave][1];
@@ -864,9 +867,15 @@ __global__ __launch_bounds__(kFThreads) void score_topk_kernel(
       uint32_t key[KPL];
       uint32_t mk = 0;  // 0: not a candidate (below every score's key)
 #pragma unroll
+      for (int t = 0; t < KPL; ++t)  // every read issued (clamped into the row)
+        key[t] = keys[rr * NBP + min(lane + kWave * t, NBP - 1)];
+#pragma unroll
       for (int t = 0; t < KPL; ++t) {
+        // opaque to the compiler, which would otherwise turn the select below
+        // into a branch around each read and wait on each one
+        asm volatile("" : "+v"(key[t]));
         const int j = lane + kWave * t;
-        key[t] = (j >= jlo && j < jhi) ? keys[rr * NBP + j] : 0u;
+        key[t] = (j >= jlo && j < jhi) ? key[t] : 0u;
         mk = max(mk, key[t]);
       }
       // As in the unfused kernel, the k-th largest lane maximum P bounds the
@@ -884,7 +893,7 @@ __global__ __launch_bounds__(kFThreads) void score_topk_kernel(
         for (int t = 0; t < KPL; ++t) {
           const bool ok = key[t] >= P;
           const uint64_t m = __ballot(ok);
-          const int pos = c + __popcll(m & below);
+          const int pos = c + rank_below(m);
           if (ok && pos < kWave) {
             ckey[pos] = key[t];
             cidx[pos] = (uint32_t)(lane + kWave * t);
@@ -923,7 +932,7 @@ __global__ __launch_bounds__(kFThreads) void score_topk_kernel(
         const bool sel = cm && ck > KHI;
         const uint64_t m = __ballot(sel);
         if (KLO > KHI && __popcll(m) == k) {
-          if (sel) out[__popcll(m & below)] = cj;
+          if (sel) out[rank_below(m)] = cj;
           done = true;
         } else if (KLO >= P) {
           // Every key >= KLO is >= P, hence a candidate: the band is the
@@ -970,7 +979,7 @@ __global__ __launch_bounds__(kFThreads) void score_topk_kernel(
             const bool sb = cin < k ? select_lanes(bhi, blo, band, k - cin) : false;
             const bool keep = sel || sb;
             const uint64_t km = __ballot(keep);
-            if (keep) out[__popcll(km & below)] = cj;
+            if (keep) out[rank_below(km)] = cj;
             done = true;
           }
         }
@@ -1008,7 +1017,7 @@ __global__ __launch_bounds__(kFThreads) void score_topk_kernel(
           for (int t = 0; t < KPL; ++t) {
             const bool b = key[t] != 0u && key[t] <= KHI && key[t] >= KLO;
             const uint64_t m = __ballot(b);
-            if (b) cidx[base + __popcll(m & below)] = (uint32_t)(lane + kWave * t);
+            if (b) cidx[base + rank_below(m)] = (uint32_t)(lane + kWave * t);
             base += __popcll(m);
           }
           __builtin_amdgcn_s_waitcnt(0xC07F);
@@ -1044,10 +1053,10 @@ __global__ __launch_bounds__(kFThreads) void score_topk_kernel(
           for (int t = 0; t < KPL; ++t) {
             const bool b = key[t] != 0u && key[t] <= KHI && key[t] >= KLO;
             const uint64_t bmask = __ballot(b);
-            const bool sel = key[t] > KHI || (b && ckey[base + __popcll(bmask & below)] != 0u);
+            const bool sel = key[t] > KHI || (b && ckey[base + rank_below(bmask)] != 0u);
             base += __popcll(bmask);
             const uint64_t m = __ballot(sel);
-            const int pos = taken + __popcll(m & below);
+            const int pos = taken + rank_below(m);
             if (sel && pos < k) out[pos] = lane + kWave * t;
             taken += __popcll(m);
           }
