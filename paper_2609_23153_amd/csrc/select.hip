@@ -685,6 +685,13 @@ __global__ __launch_bounds__(kFThreads) void score_topk_kernel(
   // key area (not in use yet), block kQB w + u in key row w + kFWaves u (hi
   // words of channels 8 c .. 8 c + 7 at word 4 c, lo words at 64 + 4 c, the
   // norm at 128).  Blocks past nb pool to zero.
+  // the head's key norms, read ahead of the pooling (a clamped index repeats
+  // a norm, which does not change their max)
+  constexpr int kKnLoads = (NBP + kFThreads - 1) / kFThreads;
+  float kv[kKnLoads];
+#pragma unroll
+  for (int u = 0; u < kKnLoads; ++u)
+    kv[u] = knorm[(int64_t)bh * nb + min((int)threadIdx.x + kFThreads * u, nb - 1)];
   const uint16_t* qhead = q + (bh / cs.H) * qs.b + (bh % cs.H) * qs.h;
   auto park = [&](const double (&acc)[8], int u) __attribute__((always_inline)) {
     const int i = it * kFRows + kQB * wave + u;
@@ -724,10 +731,9 @@ __global__ __launch_bounds__(kFThreads) void score_topk_kernel(
 
   // kn_max of the head (a non-finite norm makes it +inf)
   float m = 0.f;
-  for (int j = threadIdx.x; j < nb; j += kFThreads) {
-    const float v = knorm[(int64_t)bh * nb + j];
-    m = v <= 3.4028235e38f ? fmaxf(m, v) : __builtin_huge_valf();
-  }
+#pragma unroll
+  for (int u = 0; u < kKnLoads; ++u)
+    m = kv[u] <= 3.4028235e38f ? fmaxf(m, kv[u]) : __builtin_huge_valf();
   m = wave_max(m);
   if (lane == 0) wmax[wave] = m;
   __syncthreads();
