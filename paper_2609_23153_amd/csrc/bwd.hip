@@ -59,8 +59,15 @@ __device__ __forceinline__ int xcd_item(int slot, int G) {
   return (r / kRunB) * kGroup + (slot & 7) * kRunB + r % kRunB;
 }
 
-// 16-byte chunk c of tile row r sits at slot c ^ (r & 15).
-__device__ __forceinline__ int swz(int row, int c) { return c ^ (row & 15); }
+// 16-byte chunk c of tile row r sits at slot c ^ h(r), h(r) = 4 (r % 4) +
+// (r / 4) % 4: a permutation of r % 16, so the row reads (16 rows, one chunk
+// per pass of a 16-byte read) fall in 16 different bank groups, and the two
+// bits 4 (r % 4) differ across 4 consecutive rows, so the transposed reads
+// (4 rows x 4 consecutive chunks per half-wave) do too.  The plain r % 16
+// served the row reads only: the transposed reads met 4-way bank conflicts.
+__device__ __forceinline__ int swz(int row, int c) {
+  return c ^ (((row & 3) << 2) | ((row >> 2) & 3));
+}
 
 // Row fragment (A or B operand of a 32x32x16 product over the 128 channels):
 // tile row `row`, channels 16 ks + 8 g .. +7.
