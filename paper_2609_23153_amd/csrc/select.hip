@@ -666,7 +666,6 @@ __global__ __launch_bounds__(kFThreads) void score_topk_kernel(
   __shared__ __align__(16) uint32_t keys[kFRows * NBP];
   __shared__ uint32_t cand[kFWaves][2][kWave];
   __shared__ float wmax[kFWaves];
-  __shared__ float qn_lds[kFRows];
   const int nb = cs.nb;
   constexpr int kQB = kFRows / kFWaves;  // query blocks pooled per wave
   // Consecutive tiles (the same head's key blocks) run on one XCD: workgroup
@@ -679,19 +678,20 @@ __global__ __launch_bounds__(kFThreads) void score_topk_kernel(
   const int l32 = lane & 31, g = lane >> 5;
   const int c8 = lane & 15, r0 = lane >> 4;
 
+  // The head's key norms, read ahead of the pooling (a clamped index repeats
+  // a norm, which does not change their max).
+  constexpr int kKnLoads = (NBP + kFThreads - 1) / kFThreads;
+  float kv[kKnLoads];
+#pragma unroll
+  for (int u = 0; u < kKnLoads; ++u)
+    kv[u] = knorm[(int64_t)bh * nb + min((int)threadIdx.x + kFThreads * u, nb - 1)];
+
   // Query pooling (the same arithmetic as the K pooling): wave w pools the
   // tile's query blocks kQB w + u.  The fp64 sums go to qhat for the
   // rescoring paths; the hi/lo operand words and the norm are parked in the
   // key area (not in use yet), block kQB w + u in key row w + kFWaves u (hi
   // words of channels 8 c .. 8 c + 7 at word 4 c, lo words at 64 + 4 c, the
   // norm at 128).  Blocks past nb pool to zero.
-  // the head's key norms, read ahead of the pooling (a clamped index repeats
-  // a norm, which does not change their max)
-  constexpr int kKnLoads = (NBP + kFThreads - 1) / kFThreads;
-  float kv[kKnLoads];
-#pragma unroll
-  for (int u = 0; u < kKnLoads; ++u)
-    kv[u] = knorm[(int64_t)bh * nb + min((int)threadIdx.x + kFThreads * u, nb - 1)];
   const uint16_t* qhead = q + (bh / cs.H) * qs.b + (bh % cs.H) * qs.h;
   auto park = [&](const double (&acc)[8], int u) __attribute__((always_inline)) {
     const int i = it * kFRows + kQB * wave + u;
