@@ -153,6 +153,17 @@ def test_select_on_chip_capacity_edges(nb):
     select_and_check(q, k, 64, 300, f"nb={nb}")
 
 
+@pytest.mark.parametrize("N,block", [(4160, 128), (1000, 64)])
+def test_select_token_major_batched(N, block):
+    """Token-major [B, L, H, d] views with two batches: the fused kernel's
+    in-kernel query pooling and the key pooling address every (b, h) through
+    the strides; lists bit-exact, including the ragged last block."""
+    g = torch.Generator().manual_seed(7 * N + block)
+    base = [torch.randn(2, N, 3, 128, generator=g).to(torch.bfloat16) for _ in range(2)]
+    q, k = (t.permute(0, 2, 1, 3) for t in base)
+    select_and_check(q, k, block, 1000, f"token-major B=2 N={N} b={block}")
+
+
 def test_select_kmax_padding():
     g = torch.Generator().manual_seed(3)
     q = torch.randn(1, 1, 2048, 128, generator=g).to(torch.bfloat16)
