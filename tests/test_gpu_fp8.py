@@ -87,6 +87,17 @@ def test_quant_fp8_tiles_tails(N, block):
         quant_check(x, block, f"N={N} b={block} {name} tiles", operand=op)
 
 
+@pytest.mark.parametrize("N,block", [(1000, 64), (4160, 128)])
+def test_quant_fp8_token_major(N, block):
+    """Token-major [B, L, H, d] views (strides (L H d, d, H d)): all three
+    quantisation layouts bit-exact, the strides taken from the view."""
+    g = torch.Generator().manual_seed(3 * N + block)
+    x = (torch.randn(2, N, 3, 128, generator=g) * 2).to(torch.bfloat16).permute(0, 2, 1, 3)
+    quant_check(x, block, f"token-major N={N} b={block}")
+    for op, name in ((sa.SA_FP8_K, "K"), (sa.SA_FP8_V, "V")):
+        quant_check(x, block, f"token-major N={N} b={block} {name} tiles", operand=op)
+
+
 def test_quant_fp8_outlier_workload_heads():
     wl = W.WORKLOADS["wan14b_720p_fp8"]
     heads = sorted({h for h, _ in W._outlier_pairs(wl)[0]} | {0})[:3]
